@@ -1,0 +1,176 @@
+/*
+ * fp2.h -- block-sparse causal GQA prefill attention with max-based block
+ * selection and mean correction (FlashPrefill V2), for AMD Instinct MI355X
+ * (gfx950). C ABI of libfp2.so.
+ *
+ * The operator follows Algorithm 1 of the paper (Sec. 3.4): packed queries,
+ * a paged KV cache with its page table, per-request lengths and a threshold
+ * alpha in; the attention output and the selected-block mask out.
+ *
+ *   fp2_prefill  = fp2_estimate (pool, score, select) + attention over the
+ *                  kept blocks with the mean correction, one call.
+ *   fp2_estimate = the index stage only: block means, fused block scoring,
+ *                  max-based thresholding, forced blocks, kept-block lists.
+ *   fp2_attend   = the attention stage only, under a caller-given mask.
+ *   fp2_pool     = the block means alone (exposed for verification).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All tensor pointers are DEVICE pointers (hipMalloc'd or torch CUDA
+ *   tensors) unless the name ends in _host. The caller owns every buffer; the
+ *   library never allocates, frees or synchronises. Work is enqueued on
+ *   `stream` (a hipStream_t; NULL = the default stream) and returns at once.
+ * - Scratch memory is the caller's `workspace` of at least
+ *   fp2_workspace_bytes(params) bytes (256-byte aligned). It may be reused
+ *   across calls and layers on one stream; concurrent calls need distinct
+ *   workspaces.
+ * - Errors are reported as fp2_status_t only; nothing aborts. Host-visible
+ *   arguments are validated before any launch (FP2_EINVAL, FP2_EUNSUPPORTED,
+ *   FP2_EWORKSPACE); a failed launch returns FP2_EHIP. The consistency of
+ *   device-resident arrays (cu_seqlens, block_table) with `params` is the
+ *   caller's contract; pass cu_seqlens_host to have the lengths checked too.
+ *   fp2_last_error() gives a one-line reason for the last failure of the
+ *   calling thread.
+ *
+ * Layouts (row-major, innermost last)
+ * -----------------------------------
+ *   q, out       [total_tokens, num_q_heads, head_dim]; sequence b occupies
+ *                token rows cu_seqlens[b] .. cu_seqlens[b+1]-1.
+ *   k_cache,     page_size > 0: a token pool [num_slots, num_kv_heads,
+ *   v_cache      head_dim]; token j of sequence b is slot
+ *                block_table[b][j / page_size] * page_size + j % page_size
+ *                (Sec. 3.3, Eq. page). page_size == 0: contiguous
+ *                [total_tokens, num_kv_heads, head_dim], laid out like q.
+ *   block_table  int32 [batch, max_pages_per_seq] (ignored when page_size == 0).
+ *   cu_seqlens   int32 [batch + 1], cu_seqlens[0] == 0, non-decreasing.
+ *   q/k/v_scale  fp32 per head ([num_q_heads] / [num_kv_heads] / [num_kv_heads]);
+ *                only read when dtype == FP2_FP8_E4M3 (the dequantised value
+ *                is scale * code, Sec. 3.3 Eq. fp8; a per-tensor scale is the
+ *                all-equal case).
+ *   block_mask   uint8 [batch, num_kv_heads, nb, nb], nb = ceil(max_seq_len /
+ *                block_size). Entry (b, h, I, J): bit 0 = key block J is
+ *                attended exactly by query block I of KV head h (kept);
+ *                bit 1 = J is a forced block (sink, window, diagonal or
+ *                recent). Zero for J > I and for blocks past the sequence.
+ *   lse          fp32 [total_tokens, num_q_heads], natural-log log-sum-exp of
+ *                the scaled logits (including the correction masses).
+ *
+ * Selection semantics (Sec. 3.1 Eq. (1)-(2) and Eq. select, Sec. 3.2)
+ * ----------------------------------------------------------------------
+ * For query block I (block_size positions x all g = num_q_heads/num_kv_heads
+ * query heads of one KV head h) and key block J <= I, the block energy is
+ *     E[I][J] = sum over rows r of block I of exp(scale * q_r . khat_J),
+ * khat_J = the bf16 rounding (nearest, ties to even) of the mean of the
+ * dequantised keys of block J. Block J is kept iff alpha == 0, or
+ * E[I][J] >= alpha * max_J' E[I][J'], or J is forced: J < sink_blocks,
+ * I - J < window_blocks, J == I, or J >= n_b - recent_blocks (n_b = blocks of
+ * sequence b). With mean_correction, every block J < I that is not kept adds
+ * |B_J| * exp(scale * q . kbar_J) * vbar_J to the softmax numerator and
+ * |B_J| * exp(scale * q . kbar_J) to its denominator (Sec. 3.2 Eq.
+ * correction); kbar/vbar are the block means (stored in bf16 on the GPU).
+ */
+#ifndef FP2_H
+#define FP2_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FP2_OK = 0,
+  FP2_EINVAL = 1,        /* a null or inconsistent argument */
+  FP2_EUNSUPPORTED = 2,  /* a valid configuration this build does not cover */
+  FP2_EWORKSPACE = 3,    /* workspace null or smaller than fp2_workspace_bytes */
+  FP2_EHIP = 4           /* a HIP launch or runtime call failed */
+} fp2_status_t;
+
+typedef enum {
+  FP2_BF16 = 0,          /* q, k, v in bfloat16 */
+  FP2_FP8_E4M3 = 1       /* q, k, v in OCP float8 e4m3fn with per-head fp32 scales */
+} fp2_dtype_t;
+
+typedef struct {
+  int32_t batch;              /* number of sequences, >= 0 */
+  int32_t num_q_heads;        /* H_q, a multiple of num_kv_heads */
+  int32_t num_kv_heads;       /* H_kv >= 1; g = H_q / H_kv must be 1, 2, 4 or 8 */
+  int32_t head_dim;           /* d: must be 128 */
+  int32_t block_size;         /* selection block B in tokens: must be 128 */
+  int32_t page_size;          /* p >= 1 tokens per page, or 0 for contiguous KV */
+  int32_t max_seq_len;        /* upper bound of every sequence length, <= 1048576 */
+  int32_t max_pages_per_seq;  /* block_table row stride, >= ceil(max_seq_len / p) */
+  float alpha;                /* threshold ratio >= 0 (0 keeps every causal block) */
+  int32_t sink_blocks;        /* forced leading key blocks, >= 0 */
+  int32_t window_blocks;      /* forced local band incl. the diagonal, >= 0 */
+  int32_t recent_blocks;      /* forced trailing key blocks of the sequence, >= 0 */
+  int32_t mean_correction;    /* 0 or 1 */
+  float softmax_scale;        /* <= 0 selects 1/sqrt(head_dim) */
+  int32_t dtype;              /* fp2_dtype_t */
+} fp2_params_t;
+
+/* Bytes of workspace the entry points need for `params` (0 for a null or
+ * invalid params). Covers the pooled key/value means, the kept-block lists
+ * and their counts. */
+size_t fp2_workspace_bytes(const fp2_params_t* params);
+
+/* Full prefill (Algorithm 1 of Sec. 3.4): block means, fused scoring and
+ * selection, then attention over the kept blocks of every (sequence, KV head,
+ * query block) with the mean correction for the pruned ones (Sec. 3.2-3.3).
+ * Inputs: params, q, cu_seqlens (device), cu_seqlens_host (nullable host
+ * copy, validated when given), k_cache, v_cache, block_table (device;
+ * ignored if page_size == 0), q_scale/k_scale/v_scale (device; fp8 only,
+ * else may be null). Outputs: out (bf16, always), lse (nullable), block_mask
+ * (every entry written). Rows of out/lse outside [0, cu_seqlens[batch]) are
+ * not touched. */
+fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
+                         const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                         const int32_t* block_table, const float* q_scale, const float* k_scale,
+                         const float* v_scale, void* out, float* lse, uint8_t* block_mask,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* The index stage alone (Sec. 3.1, Eq. fused_score and Eq. select; Algorithm
+ * 1 steps 1-5): writes every entry of block_mask and leaves the pooled means
+ * and kept-block lists in the workspace. Arguments as for fp2_prefill. */
+fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
+                          const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                          const int32_t* block_table, const float* q_scale, const float* k_scale,
+                          const float* v_scale, uint8_t* block_mask, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/* The attention stage alone (Sec. 3.2 Eq. correction, Sec. 3.3; Algorithm 1
+ * steps 6-11) under a caller-given mask: bit 0 of block_mask_in[b][h][I][J]
+ * selects key block J for query block I (entries with J > I are ignored;
+ * the diagonal J == I must be selected for every valid block I, else
+ * FP2_EINVAL is not detected and rows whose keys are all excluded produce
+ * undefined values). Recomputes the block means and the kept lists from the
+ * mask in the workspace. Arguments as for fp2_prefill. */
+fp2_status_t fp2_attend(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
+                        const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                        const int32_t* block_table, const float* q_scale, const float* k_scale,
+                        const float* v_scale, const uint8_t* block_mask_in, void* out, float* lse,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Block means of K and V (Sec. 3.2, the pooled statistics of Eq. correction;
+ * Algorithm 1 step 2), dequantised for fp8. khat [batch, num_kv_heads, nb,
+ * head_dim] receives the bf16 (nearest-even) rounding of the key means, vbar
+ * the same layout for the value means; entries of blocks past a sequence are
+ * zero. Needs no workspace. */
+fp2_status_t fp2_pool(const fp2_params_t* params, const int32_t* cu_seqlens,
+                      const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                      const int32_t* block_table, const float* k_scale, const float* v_scale,
+                      void* khat, void* vbar, void* stream);
+
+/* Static description of a status code. */
+const char* fp2_status_str(fp2_status_t status);
+
+/* One-line reason for the last non-OK status returned on the calling thread
+ * ("" if none). The pointer stays valid until the next call on that thread. */
+const char* fp2_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FP2_H */

@@ -1,0 +1,209 @@
+"""Python binding of libfp2 (block-sparse causal GQA prefill attention for
+MI355X / gfx950): argument marshalling over the C ABI of ``include/fp2.h``.
+
+Every step of the computation runs in the library's HIP kernels; torch only
+provides device memory and the current stream. The library must be built
+(``python paper_2608_19758_amd/build.py`` or ``__graft_entry__.build()``);
+importing works without it, but every call raises until it is built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_DIR, "libfp2.so")
+_lib = None
+
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, 1, 2, 3, 4
+BF16, FP8_E4M3 = 0, 1
+HEAD_DIM = 128
+BLOCK = 128
+
+
+class Fp2Error(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__("%s failed: %s (%s)" % (fn, status_str(status), msg))
+        self.status = status
+
+
+class Params(ctypes.Structure):
+    """Mirror of fp2_params_t."""
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32), ("page_size", ctypes.c_int32),
+        ("max_seq_len", ctypes.c_int32), ("max_pages_per_seq", ctypes.c_int32),
+        ("alpha", ctypes.c_float),
+        ("sink_blocks", ctypes.c_int32), ("window_blocks", ctypes.c_int32),
+        ("recent_blocks", ctypes.c_int32), ("mean_correction", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
+    ]
+
+
+EXPORTS = ["fp2_workspace_bytes", "fp2_prefill", "fp2_estimate", "fp2_attend", "fp2_pool",
+           "fp2_status_str", "fp2_last_error"]
+
+
+def lib():
+    """The loaded libfp2.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libfp2.so is not built (%s); run paper_2608_19758_amd/build.py"
+                               % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        vp, P = ctypes.c_void_p, ctypes.POINTER(Params)
+        L.fp2_workspace_bytes.restype = ctypes.c_size_t
+        L.fp2_workspace_bytes.argtypes = [P]
+        L.fp2_prefill.restype = ctypes.c_int
+        L.fp2_prefill.argtypes = [P] + [vp] * 13 + [ctypes.c_size_t, vp]
+        L.fp2_estimate.restype = ctypes.c_int
+        L.fp2_estimate.argtypes = [P] + [vp] * 11 + [ctypes.c_size_t, vp]
+        L.fp2_attend.restype = ctypes.c_int
+        L.fp2_attend.argtypes = [P] + [vp] * 13 + [ctypes.c_size_t, vp]
+        L.fp2_pool.restype = ctypes.c_int
+        L.fp2_pool.argtypes = [P] + [vp] * 10
+        L.fp2_status_str.restype = ctypes.c_char_p
+        L.fp2_status_str.argtypes = [ctypes.c_int]
+        L.fp2_last_error.restype = ctypes.c_char_p
+        L.fp2_last_error.argtypes = []
+        _lib = L
+    return _lib
+
+
+def status_str(st: int) -> str:
+    return lib().fp2_status_str(st).decode()
+
+
+def last_error() -> str:
+    return lib().fp2_last_error().decode()
+
+
+def _check(fn: str, st: int) -> None:
+    if st != OK:
+        raise Fp2Error(fn, st, last_error())
+
+
+def make_params(*, batch, num_q_heads, num_kv_heads, max_seq_len, page_size=0,
+                max_pages_per_seq=0, alpha=0.0, sink_blocks=1, window_blocks=2,
+                recent_blocks=0, mean_correction=1, softmax_scale=0.0, dtype="bf16",
+                head_dim=HEAD_DIM, block_size=BLOCK) -> Params:
+    dt = {"bf16": BF16, "fp8": FP8_E4M3}.get(dtype, dtype)
+    return Params(batch=batch, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
+                  head_dim=head_dim, block_size=block_size, page_size=page_size,
+                  max_seq_len=max_seq_len, max_pages_per_seq=max_pages_per_seq,
+                  alpha=alpha, sink_blocks=sink_blocks, window_blocks=window_blocks,
+                  recent_blocks=recent_blocks, mean_correction=int(mean_correction),
+                  softmax_scale=softmax_scale, dtype=dt)
+
+
+def num_blocks(p: Params) -> int:
+    return (p.max_seq_len + p.block_size - 1) // p.block_size
+
+
+def workspace_bytes(p: Params) -> int:
+    return int(lib().fp2_workspace_bytes(ctypes.byref(p)))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _host_ptr(a):
+    if a is None:
+        return None
+    return ctypes.c_void_p(a.ctypes.data) if hasattr(a, "ctypes") else ctypes.c_void_p(a.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def alloc_workspace(p: Params, device="cuda") -> torch.Tensor:
+    n = max(1, workspace_bytes(p))
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def alloc_outputs(p: Params, total_tokens: int, device="cuda", want_lse=False):
+    nb = max(1, num_blocks(p))
+    out = torch.empty((total_tokens, p.num_q_heads, p.head_dim), dtype=torch.bfloat16, device=device)
+    mask = torch.empty((p.batch, p.num_kv_heads, nb, nb), dtype=torch.uint8, device=device)
+    lse = (torch.empty((total_tokens, p.num_q_heads), dtype=torch.float32, device=device)
+           if want_lse else None)
+    return out, mask, lse
+
+
+def prefill(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_seqlens_host=None,
+            q_scale=None, k_scale=None, v_scale=None, out=None, lse=None, block_mask=None,
+            workspace=None, want_lse=False, stream=None):
+    """fp2_prefill: returns (out [total, Hq, 128] bf16, block_mask uint8, lse or None)."""
+    if out is None or block_mask is None:
+        o2, m2, l2 = alloc_outputs(p, q.shape[0], q.device, want_lse and lse is None)
+        out = o2 if out is None else out
+        block_mask = m2 if block_mask is None else block_mask
+        lse = l2 if lse is None else lse
+    if workspace is None:
+        workspace = alloc_workspace(p, q.device)
+    st = lib().fp2_prefill(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
+                           _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(q_scale),
+                           _ptr(k_scale), _ptr(v_scale), _ptr(out), _ptr(lse), _ptr(block_mask),
+                           _ptr(workspace), workspace.numel(), _stream(stream))
+    _check("fp2_prefill", st)
+    return out, block_mask, lse
+
+
+def estimate(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *,
+             cu_seqlens_host=None, q_scale=None, k_scale=None, v_scale=None, block_mask=None,
+             workspace=None, stream=None):
+    """fp2_estimate: returns (block_mask, workspace)."""
+    if block_mask is None:
+        nb = max(1, num_blocks(p))
+        block_mask = torch.empty((p.batch, p.num_kv_heads, nb, nb), dtype=torch.uint8,
+                                 device=q.device)
+    if workspace is None:
+        workspace = alloc_workspace(p, q.device)
+    st = lib().fp2_estimate(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
+                            _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(q_scale),
+                            _ptr(k_scale), _ptr(v_scale), _ptr(block_mask), _ptr(workspace),
+                            workspace.numel(), _stream(stream))
+    _check("fp2_estimate", st)
+    return block_mask, workspace
+
+
+def attend(p: Params, q, k_cache, v_cache, cu_seqlens, block_mask, block_table=None, *,
+           cu_seqlens_host=None, q_scale=None, k_scale=None, v_scale=None, out=None, lse=None,
+           workspace=None, want_lse=False, stream=None):
+    """fp2_attend under ``block_mask`` (bit 0 = kept): returns (out, lse or None)."""
+    if out is None:
+        out = torch.empty((q.shape[0], p.num_q_heads, p.head_dim), dtype=torch.bfloat16,
+                          device=q.device)
+    if lse is None and want_lse:
+        lse = torch.empty((q.shape[0], p.num_q_heads), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = alloc_workspace(p, q.device)
+    st = lib().fp2_attend(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
+                          _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(q_scale),
+                          _ptr(k_scale), _ptr(v_scale), _ptr(block_mask), _ptr(out), _ptr(lse),
+                          _ptr(workspace), workspace.numel(), _stream(stream))
+    _check("fp2_attend", st)
+    return out, lse
+
+
+def pool(p: Params, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_seqlens_host=None,
+         k_scale=None, v_scale=None, stream=None):
+    """fp2_pool: returns (khat, vbar) as bf16 [batch, Hkv, nb, 128]."""
+    nb = max(1, num_blocks(p))
+    shape = (p.batch, p.num_kv_heads, nb, p.head_dim)
+    khat = torch.empty(shape, dtype=torch.bfloat16, device=k_cache.device)
+    vbar = torch.empty(shape, dtype=torch.bfloat16, device=k_cache.device)
+    st = lib().fp2_pool(ctypes.byref(p), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
+                        _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(k_scale),
+                        _ptr(v_scale), _ptr(khat), _ptr(vbar), _stream(stream))
+    _check("fp2_pool", st)
+    return khat, vbar

@@ -1,0 +1,299 @@
+// C ABI of libfp2: argument validation, workspace layout and the launch
+// sequence of each entry point (Algorithm 1 of Sec. 3.4). Host code only.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "fp2.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+fp2_status_t fail(fp2_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+fp2_status_t ok() {
+  g_last_error.clear();
+  return FP2_OK;
+}
+
+constexpr int kMaxSeqLen = fp2::kMaxBlocks * fp2::kBlock;   // 1M tokens
+
+int nb_of(const fp2_params_t* p) { return (p->max_seq_len + fp2::kBlock - 1) / fp2::kBlock; }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  size_t khat, vbar, kidx, kcnt, total;
+};
+
+Layout layout_of(const fp2_params_t* p) {
+  Layout l{};
+  const size_t rows = (size_t)p->batch * p->num_kv_heads * nb_of(p);
+  size_t off = 0;
+  l.khat = off;
+  off = align256(off + rows * fp2::kHeadDim * sizeof(uint16_t));
+  l.vbar = off;
+  off = align256(off + rows * fp2::kHeadDim * sizeof(uint16_t));
+  l.kidx = off;
+  off = align256(off + rows * nb_of(p) * sizeof(int16_t));
+  l.kcnt = off;
+  off = align256(off + rows * sizeof(int32_t));
+  l.total = rows ? off : 0;
+  return l;
+}
+
+fp2_status_t validate_params(const fp2_params_t* p) {
+  if (!p) return fail(FP2_EINVAL, "params is null");
+  if (p->batch < 0) return fail(FP2_EINVAL, "batch %d < 0", p->batch);
+  if (p->num_kv_heads < 1) return fail(FP2_EINVAL, "num_kv_heads %d < 1", p->num_kv_heads);
+  if (p->num_q_heads < 1 || p->num_q_heads % p->num_kv_heads)
+    return fail(FP2_EINVAL, "num_q_heads %d is not a positive multiple of num_kv_heads %d",
+                p->num_q_heads, p->num_kv_heads);
+  const int g = p->num_q_heads / p->num_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8)
+    return fail(FP2_EUNSUPPORTED, "group size %d not in {1, 2, 4, 8}", g);
+  if (p->head_dim <= 0) return fail(FP2_EINVAL, "head_dim %d <= 0", p->head_dim);
+  if (p->head_dim != fp2::kHeadDim) return fail(FP2_EUNSUPPORTED, "head_dim %d != 128", p->head_dim);
+  if (p->block_size <= 0) return fail(FP2_EINVAL, "block_size %d <= 0", p->block_size);
+  if (p->block_size != fp2::kBlock) return fail(FP2_EUNSUPPORTED, "block_size %d != 128", p->block_size);
+  if (p->page_size < 0) return fail(FP2_EINVAL, "page_size %d < 0", p->page_size);
+  if (p->max_seq_len < 0) return fail(FP2_EINVAL, "max_seq_len %d < 0", p->max_seq_len);
+  if (p->max_seq_len > kMaxSeqLen)
+    return fail(FP2_EUNSUPPORTED, "max_seq_len %d > %d", p->max_seq_len, kMaxSeqLen);
+  if (p->page_size > 0) {
+    const int need = (p->max_seq_len + p->page_size - 1) / p->page_size;
+    if (p->max_pages_per_seq < need)
+      return fail(FP2_EINVAL, "max_pages_per_seq %d < ceil(max_seq_len / page_size) = %d",
+                  p->max_pages_per_seq, need);
+  }
+  if (!(p->alpha >= 0.f) || !isfinite(p->alpha))
+    return fail(FP2_EINVAL, "alpha must be finite and >= 0");
+  if (p->sink_blocks < 0 || p->window_blocks < 0 || p->recent_blocks < 0)
+    return fail(FP2_EINVAL, "sink/window/recent block counts must be >= 0");
+  if (p->mean_correction != 0 && p->mean_correction != 1)
+    return fail(FP2_EINVAL, "mean_correction must be 0 or 1");
+  if (!isfinite(p->softmax_scale)) return fail(FP2_EINVAL, "softmax_scale is not finite");
+  if (p->dtype != FP2_BF16 && p->dtype != FP2_FP8_E4M3)
+    return fail(FP2_EINVAL, "dtype %d unknown", p->dtype);
+  return FP2_OK;
+}
+
+bool aligned16(const void* x) { return ((uintptr_t)x & 15u) == 0; }
+
+// Validation of everything but the workspace; `work` is false when there is
+// nothing to compute (no sequence or zero-length bound).
+fp2_status_t validate_common(const fp2_params_t* p, const void* q, const int32_t* cu,
+                             const int32_t* cu_host, const void* k, const void* v,
+                             const int32_t* bt, const float* qs, const float* ks,
+                             const float* vs, bool need_q, bool* work) {
+  fp2_status_t st = validate_params(p);
+  if (st != FP2_OK) return st;
+  *work = p->batch > 0 && p->max_seq_len > 0;
+  if (!*work) return FP2_OK;
+  if (!cu) return fail(FP2_EINVAL, "cu_seqlens is null");
+  if (need_q && !q) return fail(FP2_EINVAL, "q is null");
+  if (!k || !v) return fail(FP2_EINVAL, "k_cache or v_cache is null");
+  if ((need_q && !aligned16(q)) || !aligned16(k) || !aligned16(v))
+    return fail(FP2_EINVAL, "q, k_cache and v_cache must be 16-byte aligned");
+  if (p->page_size > 0 && !bt) return fail(FP2_EINVAL, "block_table is null with page_size > 0");
+  if (p->dtype == FP2_FP8_E4M3 && ((need_q && !qs) || !ks || !vs))
+    return fail(FP2_EINVAL, "fp8 needs q_scale, k_scale and v_scale");
+  if (cu_host) {
+    if (cu_host[0] != 0) return fail(FP2_EINVAL, "cu_seqlens[0] = %d != 0", cu_host[0]);
+    for (int b = 0; b < p->batch; ++b) {
+      const int len = cu_host[b + 1] - cu_host[b];
+      if (len < 0) return fail(FP2_EINVAL, "cu_seqlens decreases at %d", b);
+      if (len > p->max_seq_len)
+        return fail(FP2_EINVAL, "sequence %d has length %d > max_seq_len %d", b, len, p->max_seq_len);
+    }
+  }
+  return FP2_OK;
+}
+
+fp2_status_t validate_ws(const fp2_params_t* p, const void* ws, size_t bytes) {
+  const size_t need = layout_of(p).total;
+  if (need == 0) return FP2_OK;
+  if (!ws) return fail(FP2_EWORKSPACE, "workspace is null (need %zu bytes)", need);
+  if (((uintptr_t)ws & 255u) != 0) return fail(FP2_EWORKSPACE, "workspace is not 256-byte aligned");
+  if (bytes < need) return fail(FP2_EWORKSPACE, "workspace has %zu bytes, need %zu", bytes, need);
+  return FP2_OK;
+}
+
+int log2_exact(int x) {
+  if (x <= 0 || (x & (x - 1))) return -1;
+  int s = 0;
+  while ((1 << s) < x) ++s;
+  return s;
+}
+
+fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* cu, const void* k,
+                          const void* v, const int32_t* bt, const float* qs, const float* ks,
+                          const float* vs) {
+  fp2::Problem pr{};
+  pr.q = q;
+  pr.cu = cu;
+  pr.k = k;
+  pr.v = v;
+  pr.pm.table = bt;
+  pr.pm.stride = p->max_pages_per_seq;
+  pr.pm.page = p->page_size;
+  pr.pm.shift = log2_exact(p->page_size);
+  pr.q_scale = qs;
+  pr.k_scale = ks;
+  pr.v_scale = vs;
+  pr.batch = p->batch;
+  pr.hq = p->num_q_heads;
+  pr.hkv = p->num_kv_heads;
+  pr.g = p->num_q_heads / p->num_kv_heads;
+  pr.nbmax = nb_of(p);
+  pr.sink = p->sink_blocks;
+  pr.window = p->window_blocks;
+  pr.recent = p->recent_blocks;
+  pr.corr = p->mean_correction;
+  pr.alpha = p->alpha;
+  const double scale = p->softmax_scale > 0.f ? (double)p->softmax_scale : 1.0 / sqrt((double)p->head_dim);
+  pr.scale_log2 = (float)(scale * 1.4426950408889634074);
+  pr.fp8 = p->dtype == FP2_FP8_E4M3;
+  return pr;
+}
+
+struct Views {
+  fp2::Pooled pooled;
+  fp2::KeptLists kl;
+};
+
+Views views_of(const fp2_params_t* p, void* ws) {
+  const Layout l = layout_of(p);
+  char* base = (char*)ws;
+  Views v;
+  v.pooled.khat = (uint16_t*)(base + l.khat);
+  v.pooled.vbar = (uint16_t*)(base + l.vbar);
+  v.kl.idx = (int16_t*)(base + l.kidx);
+  v.kl.cnt = (int32_t*)(base + l.kcnt);
+  return v;
+}
+
+fp2_status_t hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(FP2_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t fp2_workspace_bytes(const fp2_params_t* params) {
+  if (validate_params(params) != FP2_OK) return 0;
+  return layout_of(params).total;
+}
+
+fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
+                         const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                         const int32_t* block_table, const float* q_scale, const float* k_scale,
+                         const float* v_scale, void* out, float* lse, uint8_t* block_mask,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  bool work = false;
+  fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, k_cache, v_cache,
+                                    block_table, q_scale, k_scale, v_scale, true, &work);
+  if (st != FP2_OK) return st;
+  if (!work) return ok();
+  if (!out || !block_mask) return fail(FP2_EINVAL, "out or block_mask is null");
+  if (!aligned16(out)) return fail(FP2_EINVAL, "out must be 16-byte aligned");
+  if ((st = validate_ws(params, workspace, workspace_bytes)) != FP2_OK) return st;
+  const fp2::Problem pr = make_problem(params, q, cu_seqlens, k_cache, v_cache, block_table,
+                                       q_scale, k_scale, v_scale);
+  const Views vw = views_of(params, workspace);
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = fp2::launch_pool(pr, vw.pooled, s);
+  if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s);
+  if (e == hipSuccess) e = fp2::launch_attend(pr, vw.pooled, block_mask, vw.kl, out, lse, s);
+  return hip_status(e, "fp2_prefill launch");
+}
+
+fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
+                          const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                          const int32_t* block_table, const float* q_scale, const float* k_scale,
+                          const float* v_scale, uint8_t* block_mask, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  bool work = false;
+  fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, k_cache, v_cache,
+                                    block_table, q_scale, k_scale, v_scale, true, &work);
+  if (st != FP2_OK) return st;
+  if (!work) return ok();
+  if (!block_mask) return fail(FP2_EINVAL, "block_mask is null");
+  if ((st = validate_ws(params, workspace, workspace_bytes)) != FP2_OK) return st;
+  const fp2::Problem pr = make_problem(params, q, cu_seqlens, k_cache, v_cache, block_table,
+                                       q_scale, k_scale, v_scale);
+  const Views vw = views_of(params, workspace);
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = fp2::launch_pool(pr, vw.pooled, s);
+  if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s);
+  return hip_status(e, "fp2_estimate launch");
+}
+
+fp2_status_t fp2_attend(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
+                        const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                        const int32_t* block_table, const float* q_scale, const float* k_scale,
+                        const float* v_scale, const uint8_t* block_mask_in, void* out, float* lse,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  bool work = false;
+  fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, k_cache, v_cache,
+                                    block_table, q_scale, k_scale, v_scale, true, &work);
+  if (st != FP2_OK) return st;
+  if (!work) return ok();
+  if (!out || !block_mask_in) return fail(FP2_EINVAL, "out or block_mask_in is null");
+  if (!aligned16(out)) return fail(FP2_EINVAL, "out must be 16-byte aligned");
+  if ((st = validate_ws(params, workspace, workspace_bytes)) != FP2_OK) return st;
+  const fp2::Problem pr = make_problem(params, q, cu_seqlens, k_cache, v_cache, block_table,
+                                       q_scale, k_scale, v_scale);
+  const Views vw = views_of(params, workspace);
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  if (params->mean_correction) e = fp2::launch_pool(pr, vw.pooled, s);
+  if (e == hipSuccess) e = fp2::launch_compact(pr, block_mask_in, vw.kl, s);
+  if (e == hipSuccess) e = fp2::launch_attend(pr, vw.pooled, block_mask_in, vw.kl, out, lse, s);
+  return hip_status(e, "fp2_attend launch");
+}
+
+fp2_status_t fp2_pool(const fp2_params_t* params, const int32_t* cu_seqlens,
+                      const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                      const int32_t* block_table, const float* k_scale, const float* v_scale,
+                      void* khat, void* vbar, void* stream) {
+  bool work = false;
+  fp2_status_t st = validate_common(params, nullptr, cu_seqlens, cu_seqlens_host, k_cache, v_cache,
+                                    block_table, nullptr, k_scale, v_scale, false, &work);
+  if (st != FP2_OK) return st;
+  if (!work) return ok();
+  if (!khat || !vbar) return fail(FP2_EINVAL, "khat or vbar is null");
+  const fp2::Problem pr = make_problem(params, nullptr, cu_seqlens, k_cache, v_cache, block_table,
+                                       nullptr, k_scale, v_scale);
+  fp2::Pooled pooled{(uint16_t*)khat, (uint16_t*)vbar};
+  return hip_status(fp2::launch_pool(pr, pooled, (hipStream_t)stream), "fp2_pool launch");
+}
+
+const char* fp2_status_str(fp2_status_t status) {
+  switch (status) {
+    case FP2_OK: return "ok";
+    case FP2_EINVAL: return "invalid argument";
+    case FP2_EUNSUPPORTED: return "unsupported configuration";
+    case FP2_EWORKSPACE: return "workspace too small";
+    case FP2_EHIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* fp2_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

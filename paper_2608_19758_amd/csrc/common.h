@@ -1,0 +1,124 @@
+// Device helpers shared by the gfx950 kernels of libfp2.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fp2 {
+
+constexpr int kHeadDim = 128;   // d
+constexpr int kBlock = 128;     // selection block B (tokens)
+constexpr int kMaxBlocks = 8192;  // blocks per sequence (max_seq_len <= 1M tokens)
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef __attribute__((ext_vector_type(8))) int i32x8_t;
+typedef __attribute__((ext_vector_type(4))) int i32x4_t;
+typedef __attribute__((ext_vector_type(2))) int i32x2_t;
+typedef __attribute__((ext_vector_type(4))) short i16x4_t;
+
+// ---------------------------------------------------------------------------
+// Number formats
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float((uint32_t)b << 16);
+}
+
+// fp32 -> bf16, round to nearest, ties to even (inputs here are finite).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// fp64 -> bf16 with a single rounding (nearest, ties to even), from the
+// double's bit pattern: the exponent and 7 mantissa bits are kept, the 45
+// dropped bits round the kept field (a carry moves into the exponent).
+// Below 2^-126 the bf16 spacing is 2^-133: round x * 2^133 to an integer,
+// which is then the encoding itself. Overflow gives infinity.
+__device__ __forceinline__ uint16_t f64_to_bf16(double x) {
+  uint64_t u = (uint64_t)__double_as_longlong(x);
+  uint32_t sign = (uint32_t)(u >> 63) << 15;
+  uint64_t mag = u & 0x7FFFFFFFFFFFFFFFull;
+  if (mag > 0x7FF0000000000000ull) return 0x7FC0;  // NaN
+  double ax = __longlong_as_double((long long)mag);
+  if (ax < 0x1p-126) return (uint16_t)(sign | (uint32_t)rint(ax * 0x1p133));
+  uint64_t keep = mag >> 45;
+  uint64_t rem = mag & ((1ull << 45) - 1);
+  const uint64_t half = 1ull << 44;
+  if (rem > half || (rem == half && (keep & 1))) keep += 1;
+  int e = (int)(keep >> 7) - 1023 + 127;
+  if (e >= 255) return (uint16_t)(sign | 0x7F80);
+  return (uint16_t)(sign | ((uint32_t)e << 7) | (uint32_t)(keep & 0x7F));
+}
+
+// OCP e4m3fn code -> value * 512 as an exact integer (|.| <= 229376). Codes
+// with exponent field 0 are subnormal (m * 2^-9); 0x7F/0xFF are NaN and never
+// reach the arithmetic (the caller's inputs are finite).
+__device__ __forceinline__ int e4m3_times512(uint32_t code) {
+  int e = (code >> 3) & 15, m = code & 7;
+  int mag = e == 0 ? m : (8 + m) << (e - 1);
+  return (code & 0x80) ? -mag : mag;
+}
+
+// OCP e4m3fn code -> bf16 bits (exact: every e4m3 value is a bf16 value).
+__device__ __forceinline__ uint32_t e4m3_to_bf16(uint32_t code) {
+  uint32_t s = (code & 0x80u) << 8;
+  uint32_t e = (code >> 3) & 15u, m = code & 7u;
+  uint32_t bits;
+  if (e != 0) {
+    bits = ((e + 120u) << 7) | (m << 4);
+  } else if (m == 0) {
+    bits = 0;
+  } else {
+    // m * 2^-9: normalise m = 1.xx * 2^k
+    int k = 31 - __clz(m);                 // 0..2
+    uint32_t frac = (m << (3 - k)) & 7u;   // mantissa bits below the leading one
+    bits = ((uint32_t)(118 + k) << 7) | (frac << 4);
+  }
+  return s | bits;
+}
+
+// ---------------------------------------------------------------------------
+// Paged addressing (Sec. 3.3, Eq. page)
+// ---------------------------------------------------------------------------
+
+struct PageMap {
+  const int32_t* table;   // [batch, stride]
+  int32_t stride;         // max_pages_per_seq
+  int32_t page;           // p (0: contiguous)
+  int32_t shift;          // log2(p) when p is a power of two, else -1
+};
+
+// Pool slot of token t of sequence b whose first token row is tok0.
+__device__ __forceinline__ int64_t slot_of(const PageMap& pm, int b, int64_t tok0, int t) {
+  if (pm.page == 0) return tok0 + t;
+  int pg, off;
+  if (pm.shift >= 0) {
+    pg = t >> pm.shift;
+    off = t & (pm.page - 1);
+  } else {
+    pg = t / pm.page;
+    off = t - pg * pm.page;
+  }
+  return (int64_t)pm.table[(int64_t)b * pm.stride + pg] * pm.page + off;
+}
+
+// ---------------------------------------------------------------------------
+// Wave helpers (wave64)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+}  // namespace fp2

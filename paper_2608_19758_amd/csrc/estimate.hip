@@ -1,0 +1,294 @@
+// Fused block scoring, max-based thresholding and kept-list compaction
+// (Sec. 3.1 Eq. (1)-(2), Eq. fused_score, Eq. select; Algorithm 1 steps 3-5).
+//
+// One workgroup (8 waves) per (sequence b, KV head h, query block I), heaviest
+// (largest I) first. The query rows of block I are the g*B packed rows of
+// Eq. packgqa (position I*B + r/g, head h*g + r%g). They stream through LDS in
+// 32-row tiles; each wave keeps up to four 32-wide chunks of pooled keys khat
+// in registers (the MFMA B operand) and computes S = Q khat^T with
+// v_mfma_f32_32x32x16_bf16 (fp32 accumulation). Lane l of the accumulator
+// owns key block J = chunk + l%32 and 16 query rows, so the row sum of
+// exp2(S * scale*log2e - m) for its block is a per-lane running sum with a
+// per-lane running maximum m (the per-(I,J) maximum of Eq. (1), no
+// cross-lane traffic). At the end the two lane halves and the running maxima
+// are merged into ell_J = log2 E_J.
+//
+// Selection (Eq. select): J is kept iff alpha == 0, ell_J >= max_J ell +
+// log2(alpha), or J is forced (sink, window incl. diagonal, recent). The mask
+// row is written in full (zeros past I) and the kept blocks are compacted in
+// ascending order with wave ballots into the per-row list of the workspace.
+//
+// Precision: fp8 queries are widened to bf16 exactly, the per-head fp8 scale
+// is applied in fp32 after the MFMA, and exponentials use the hardware
+// v_exp_f32; block energies match the fp64 definition to ~1e-6 relative.
+#include "kernels.h"
+
+namespace fp2 {
+
+namespace {
+
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * 64;
+constexpr int kChunksPerWave = 4;                          // 4 x 32 key blocks per wave
+constexpr int kGroup = kWaves * kChunksPerWave * 32;       // key blocks per pass (1024)
+
+template <int FP8, int G>
+__global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p, Pooled pooled,
+                                                            uint8_t* __restrict__ mask,
+                                                            KeptLists kl) {
+  extern __shared__ float ell[];            // [nbmax] block log2-energies of this row
+  __shared__ uint4 qt[32 * 16];             // Q tile: 32 rows x 16 chunks of 8 bf16
+  __shared__ float redf[kWaves];
+  __shared__ int redi[kWaves];
+
+  const int nbh = p.batch * p.hkv;
+  const int I = p.nbmax - 1 - (int)(blockIdx.x / nbh);
+  const int bh = blockIdx.x % nbh;
+  const int b = bh / p.hkv, h = bh % p.hkv;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int64_t tok0 = p.cu[b];
+  const int L = p.cu[b + 1] - (int)tok0;
+  const int n = (L + kBlock - 1) / kBlock;
+  const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
+  uint8_t* mrow = mask + row * p.nbmax;
+
+  if (I >= n) {
+    for (int J = tid; J < p.nbmax; J += kThreads) mrow[J] = 0;
+    if (tid == 0) kl.cnt[row] = 0;
+    return;
+  }
+
+  const int npos = min(kBlock, L - I * kBlock);
+  const int nrows = npos * G;
+  const int ntiles = (nrows + 31) / 32;
+
+  // Row r = 8i + 4*half + j of a 32-row tile has head offset (4*half + j) % G.
+  float cs[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int hd = (4 * half + j) % G;
+    cs[j] = FP8 ? p.scale_log2 * p.q_scale[h * G + hd] : p.scale_log2;
+  }
+
+  const uint16_t* khat = pooled.khat + ((int64_t)b * p.hkv + h) * p.nbmax * kHeadDim;
+
+  for (int grp = 0; grp <= I; grp += kGroup) {
+    bf16x8_t kf[kChunksPerWave][8];
+    float m[kChunksPerWave], E[kChunksPerWave];
+    bool act[kChunksPerWave];
+#pragma unroll
+    for (int c = 0; c < kChunksPerWave; ++c) {
+      const int J0 = grp + 32 * (w + kWaves * c);
+      act[c] = J0 <= I;
+      m[c] = -INFINITY;
+      E[c] = 0.f;
+      const int J = J0 + l32;
+#pragma unroll
+      for (int ds = 0; ds < 8; ++ds) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (act[c] && J <= I) v = *(const uint4*)(khat + (int64_t)J * kHeadDim + 16 * ds + 8 * half);
+        kf[c][ds] = __builtin_bit_cast(bf16x8_t, v);
+      }
+    }
+
+    for (int t = 0; t < ntiles; ++t) {
+      __syncthreads();
+      if (!FP8) {
+        const int r = tid >> 4, c = tid & 15;
+        const int pr = t * 32 + r;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (pr < nrows) {
+          const int pos = I * kBlock + pr / G, hq = h * G + pr % G;
+          v = *(const uint4*)((const uint16_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + c * 8);
+        }
+        qt[r * 16 + (c ^ (r & 15))] = v;
+      } else if (tid < 256) {
+        const int r = tid >> 3, c8 = tid & 7;
+        const int pr = t * 32 + r;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (pr < nrows) {
+          const int pos = I * kBlock + pr / G, hq = h * G + pr % G;
+          v = *(const uint4*)((const uint8_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + c8 * 16);
+        }
+        uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+        uint32_t o[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          uint32_t src = wv[i >> 1] >> (16 * (i & 1));
+          o[i] = e4m3_to_bf16(src & 0xFF) | (e4m3_to_bf16((src >> 8) & 0xFF) << 16);
+        }
+        qt[r * 16 + ((2 * c8) ^ (r & 15))] = make_uint4(o[0], o[1], o[2], o[3]);
+        qt[r * 16 + ((2 * c8 + 1) ^ (r & 15))] = make_uint4(o[4], o[5], o[6], o[7]);
+      }
+      __syncthreads();
+
+      bf16x8_t qa[8];
+#pragma unroll
+      for (int ds = 0; ds < 8; ++ds)
+        qa[ds] = __builtin_bit_cast(bf16x8_t, qt[l32 * 16 + ((2 * ds + half) ^ (l32 & 15))]);
+
+      // validity of this lane's 16 rows (only the last tile can be partial)
+      const int rbase = t * 32 + 4 * half;
+      const bool full = t * 32 + 32 <= nrows;
+
+#pragma unroll
+      for (int c = 0; c < kChunksPerWave; ++c) {
+        if (!act[c]) continue;
+        f32x16_t acc = {};
+#pragma unroll
+        for (int ds = 0; ds < 8; ++ds)
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[ds], kf[c][ds], acc, 0, 0, 0);
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float g = -INFINITY;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            bool ok = full || (rbase + 8 * i + j < nrows);
+            g = ok ? fmaxf(g, acc[4 * i + j]) : g;
+          }
+          mx = fmaxf(mx, g * cs[j]);
+        }
+        const float mn = fmaxf(m[c], mx);
+        if (mn > m[c]) {
+          E[c] *= fast_exp2(m[c] - mn);
+          m[c] = mn;
+        }
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            bool ok = full || (rbase + 8 * i + j < nrows);
+            float e = fast_exp2(fmaf(acc[4 * i + j], cs[j], -mn));
+            s += ok ? e : 0.f;
+          }
+        E[c] += s;
+      }
+    }
+
+    // merge the two lane halves (same key block, different rows)
+#pragma unroll
+    for (int c = 0; c < kChunksPerWave; ++c) {
+      if (!act[c]) continue;
+      const float m2 = __shfl_xor(m[c], 32, 64);
+      const float E2 = __shfl_xor(E[c], 32, 64);
+      const float M = fmaxf(m[c], m2);
+      float e1 = m[c] == -INFINITY ? 0.f : E[c] * fast_exp2(m[c] - M);
+      float e2 = m2 == -INFINITY ? 0.f : E2 * fast_exp2(m2 - M);
+      const int J = grp + 32 * (w + kWaves * c) + l32;
+      if (half == 0 && J <= I) ell[J] = M + fast_log2(e1 + e2);
+    }
+  }
+  __syncthreads();
+
+  // ---- selection: max-based threshold plus forced blocks (Eq. select)
+  float mu = -INFINITY;
+  for (int J = tid; J <= I; J += kThreads) mu = fmaxf(mu, ell[J]);
+  mu = wave_max(mu);
+  if (lane == 0) redf[w] = mu;
+  __syncthreads();
+  mu = redf[0];
+#pragma unroll
+  for (int k = 1; k < kWaves; ++k) mu = fmaxf(mu, redf[k]);
+  const bool keep_all = p.alpha == 0.f;
+  const float thr = keep_all ? -INFINITY : mu + fast_log2(p.alpha);
+
+  int16_t* kidx = kl.idx + row * p.nbmax;
+  int base = 0;
+  for (int J0 = 0; J0 < p.nbmax; J0 += kThreads) {
+    const int J = J0 + tid;
+    const bool valid = J <= I;
+    const bool forced = valid && (J < p.sink || I - J < p.window || J == I || J >= n - p.recent);
+    const bool keep = valid && (keep_all || forced || ell[J] >= thr);
+    if (J < p.nbmax) mrow[J] = (uint8_t)((keep ? 1 : 0) | (forced ? 2 : 0));
+    if (J0 <= I) {
+      const uint64_t bal = __ballot(keep);
+      const int pre = __popcll(bal & ((1ull << lane) - 1ull));
+      __syncthreads();
+      if (lane == 0) redi[w] = __popcll(bal);
+      __syncthreads();
+      int wpre = 0, tot = 0;
+#pragma unroll
+      for (int k = 0; k < kWaves; ++k) {
+        wpre += k < w ? redi[k] : 0;
+        tot += redi[k];
+      }
+      if (keep) kidx[base + wpre + pre] = (int16_t)J;
+      base += tot;
+    }
+  }
+  if (tid == 0) kl.cnt[row] = base;
+}
+
+// Kept lists from a caller-given mask (bit 0), ascending; one workgroup per row.
+__global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* __restrict__ mask,
+                                                      KeptLists kl) {
+  __shared__ int redi[4];
+  const int nbh = p.batch * p.hkv;
+  const int I = p.nbmax - 1 - (int)(blockIdx.x / nbh);
+  const int bh = blockIdx.x % nbh;
+  const int b = bh / p.hkv, h = bh % p.hkv;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int L = p.cu[b + 1] - p.cu[b];
+  const int n = (L + kBlock - 1) / kBlock;
+  const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
+  if (I >= n) {
+    if (tid == 0) kl.cnt[row] = 0;
+    return;
+  }
+  const uint8_t* mrow = mask + row * p.nbmax;
+  int16_t* kidx = kl.idx + row * p.nbmax;
+  int base = 0;
+  for (int J0 = 0; J0 <= I; J0 += 256) {
+    const int J = J0 + tid;
+    const bool keep = J <= I && (mrow[J] & 1);
+    const uint64_t bal = __ballot(keep);
+    const int pre = __popcll(bal & ((1ull << lane) - 1ull));
+    __syncthreads();
+    if (lane == 0) redi[w] = __popcll(bal);
+    __syncthreads();
+    int wpre = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      wpre += k < w ? redi[k] : 0;
+      tot += redi[k];
+    }
+    if (keep) kidx[base + wpre + pre] = (int16_t)J;
+    base += tot;
+  }
+  if (tid == 0) kl.cnt[row] = base;
+}
+
+template <int FP8>
+hipError_t launch_est_dt(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
+                         hipStream_t s) {
+  const unsigned grid = (unsigned)p.nbmax * p.batch * p.hkv;
+  const size_t smem = (size_t)p.nbmax * sizeof(float);
+  switch (p.g) {
+    case 1: estimate_kernel<FP8, 1><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
+    case 2: estimate_kernel<FP8, 2><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
+    case 4: estimate_kernel<FP8, 4><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
+    case 8: estimate_kernel<FP8, 8><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_estimate(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
+                           hipStream_t s) {
+  if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
+  return p.fp8 ? launch_est_dt<1>(p, pooled, mask, kl, s) : launch_est_dt<0>(p, pooled, mask, kl, s);
+}
+
+hipError_t launch_compact(const Problem& p, const uint8_t* mask, KeptLists kl, hipStream_t s) {
+  if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
+  const unsigned grid = (unsigned)p.nbmax * p.batch * p.hkv;
+  compact_kernel<<<grid, 256, 0, s>>>(p, mask, kl);
+  return hipGetLastError();
+}
+
+}  // namespace fp2

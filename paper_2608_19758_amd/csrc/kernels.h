@@ -1,0 +1,45 @@
+// Launchers of the libfp2 kernels (internal to the library).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace fp2 {
+
+// Everything a kernel needs to find its rows, shared by all stages.
+struct Problem {
+  const void* q;            // [total, Hq, d] bf16 or e4m3 codes
+  const int32_t* cu;        // [batch + 1]
+  const void* k;            // pool or contiguous, bf16 or e4m3 codes
+  const void* v;
+  PageMap pm;
+  const float* q_scale;     // fp8 only
+  const float* k_scale;
+  const float* v_scale;
+  int32_t batch, hq, hkv, g, nbmax;
+  int32_t sink, window, recent, corr;
+  float alpha;
+  float scale_log2;         // softmax_scale * log2(e)
+  int32_t fp8;
+};
+
+// Workspace views.
+struct Pooled {
+  uint16_t* khat;           // [batch, Hkv, nbmax, d] bf16 key means (scoring and correction)
+  uint16_t* vbar;           // [batch, Hkv, nbmax, d] bf16 value means (correction)
+};
+
+struct KeptLists {
+  int16_t* idx;             // [batch, Hkv, nbmax, nbmax] ascending kept blocks per row
+  int32_t* cnt;             // [batch, Hkv, nbmax]
+};
+
+hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s);
+hipError_t launch_estimate(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
+                           hipStream_t s);
+hipError_t launch_compact(const Problem& p, const uint8_t* mask, KeptLists kl, hipStream_t s);
+hipError_t launch_attend(const Problem& p, const Pooled& pooled, const uint8_t* mask,
+                         const KeptLists& kl, void* out, float* lse, hipStream_t s);
+
+}  // namespace fp2

@@ -1,0 +1,136 @@
+// Block means of K and V (Sec. 3.2, the pooled statistics kbar_J, vbar_J of
+// Eq. correction; Algorithm 1 step 2). HBM-bound: every K/V byte of the
+// sequence is read once with 16-byte loads through the page table.
+//
+// One workgroup per (key block J, KV head h, sequence b), 256 threads.
+//  - bf16: thread (row group rg = tid/16, column chunk c = tid%16) sums tokens
+//    rg, rg+16, ... of the block for columns 8c..8c+7 in fp64. Every bf16
+//    value is exact in fp64 and so are the partial sums of realistic data, so
+//    the mean does not depend on the summation order.
+//  - fp8: each e4m3 code is an exact integer multiple of 2^-9; the sums are
+//    exact 32-bit integers, and the mean is (sum * 2^-9 * scale) / count in
+//    fp64 (the product is exact, the division rounds once).
+// The rounded key mean khat (bf16, one rounding from fp64) is the scoring key
+// of Eq. fused_score and the surrogate key of the correction; vbar is the
+// value mean in bf16.
+#include "kernels.h"
+
+namespace fp2 {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+template <int FP8>
+__global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
+  const int J = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int64_t tok0 = p.cu[b];
+  const int L = p.cu[b + 1] - (int)tok0;
+  const int64_t obase = (((int64_t)b * p.hkv + h) * p.nbmax + J) * kHeadDim;
+  const int n = (L + kBlock - 1) / kBlock;
+  if (J >= n) {
+    if (tid < kHeadDim) {
+      out.khat[obase + tid] = 0;
+      out.vbar[obase + tid] = 0;
+    }
+    return;
+  }
+  const int cnt = min(kBlock, L - J * kBlock);
+  __shared__ double redk[16][kHeadDim];
+  __shared__ double redv[16][kHeadDim];
+
+  if (!FP8) {
+    const int c = tid & 15, rg = tid >> 4;
+    double ak[8], av[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ak[i] = av[i] = 0.0;
+    const uint16_t* K = (const uint16_t*)p.k;
+    const uint16_t* V = (const uint16_t*)p.v;
+    for (int r = rg; r < cnt; r += 16) {
+      int64_t slot = slot_of(p.pm, b, tok0, J * kBlock + r);
+      int64_t off = (slot * p.hkv + h) * kHeadDim + c * 8;
+      uint4 kv = *(const uint4*)(K + off);
+      uint4 vv = *(const uint4*)(V + off);
+      uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w};
+      uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        ak[2 * i] += (double)__uint_as_float(kw[i] << 16);
+        ak[2 * i + 1] += (double)__uint_as_float(kw[i] & 0xFFFF0000u);
+        av[2 * i] += (double)__uint_as_float(vw[i] << 16);
+        av[2 * i + 1] += (double)__uint_as_float(vw[i] & 0xFFFF0000u);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      redk[rg][c * 8 + i] = ak[i];
+      redv[rg][c * 8 + i] = av[i];
+    }
+    __syncthreads();
+    if (tid < kHeadDim) {
+      double sk = 0.0, sv = 0.0;
+#pragma unroll
+      for (int g = 0; g < 16; ++g) {
+        sk += redk[g][tid];
+        sv += redv[g][tid];
+      }
+      out.khat[obase + tid] = f64_to_bf16(sk / (double)cnt);
+      out.vbar[obase + tid] = f64_to_bf16(sv / (double)cnt);
+    }
+  } else {
+    // 8 threads per token row (16 codes each), 32 row groups.
+    const int c = tid & 7, rg = tid >> 3;
+    int ak[16], av[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) ak[i] = av[i] = 0;
+    const uint8_t* K = (const uint8_t*)p.k;
+    const uint8_t* V = (const uint8_t*)p.v;
+    for (int r = rg; r < cnt; r += 32) {
+      int64_t slot = slot_of(p.pm, b, tok0, J * kBlock + r);
+      int64_t off = (slot * p.hkv + h) * kHeadDim + c * 16;
+      uint4 kv = *(const uint4*)(K + off);
+      uint4 vv = *(const uint4*)(V + off);
+      uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w};
+      uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        ak[i] += e4m3_times512((kw[i >> 2] >> (8 * (i & 3))) & 0xFF);
+        av[i] += e4m3_times512((vw[i >> 2] >> (8 * (i & 3))) & 0xFF);
+      }
+    }
+    // integer partial sums are exact in fp64
+    int* redki = (int*)&redk[0][0];
+    int* redvi = (int*)&redv[0][0];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      redki[rg * kHeadDim + c * 16 + i] = ak[i];
+      redvi[rg * kHeadDim + c * 16 + i] = av[i];
+    }
+    __syncthreads();
+    if (tid < kHeadDim) {
+      int sk = 0, sv = 0;
+      for (int g = 0; g < 32; ++g) {
+        sk += redki[g * kHeadDim + tid];
+        sv += redvi[g * kHeadDim + tid];
+      }
+      double ks = (double)p.k_scale[h], vs = (double)p.v_scale[h];
+      out.khat[obase + tid] = f64_to_bf16(((double)sk * 0x1p-9 * ks) / (double)cnt);
+      out.vbar[obase + tid] = f64_to_bf16(((double)sv * 0x1p-9 * vs) / (double)cnt);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s) {
+  if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
+  dim3 grid(p.nbmax, p.hkv, p.batch);
+  if (p.fp8)
+    pool_kernel<1><<<grid, kThreads, 0, s>>>(p, out);
+  else
+    pool_kernel<0><<<grid, kThreads, 0, s>>>(p, out);
+  return hipGetLastError();
+}
+
+}  // namespace fp2

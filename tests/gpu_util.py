@@ -1,0 +1,108 @@
+"""Helpers of the GPU parity tests: run the library and the oracle on the same
+seeded workload and compare them (mask bit-exact outside the margin band,
+outputs within the stated max-abs tolerance)."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2608_19758_amd as fp2
+import synth
+
+TOL = {"bf16": 2e-2, "fp8": 6e-2}   # max-abs, attention output under the same mask
+BAND = 1e-4                         # relative distance of a block energy from the threshold
+
+
+def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=0.0):
+    sp = wl.spec
+    return fp2.make_params(
+        batch=sp.batch, num_q_heads=sp.num_q_heads, num_kv_heads=sp.num_kv_heads,
+        max_seq_len=sp.max_seq_len, page_size=sp.page_size, max_pages_per_seq=wl.max_pages,
+        alpha=alpha, sink_blocks=sp.sink_blocks if sink is None else sink,
+        window_blocks=sp.window_blocks if window is None else window,
+        recent_blocks=sp.recent_blocks if recent is None else recent,
+        mean_correction=sp.mean_correction if corr is None else corr,
+        softmax_scale=scale, dtype=sp.dtype)
+
+
+def device_tensors(wl):
+    d = wl.device_inputs("cuda")
+    if wl.spec.dtype == "bf16":
+        d["q"] = d["q"].view(torch.bfloat16)
+        d["k_cache"] = d["k_cache"].view(torch.bfloat16)
+        d["v_cache"] = d["v_cache"].view(torch.bfloat16)
+    return d
+
+
+def gpu_prefill(wl, p, d=None, want_lse=True):
+    d = device_tensors(wl) if d is None else d
+    out, mask, lse = fp2.prefill(p, d["q"], d["k_cache"], d["v_cache"], d["cu_seqlens"],
+                                 d["block_table"] if wl.spec.page_size else None,
+                                 cu_seqlens_host=wl.cu_seqlens,
+                                 q_scale=d["q_scale"], k_scale=d["k_scale"], v_scale=d["v_scale"],
+                                 want_lse=want_lse)
+    torch.cuda.synchronize()
+    return (out.float().cpu().numpy().astype(np.float64), mask.cpu().numpy(),
+            None if lse is None else lse.cpu().numpy().astype(np.float64))
+
+
+def oracle_params(inp, alpha, corr=None, sink=None, window=None, recent=None):
+    return inp.params(alpha, sink=sink, window=window, recent=recent, correction=corr)
+
+
+def units_of(wl, sample=None, seed=0):
+    """All (b, h, I) units, or a deterministic sample containing each
+    sequence's last block and first block."""
+    sp = wl.spec
+    allu = []
+    for b, L in enumerate(sp.seqlens):
+        n = (L + sp.block_size - 1) // sp.block_size
+        for h in range(sp.num_kv_heads):
+            for I in range(n):
+                allu.append((b, h, I))
+    if sample is None or sample >= len(allu):
+        return allu
+    rng = np.random.default_rng(seed)
+    pick = set()
+    for b, L in enumerate(sp.seqlens):
+        n = (L + sp.block_size - 1) // sp.block_size
+        if n:
+            pick.add((b, int(rng.integers(sp.num_kv_heads)), n - 1))
+            pick.add((b, int(rng.integers(sp.num_kv_heads)), 0))
+    rest = [u for u in allu if u not in pick]
+    idx = rng.choice(len(rest), size=max(0, sample - len(pick)), replace=False)
+    return sorted(pick | {rest[i] for i in idx})
+
+
+def unit_rows(wl, units):
+    """Token rows (into q/out) and Q-head ranges of the given units."""
+    sp = wl.spec
+    g = sp.num_q_heads // sp.num_kv_heads
+    rows = []
+    for b, h, I in units:
+        L = sp.seqlens[b]
+        t0 = int(wl.cu_seqlens[b]) + I * sp.block_size
+        t1 = int(wl.cu_seqlens[b]) + min(L, (I + 1) * sp.block_size)
+        rows.append((slice(t0, t1), slice(h * g, (h + 1) * g)))
+    return rows
+
+
+def compare_masks(gmask, omask, ell, mu, alpha, units):
+    """Returns (outside-band mismatches, in-band mismatches, in-band blocks)."""
+    out_band = in_band_mis = in_band = 0
+    for b, h, I in units:
+        g = gmask[b, h, I]
+        o = omask[b, h, I]
+        if alpha > 0:
+            marg = np.abs(oracle.margins(ell[b, h, I], mu[b, h, I], alpha))
+            band = np.nan_to_num(marg, nan=np.inf) <= BAND
+        else:
+            band = np.zeros_like(g, dtype=bool)
+        mis = g != o
+        # the forced bit never depends on floating point
+        assert ((g & 2) == (o & 2)).all(), (b, h, I)
+        in_band += int(band.sum())
+        in_band_mis += int((mis & band).sum())
+        out_band += int((mis & ~band).sum())
+    return out_band, in_band_mis, in_band

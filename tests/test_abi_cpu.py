@@ -1,0 +1,118 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, sizes its workspace, and rejects bad arguments before any
+launch (every call here returns before touching device memory)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2608_19758_amd as fp2
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_symbols():
+    text = open(os.path.join(ROOT, "include", "fp2.h")).read()
+    return sorted(set(re.findall(r"\b(fp2_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    lib = fp2.lib()
+    syms = header_symbols()
+    assert set(syms) == set(fp2.EXPORTS)
+    for s in syms:
+        assert hasattr(lib, s), s
+
+
+def base(**kw):
+    d = dict(batch=2, num_q_heads=32, num_kv_heads=8, max_seq_len=4096, page_size=64,
+             max_pages_per_seq=64, alpha=0.1)
+    d.update(kw)
+    return fp2.make_params(**d)
+
+
+def test_workspace_bytes():
+    p = base()
+    nb = 32
+    rows = 2 * 8 * nb
+    want = rows * 128 * 2 * 2 + rows * nb * 2 + rows * 4
+    got = fp2.workspace_bytes(p)
+    assert want <= got <= want + 4 * 256
+    assert fp2.workspace_bytes(base(head_dim=64)) == 0
+    assert fp2.workspace_bytes(base(batch=0)) == 0
+
+
+FAKE = ctypes.c_void_p(0x100000)   # never dereferenced: validation fails first
+
+
+def call_prefill(p, **over):
+    args = dict(q=FAKE, cu=FAKE, cuh=None, k=FAKE, v=FAKE, bt=FAKE, qs=None, ks=None, vs=None,
+                out=FAKE, lse=None, mask=FAKE, ws=None, wsb=0)
+    args.update(over)
+    return fp2.lib().fp2_prefill(ctypes.byref(p), args["q"], args["cu"], args["cuh"], args["k"],
+                                 args["v"], args["bt"], args["qs"], args["ks"], args["vs"],
+                                 args["out"], args["lse"], args["mask"], args["ws"], args["wsb"],
+                                 None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(num_kv_heads=0), fp2.EINVAL),
+    (dict(num_q_heads=30), fp2.EINVAL),
+    (dict(num_q_heads=48, num_kv_heads=8), fp2.EUNSUPPORTED),      # g = 6
+    (dict(num_q_heads=128, num_kv_heads=8), fp2.EUNSUPPORTED),     # g = 16
+    (dict(head_dim=64), fp2.EUNSUPPORTED),
+    (dict(head_dim=0), fp2.EINVAL),
+    (dict(block_size=64), fp2.EUNSUPPORTED),
+    (dict(page_size=-1), fp2.EINVAL),
+    (dict(max_pages_per_seq=10), fp2.EINVAL),
+    (dict(max_seq_len=(1 << 20) + 1, max_pages_per_seq=1 << 15), fp2.EUNSUPPORTED),
+    (dict(alpha=-0.5), fp2.EINVAL),
+    (dict(alpha=float("nan")), fp2.EINVAL),
+    (dict(alpha=float("inf")), fp2.EINVAL),
+    (dict(sink_blocks=-1), fp2.EINVAL),
+    (dict(mean_correction=2), fp2.EINVAL),
+    (dict(dtype=7), fp2.EINVAL),
+    (dict(batch=-1), fp2.EINVAL),
+])
+def test_invalid_params(kw, status):
+    assert call_prefill(base(**kw)) == status
+    assert fp2.last_error() != ""
+
+
+def test_null_and_workspace_errors():
+    p = base()
+    assert call_prefill(p, q=None) == fp2.EINVAL
+    assert call_prefill(p, cu=None) == fp2.EINVAL
+    assert call_prefill(p, bt=None) == fp2.EINVAL
+    assert call_prefill(p, out=None) == fp2.EINVAL
+    assert call_prefill(p, mask=None) == fp2.EINVAL
+    assert call_prefill(p, q=ctypes.c_void_p(0x100008)) == fp2.EINVAL    # misaligned
+    assert call_prefill(base(dtype="fp8")) == fp2.EINVAL                 # scales missing
+    assert call_prefill(p) == fp2.EWORKSPACE
+    need = fp2.workspace_bytes(p)
+    assert call_prefill(p, ws=FAKE, wsb=need - 1) == fp2.EWORKSPACE
+    assert call_prefill(p, ws=ctypes.c_void_p(0x100010), wsb=need) == fp2.EWORKSPACE  # alignment
+    assert "workspace" in fp2.last_error()
+
+
+def test_host_lengths_checked():
+    p = base()
+    bad = np.array([0, 5000, 6000], dtype=np.int32)       # 5000 > max_seq_len
+    assert call_prefill(p, cuh=ctypes.c_void_p(bad.ctypes.data)) == fp2.EINVAL
+    bad2 = np.array([1, 2, 3], dtype=np.int32)
+    assert call_prefill(p, cuh=ctypes.c_void_p(bad2.ctypes.data)) == fp2.EINVAL
+    bad3 = np.array([0, 10, 5], dtype=np.int32)
+    assert call_prefill(p, cuh=ctypes.c_void_p(bad3.ctypes.data)) == fp2.EINVAL
+
+
+def test_noop_problems_return_ok():
+    assert call_prefill(base(batch=0), q=None, cu=None, k=None, v=None, out=None, mask=None) == fp2.OK
+    assert call_prefill(base(max_seq_len=0), q=None, k=None, v=None, out=None, mask=None) == fp2.OK
+
+
+def test_status_strings():
+    for s in range(5):
+        assert fp2.status_str(s)
+    assert fp2.status_str(99) == "unknown status"
