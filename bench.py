@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Benchmark of the block-sparse causal GQA prefill operator on one MI355X.
+
+One step = one fp2_prefill call (block means, fused scoring and selection,
+sparse attention with the mean correction) over one synthetic layer whose
+inputs are already resident in HBM. Default workload: 128K tokens, 32 query /
+8 KV heads, head_dim 128, block 128, paged KV (page 64), fp8 e4m3 with
+per-head scales, threshold calibrated to ~5% kept blocks, correction on.
+
+Prints ONE JSON line with the dense-equivalent throughput, the latency, the
+kept-block ratio, a roofline entry for the attention kernel (the dominant
+kernel), the oracle timed on the host cores on a bounded sample, and the
+other 128K variants (kept ratio, correction off, bf16, GQA 8:1).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "128K prefill attn latency + dense-equiv TFLOP/s (bf16/fp8); kept-block ratio"
+PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama128k_fp8")
+    ap.add_argument("--target", default="0.05", help="kept-ratio target the alpha was calibrated for")
+    ap.add_argument("--no-variants", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-units", type=int, default=64,
+                    help="(sequence, KV head, query block) units the oracle runs for the CPU baseline")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="only run the timed loop of the default workload (for rocprofv3)")
+    return ap.parse_args()
+
+
+def setup(name, target, correction=None):
+    import torch
+    import numpy as np  # noqa: F401
+    import paper_2608_19758_amd as fp2
+    import synth
+
+    spec = synth.named(name)
+    if correction is not None:
+        spec = spec.replace(mean_correction=int(correction))
+    wl = synth.generate(spec)
+    alpha = synth.alpha_for(name, target)
+    d = wl.device_inputs("cuda")
+    if spec.dtype == "bf16":
+        for k in ("q", "k_cache", "v_cache"):
+            d[k] = d[k].view(torch.bfloat16)
+    p = fp2.make_params(batch=spec.batch, num_q_heads=spec.num_q_heads,
+                        num_kv_heads=spec.num_kv_heads, max_seq_len=spec.max_seq_len,
+                        page_size=spec.page_size, max_pages_per_seq=wl.max_pages, alpha=alpha,
+                        sink_blocks=spec.sink_blocks, window_blocks=spec.window_blocks,
+                        recent_blocks=spec.recent_blocks, mean_correction=spec.mean_correction,
+                        dtype=spec.dtype)
+    out, mask, _ = fp2.alloc_outputs(p, spec.total_tokens)
+    mask2 = torch.empty_like(mask)
+    ws = fp2.alloc_workspace(p)
+    ws2 = fp2.alloc_workspace(p)
+    bt = d["block_table"] if spec.page_size else None
+    kw = dict(cu_seqlens_host=wl.cu_seqlens, q_scale=d["q_scale"], k_scale=d["k_scale"],
+              v_scale=d["v_scale"])
+
+    def run_prefill():
+        fp2.prefill(p, d["q"], d["k_cache"], d["v_cache"], d["cu_seqlens"], bt, out=out,
+                    block_mask=mask, workspace=ws, **kw)
+
+    def run_estimate():
+        fp2.estimate(p, d["q"], d["k_cache"], d["v_cache"], d["cu_seqlens"], bt,
+                     block_mask=mask2, workspace=ws2, **kw)
+
+    return dict(spec=spec, wl=wl, alpha=alpha, p=p, d=d, out=out, mask=mask,
+                run_prefill=run_prefill, run_estimate=run_estimate)
+
+
+def time_loop(fn, steps, warmup):
+    """Average ms per call with HIP events on the current stream (the stream
+    the library launches on), bracketed by device synchronisation."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    return e0.elapsed_time(e1) / steps, (t1 - t0) * 1e3 / steps
+
+
+def measure(cfg, steps, warmup):
+    from paper_2608_19758_amd import accounting as acc
+    sp = cfg["spec"]
+    t_pre, wall = time_loop(cfg["run_prefill"], steps, warmup)
+    t_est, _ = time_loop(cfg["run_estimate"], steps, warmup)
+    cfg["run_prefill"]()
+    mask = cfg["mask"].cpu().numpy()
+    kept_ratio = acc.block_counts(mask, sp.seqlens, sp.block_size, False)[0] / max(
+        1, sum(((L + 127) // 128) * ((L + 127) // 128 + 1) // 2 for L in sp.seqlens) * sp.num_kv_heads)
+    dense = acc.dense_equiv_flops(sp.seqlens, sp.num_q_heads)
+    fk, fc = acc.attention_flops(mask, sp.seqlens, sp.num_q_heads, sp.num_kv_heads,
+                                 correction=bool(sp.mean_correction))
+    t_attn = max(1e-6, t_pre - t_est)
+    main_peak = PEAK_TFLOPS[sp.dtype]
+    # time-weighted peak: kept tiles run at the dtype's MFMA peak, the
+    # correction chunks on bf16 MFMA
+    peak = (fk + fc) / (fk / main_peak + fc / PEAK_TFLOPS["bf16"]) if (fk + fc) else main_peak
+    achieved = (fk + fc) / (t_attn * 1e-3) / 1e12
+    est_bytes = acc.estimation_bytes(sp.seqlens, sp.num_q_heads, sp.num_kv_heads,
+                                     elem=1 if sp.dtype == "fp8" else 2)
+    return dict(
+        ms_per_step=t_pre, wall_ms_per_step=wall, estimate_ms=t_est, attention_ms=t_attn,
+        dense_tflops=dense / (t_pre * 1e-3) / 1e12, kept_ratio=kept_ratio,
+        attention=dict(executed_tflop=(fk + fc) / 1e12, kept_tflop=fk / 1e12, corr_tflop=fc / 1e12,
+                       achieved_tflops=achieved, peak_tflops=peak, frac=achieved / peak),
+        estimation=dict(alg_bytes=est_bytes, gbs=est_bytes / (t_est * 1e-3) / 1e9,
+                        hbm_frac=est_bytes / (t_est * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                        scoring_tflop=acc.scoring_flops(sp.seqlens, sp.num_q_heads) / 1e12),
+    )
+
+
+def cpu_baseline(cfg, nunits):
+    """The oracle on a bounded sample of the same workload: every KV head,
+    query blocks at an even stride (heaviest included); estimation plus
+    attention of those units under the oracle's own mask."""
+    import numpy as np
+    import oracle
+    sp, wl = cfg["spec"], cfg["wl"]
+    B, g = sp.block_size, sp.num_q_heads // sp.num_kv_heads
+    n = (sp.seqlens[0] + B - 1) // B
+    per_head = max(1, nunits // sp.num_kv_heads)
+    Is = sorted(set(np.linspace(n - 1, 0, per_head).round().astype(int).tolist()))
+    units = [(0, h, I) for h in range(sp.num_kv_heads) for I in Is]
+    inp = oracle.Inputs(wl)
+    op = inp.params(cfg["alpha"])
+    t0 = time.perf_counter()
+    mask = oracle.estimate(inp, op, units=units)
+    oracle.attend(inp, op, mask, units=units)
+    dt = time.perf_counter() - t0
+    L = sp.seqlens[0]
+    flops = 0.0
+    for _, _, I in units:
+        p0, p1 = I * B, min(L, (I + 1) * B)
+        pos = np.arange(p0, p1)
+        flops += float(g * 4 * sp.head_dim * (pos + 1).sum())
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s (dense-equivalent)",
+            "cores": op.nthreads, "kind": "oracle",
+            "sample": "%d units (all %d KV heads x %d query blocks at an even stride, incl. the last) "
+                      "of %s: estimation + attention, %.1f s" % (len(units), sp.num_kv_heads,
+                                                                 len(Is), sp.name, dt),
+            "seconds": dt}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: this operator build has no multi-GPU path "
+              "(sharding by KV head is described in DESIGN.md); got --gpus %d, WORLD_SIZE %d"
+              % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    cfg = setup(args.workload, args.target)
+    if args.profile_only:
+        t, _ = time_loop(cfg["run_prefill"], args.steps, args.warmup)
+        print(json.dumps({"profile_only": True, "ms_per_step": t}), flush=True)
+        return
+    m = measure(cfg, args.steps, args.warmup)
+    sp = cfg["spec"]
+    print("[bench] %s: %.3f ms, %.1f dense-equiv TFLOP/s, kept %.4f" % (
+        sp.name, m["ms_per_step"], m["dense_tflops"], m["kept_ratio"]), file=sys.stderr, flush=True)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, args.cpu_units)
+        print("[bench] cpu baseline: %s" % cpu["sample"], file=sys.stderr, flush=True)
+
+    variants = []
+    if not args.no_variants:
+        vlist = [("llama128k_fp8", "0.10", None), ("llama128k_fp8", "0.02", None),
+                 ("llama128k_fp8", "0.05", 0), ("llama128k_bf16", "0.05", None),
+                 ("wide128k_bf16", "0.009", None), ("wide128k_fp8", "0.009", None)]
+        del cfg
+        torch.cuda.empty_cache()
+        for name, tgt, corr in vlist:
+            if name == args.workload and tgt == args.target and corr is None:
+                continue
+            c = setup(name, tgt, corr)
+            r = measure(c, max(5, args.steps // 2), max(2, args.warmup // 2))
+            variants.append({"workload": name, "kept_target": float(tgt),
+                             "mean_correction": c["spec"].mean_correction,
+                             "ms": round(r["ms_per_step"], 4),
+                             "dense_tflops": round(r["dense_tflops"], 2),
+                             "kept_ratio": round(r["kept_ratio"], 5),
+                             "attention_ms": round(r["attention_ms"], 4),
+                             "estimate_ms": round(r["estimate_ms"], 4),
+                             "attention_mfma_frac": round(r["attention"]["frac"], 4)})
+            print("[bench] variant %s" % json.dumps(variants[-1]), file=sys.stderr, flush=True)
+            del c
+            torch.cuda.empty_cache()
+
+    att = m["attention"]
+    line = {
+        "metric": METRIC,
+        "value": round(m["dense_tflops"], 3),
+        "unit": "TFLOP/s (dense-equivalent)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(m["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": sp.dtype,
+        "data": "synthetic",
+        "config": {"workload": sp.name, "seq_len": sp.max_seq_len, "batch": sp.batch,
+                   "num_q_heads": sp.num_q_heads, "num_kv_heads": sp.num_kv_heads,
+                   "head_dim": sp.head_dim, "block_size": sp.block_size,
+                   "page_size": sp.page_size, "alpha": cfg_alpha(args),
+                   "kept_target": float(args.target), "sink_blocks": sp.sink_blocks,
+                   "window_blocks": sp.window_blocks, "mean_correction": sp.mean_correction},
+        "kept_ratio": round(m["kept_ratio"], 5),
+        "latency_ms": {"prefill": round(m["ms_per_step"], 4),
+                       "estimate": round(m["estimate_ms"], 4),
+                       "attention": round(m["attention_ms"], 4)},
+        "roofline": {"bound": "mfma", "kernel": "attend_kernel",
+                     "achieved": round(att["achieved_tflops"], 2),
+                     "peak": round(att["peak_tflops"], 1), "unit": "TFLOP/s",
+                     "frac": round(att["frac"], 4), "traffic": None},
+        "estimation": {"hbm_gbs": round(m["estimation"]["gbs"], 1),
+                       "hbm_frac": round(m["estimation"]["hbm_frac"], 4)},
+        "cpu_baseline": None if cpu is None else {k: (round(v, 6) if isinstance(v, float) else v)
+                                                  for k, v in cpu.items() if k != "seconds"},
+        "variants": variants,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cfg_alpha(args):
+    import synth
+    return synth.alpha_for(args.workload, args.target)
+
+
+if __name__ == "__main__":
+    main()

@@ -47,7 +47,7 @@ Layout layout_of(const fp2_params_t* p) {
   l.vbar = off;
   off = align256(off + rows * fp2::kHeadDim * sizeof(uint16_t));
   l.kidx = off;
-  off = align256(off + rows * nb_of(p) * sizeof(int16_t));
+  off = align256(off + rows * nb_of(p) * sizeof(int32_t));
   l.kcnt = off;
   off = align256(off + rows * sizeof(int32_t));
   l.total = rows ? off : 0;
@@ -180,7 +180,7 @@ Views views_of(const fp2_params_t* p, void* ws) {
   Views v;
   v.pooled.khat = (uint16_t*)(base + l.khat);
   v.pooled.vbar = (uint16_t*)(base + l.vbar);
-  v.kl.idx = (int16_t*)(base + l.kidx);
+  v.kl.idx = (int32_t*)(base + l.kidx);
   v.kl.cnt = (int32_t*)(base + l.kcnt);
   return v;
 }

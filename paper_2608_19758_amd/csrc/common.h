@@ -67,21 +67,14 @@ __device__ __forceinline__ int e4m3_times512(uint32_t code) {
 }
 
 // OCP e4m3fn code -> bf16 bits (exact: every e4m3 value is a bf16 value).
+// Normal codes rebias the exponent (7 -> 127); subnormal codes m * 2^-9 are
+// formed as an exact float product. Branch-free.
 __device__ __forceinline__ uint32_t e4m3_to_bf16(uint32_t code) {
-  uint32_t s = (code & 0x80u) << 8;
-  uint32_t e = (code >> 3) & 15u, m = code & 7u;
-  uint32_t bits;
-  if (e != 0) {
-    bits = ((e + 120u) << 7) | (m << 4);
-  } else if (m == 0) {
-    bits = 0;
-  } else {
-    // m * 2^-9: normalise m = 1.xx * 2^k
-    int k = 31 - __clz(m);                 // 0..2
-    uint32_t frac = (m << (3 - k)) & 7u;   // mantissa bits below the leading one
-    bits = ((uint32_t)(118 + k) << 7) | (frac << 4);
-  }
-  return s | bits;
+  const uint32_t s = (code & 0x80u) << 8;
+  const uint32_t e = (code >> 3) & 15u, m = code & 7u;
+  const uint32_t normal = ((e + 120u) << 7) | (m << 4);
+  const uint32_t sub = __float_as_uint((float)m * 0x1p-9f) >> 16;
+  return s | (e != 0u ? normal : sub);
 }
 
 // ---------------------------------------------------------------------------

@@ -195,7 +195,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p, Pooled po
   const bool keep_all = p.alpha == 0.f;
   const float thr = keep_all ? -INFINITY : mu + fast_log2(p.alpha);
 
-  int16_t* kidx = kl.idx + row * p.nbmax;
+  int32_t* kidx = kl.idx + row * p.nbmax;
   int base = 0;
   for (int J0 = 0; J0 < p.nbmax; J0 += kThreads) {
     const int J = J0 + tid;
@@ -215,7 +215,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p, Pooled po
         wpre += k < w ? redi[k] : 0;
         tot += redi[k];
       }
-      if (keep) kidx[base + wpre + pre] = (int16_t)J;
+      if (keep) kidx[base + wpre + pre] = J;
       base += tot;
     }
   }
@@ -239,7 +239,7 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
     return;
   }
   const uint8_t* mrow = mask + row * p.nbmax;
-  int16_t* kidx = kl.idx + row * p.nbmax;
+  int32_t* kidx = kl.idx + row * p.nbmax;
   int base = 0;
   for (int J0 = 0; J0 <= I; J0 += 256) {
     const int J = J0 + tid;
@@ -255,7 +255,7 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
       wpre += k < w ? redi[k] : 0;
       tot += redi[k];
     }
-    if (keep) kidx[base + wpre + pre] = (int16_t)J;
+    if (keep) kidx[base + wpre + pre] = J;
     base += tot;
   }
   if (tid == 0) kl.cnt[row] = base;

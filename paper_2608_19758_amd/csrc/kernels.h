@@ -31,7 +31,7 @@ struct Pooled {
 };
 
 struct KeptLists {
-  int16_t* idx;             // [batch, Hkv, nbmax, nbmax] ascending kept blocks per row
+  int32_t* idx;             // [batch, Hkv, nbmax, nbmax] ascending kept blocks per row
   int32_t* cnt;             // [batch, Hkv, nbmax]
 };
 

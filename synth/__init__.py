@@ -88,15 +88,16 @@ class Spec:
         return dataclasses.replace(self, **kw)
 
 
-def _normal(seed: int, tag: int, b: int, rows: int, heads: int, d: int) -> np.ndarray:
-    """N(0,1) float32 array [rows, heads, d], drawn in fixed-size token chunks."""
-    out = np.empty((rows, heads, d), dtype=np.float32)
+def _normal(seed: int, tag: int, b: int, out: np.ndarray) -> None:
+    """Fill ``out`` [rows, heads, d] (float32) with N(0,1), drawn in fixed-size
+    token chunks (chunk c from stream [seed, tag, b, c])."""
+    rows, heads, d = out.shape
     nchunks = (rows + _CHUNK - 1) // _CHUNK
 
     def fill(c: int) -> None:
         r0, r1 = c * _CHUNK, min(rows, (c + 1) * _CHUNK)
         g = np.random.default_rng([seed, tag, b, c])
-        out[r0:r1] = g.standard_normal((r1 - r0, heads, d), dtype=np.float32)
+        g.standard_normal((r1 - r0, heads, d), dtype=np.float32, out=out[r0:r1])
 
     if nchunks <= 1:
         for c in range(nchunks):
@@ -104,7 +105,6 @@ def _normal(seed: int, tag: int, b: int, rows: int, heads: int, d: int) -> np.nd
     else:
         with _cf.ThreadPoolExecutor(_threads()) as ex:
             list(ex.map(fill, range(nchunks)))
-    return out
 
 
 def ragged_lengths(seed: int, batch: int, lo: int, hi: int) -> List[int]:
@@ -247,18 +247,22 @@ def generate(spec: Spec) -> Workload:
     u /= np.linalg.norm(u, axis=1, keepdims=True)
     u = u.astype(np.float32)
 
+    import torch
     qf = np.empty((total, Hq, d), dtype=np.float32)
     kf = np.empty((total, Hkv, d), dtype=np.float32)
     vf = np.empty((total, Hkv, d), dtype=np.float32)
+    qt, kt = torch.from_numpy(qf), torch.from_numpy(kf)
+    # query bias pattern: head hq of group h gets query_bias * u_h
+    qbias = torch.from_numpy(np.repeat(sp.query_bias * u, g, axis=0))          # [Hq, d]
     salient: List[List[np.ndarray]] = []
     for b, L in enumerate(sp.seqlens):
         s0 = int(cu[b])
         if L == 0:
             salient.append([np.zeros(0, dtype=np.int64) for _ in range(Hkv)])
             continue
-        qf[s0:s0 + L] = _normal(seed, 1, b, L, Hq, d)
-        kf[s0:s0 + L] = _normal(seed, 2, b, L, Hkv, d)
-        vf[s0:s0 + L] = _normal(seed, 3, b, L, Hkv, d)
+        _normal(seed, 1, b, qf[s0:s0 + L])
+        _normal(seed, 2, b, kf[s0:s0 + L])
+        _normal(seed, 3, b, vf[s0:s0 + L])
         n = (L + B - 1) // B
         per_head = []
         for h in range(Hkv):
@@ -267,10 +271,15 @@ def generate(spec: Spec) -> Workload:
             pick = (sg.choice(n - 1, size=cnt, replace=False) + 1) if cnt > 0 else np.zeros(0, dtype=np.int64)
             blocks = np.sort(np.concatenate([[0], pick])).astype(np.int64)
             per_head.append(blocks)
+            kb = torch.from_numpy(sp.key_bias * u[h])
             for J in blocks:
-                kf[s0 + J * B: s0 + min(L, (J + 1) * B), h, :] += sp.key_bias * u[h]
-            for I in range(0, n, 2):
-                qf[s0 + I * B: s0 + min(L, (I + 1) * B), h * g:(h + 1) * g, :] += sp.query_bias * u[h]
+                kt[s0 + J * B: s0 + min(L, (J + 1) * B), h, :] += kb
+        # even-indexed query blocks: whole pairs of blocks, then the tail
+        full = (L // (2 * B)) * 2 * B
+        if full:
+            qt[s0:s0 + full].view(full // (2 * B), 2, B, Hq, d)[:, 0] += qbias
+        if full < L:
+            qt[s0 + full:s0 + min(L, full + B)] += qbias
         salient.append(per_head)
 
     if sp.dtype == "bf16":
@@ -280,17 +289,20 @@ def generate(spec: Spec) -> Workload:
         vs = np.ones(Hkv, dtype=np.float32)
     elif sp.dtype == "fp8":
         def quant(x):
-            amax = np.abs(x).max(axis=(0, 2)) if x.shape[0] else np.ones(x.shape[1], np.float32)
+            t = torch.from_numpy(x)
+            if x.shape[0]:
+                amax = t.abs().amax(dim=(0, 2)).numpy()
+            else:
+                amax = np.ones(x.shape[1], np.float32)
             sc = (np.maximum(amax, 1e-30) / E4M3_MAX).astype(np.float32)
-            y = x / sc[None, :, None]
-            np.clip(y, -E4M3_MAX, E4M3_MAX, out=y)
-            return _to_e4m3_bits(y), sc
+            y = (t / torch.from_numpy(sc)[None, :, None]).clamp_(-E4M3_MAX, E4M3_MAX)
+            return y.to(torch.float8_e4m3fn).view(torch.uint8).numpy(), sc
         q, qs = quant(qf)
         k, ks = quant(kf)
         v, vs = quant(vf)
     else:
         raise ValueError(sp.dtype)
-    del qf, kf, vf
+    del qf, kf, vf, qt, kt
 
     if sp.page_size > 0:
         p = sp.page_size
