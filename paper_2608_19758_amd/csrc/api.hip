@@ -35,7 +35,7 @@ int nb_of(const fp2_params_t* p) { return (p->max_seq_len + fp2::kBlock - 1) / f
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t khat, vbar, kidx, kcnt, total;
+  size_t khat, vbar, kidx, kcnt, queue, total;
 };
 
 Layout layout_of(const fp2_params_t* p) {
@@ -50,6 +50,8 @@ Layout layout_of(const fp2_params_t* p) {
   off = align256(off + rows * nb_of(p) * sizeof(int32_t));
   l.kcnt = off;
   off = align256(off + rows * sizeof(int32_t));
+  l.queue = off;
+  off += 256;
   l.total = rows ? off : 0;
   return l;
 }
@@ -182,6 +184,7 @@ Views views_of(const fp2_params_t* p, void* ws) {
   v.pooled.vbar = (uint16_t*)(base + l.vbar);
   v.kl.idx = (int32_t*)(base + l.kidx);
   v.kl.cnt = (int32_t*)(base + l.kcnt);
+  v.kl.queue = (int32_t*)(base + l.queue);
   return v;
 }
 

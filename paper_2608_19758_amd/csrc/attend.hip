@@ -2,38 +2,45 @@
 // (Sec. 3.2 Eq. correction, Sec. 3.3; Algorithm 1 steps 6-11).
 //
 // Work unit: (sequence b, KV head h, query block I) of the packed query rows
-// of Eq. packgqa. A workgroup of W waves takes 32*W of the g*B packed rows
-// (W = 8, or 4 when g = 1), so one K/V tile in LDS serves all g query heads
-// of the group. Units are dealt heaviest-first and the workgroups of a unit
-// go to the same XCD (consecutive dispatch slots of one XCD), so they share
-// K/V through its L2.
+// of Eq. packgqa. A work item is a slice of 32*W of the g*B packed rows of a
+// unit, taken by a workgroup of W waves (W = 8, or 4 when g = 1), so one K/V
+// tile in LDS serves all g query heads of the group. The grid is persistent:
+// one workgroup per compute unit (the LDS ring admits one), each taking items
+// from an atomic counter in order of decreasing query block (heaviest
+// first), so the run time of an item never holds up the dispatch of others.
 //
 // The key sequence of a unit is a list of 64-key steps: both halves of every
-// kept block, walked from the last kept index down (Eq. csr), then both
-// halves of every 128-block chunk of pooled means that holds a pruned block
-// (the correction). Steps run through a ring of LDS stages (128 KiB: 4 bf16
-// stages or 8 fp8 stages): the rows of step s+NST-1 are copied straight from
-// the page-addressed pool (Eq. page) into LDS with global_load_lds_dwordx4
-// while step s is computed, with one workgroup barrier per step. Page-table
-// and kept-list reads are scalar loads, so nothing in the loop waits on the
-// copies except the explicit count before each barrier.
+// kept block, walked from the last kept index down (Eq. csr), then the pooled
+// means of the pruned blocks J < I, 64 per step (the correction). Steps run
+// through a ring of LDS stages (128 KiB: 4 bf16 stages or 8 fp8 stages): the
+// rows of step s+NST-1 are copied straight from the page-addressed pool
+// (Eq. page) into LDS with global_load_lds_dwordx4 while step s is computed,
+// with one workgroup barrier per step. The copy addresses come from small LDS
+// tables filled once per chunk of steps (kept block index and its page-table
+// entries, or the compacted list of pruned blocks), read one step ahead, so
+// nothing in the loop waits on a global load.
 //
 // Per step:
 //  - S^T = K Q^T on the matrix cores (A = key rows from LDS, B = the wave's
 //    32 query rows held in registers). Lane l then owns query l%32 and 16
-//    keys per 32-key subtile, so the row max/sum of the online softmax need
-//    one exchange with lane l^32;
+//    keys per 32-key subtile, so the row maximum of the online softmax needs
+//    one exchange with lane l^32 (v_permlane32_swap);
 //  - O^T += V^T P^T: the probabilities go straight from the S^T accumulators
 //    into the B operand, and V^T comes from LDS through the gfx950
 //    transposing reads ds_read_b64_tr_b16 / _b8 (no transpose pass).
-// bf16 uses v_mfma_f32_32x32x16_bf16. fp8 (OCP e4m3fn) uses
-// v_mfma_f32_32x32x64_f8f6f4 on the raw codes; the per-head scales c_q c_k
-// are applied to the fp32 scores, the probabilities are stored as
-// e4m3(2^8 * exp(S - m)) (range [0, 256], Sec. 3.3 Eq. fp8) and c_v is
-// applied in the epilogue; the 2^8 is removed from the LSE.
-// Correction steps use the pooled means as keys khat_J and values vbar_J
-// (bf16, real units, bf16 MFMA for both dtypes), logits shifted by
-// log2|B_J| = 7 (Sec. 3.2 implementation paragraph).
+// fp8 (OCP e4m3fn) uses v_mfma_f32_32x32x64_f8f6f4 on the raw codes; the
+// per-head scales c_q c_k are applied to the fp32 scores, the probabilities
+// are stored as e4m3(2^8 * exp(S - m)) (range [0, 256]) and the denominator
+// sums those stored values (Sec. 3.3 Eq. fp8); c_v is applied in the
+// epilogue and the 2^8 is removed from the LSE. The fp8 loop is software
+// pipelined: the scores of step s+1 are issued to the matrix cores before
+// the softmax of step s runs on the vector ALUs.
+// bf16 uses v_mfma_f32_32x32x16_bf16. Correction steps use the pooled means
+// as keys khat_J and values vbar_J (bf16, real units, bf16 MFMA for both
+// dtypes), logits shifted by log2|B_J| = 7 (Sec. 3.2 implementation
+// paragraph).
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace fp2 {
@@ -41,8 +48,12 @@ namespace fp2 {
 namespace {
 
 constexpr float kLn2 = 0.69314718055994530942f;
-constexpr int kStep = 64;           // keys per pipeline step
-constexpr int kRingU4 = 8192;       // LDS ring: 128 KiB in 16-byte slots
+constexpr int kStep = 64;            // keys per pipeline step
+constexpr int kRingU4 = 8192;        // LDS ring: 128 KiB in 16-byte slots
+constexpr int kJtab = 1024;          // kept blocks per table chunk
+constexpr int kTab = 2048;           // page-table entries per table chunk
+constexpr int kAuxI32 = kJtab + kTab;          // 12 KiB of tables
+constexpr int kPlist = 2 * kAuxI32;            // pruned blocks per correction chunk (u16)
 
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 typedef __attribute__((address_space(3))) i32x2_t lds_i32x2_t;
@@ -63,17 +74,17 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// Wait until the copies of the current step have landed while `ahead` later
-// steps (D copies each, at most MAXA of them) stay in flight.
-template <int D, int MAXA>
-__device__ __forceinline__ void wait_steps_ahead(int ahead) {
-  static_assert(MAXA >= 1 && MAXA <= 6 && MAXA * D < 64, "ring depth");
+// Wait until a step's copies have landed while `ahead` later steps (D copies
+// each, ahead <= 6) stay in flight.
+template <int D>
+__device__ __forceinline__ void wait_ahead(int ahead) {
+  static_assert(6 * D < 64, "ring depth");
   if (ahead <= 0) wait_vmcnt<0>();
-  else if (ahead == 1 || MAXA == 1) wait_vmcnt<D>();
-  else if (ahead == 2 || MAXA == 2) wait_vmcnt<2 * D>();
-  else if (ahead == 3 || MAXA == 3) wait_vmcnt<3 * D>();
-  else if (ahead == 4 || MAXA == 4) wait_vmcnt<4 * D>();
-  else if (ahead == 5 || MAXA == 5) wait_vmcnt<5 * D>();
+  else if (ahead == 1) wait_vmcnt<D>();
+  else if (ahead == 2) wait_vmcnt<2 * D>();
+  else if (ahead == 3) wait_vmcnt<3 * D>();
+  else if (ahead == 4) wait_vmcnt<4 * D>();
+  else if (ahead == 5) wait_vmcnt<5 * D>();
   else wait_vmcnt<6 * D>();
 }
 
@@ -97,228 +108,189 @@ __device__ __forceinline__ void dma16(const void* g, uint4* lds) {
 }
 #pragma clang diagnostic pop
 
-// Scalar (wave-uniform) 32-bit load of read-only data written before the
-// kernel started; counted by lgkmcnt, so it never waits on the copies.
-__device__ __forceinline__ int sload_i32(const int32_t* ptr) {
-  int v;
-  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(ptr));
-  return v;
-}
-
-// Step ring: steps 0 .. nsteps-1; issue(stage, s) starts the copies of step
-// s (D per thread), compute(stage, s) consumes it. Stage of step s: s % NST.
-template <int NST, int D, class Issue, class Compute>
-__device__ __forceinline__ void run_ring(uint4* ring, int stage_u4, int nsteps, Issue issue,
-                                         Compute compute) {
-#pragma unroll 1
-  for (int s = 0; s < NST - 1 && s < nsteps; ++s) issue(ring + s * stage_u4, s);
-#pragma unroll 1
-  for (int s = 0; s < nsteps; ++s) {
-    wait_steps_ahead<D, NST - 2>(min(NST - 2, nsteps - 1 - s));
-    lds_barrier();   // step s visible to all; every wave is done with step s-1
-    if (s + NST - 1 < nsteps) issue(ring + ((s + NST - 1) % NST) * stage_u4, s + NST - 1);
-    compute(ring + (s % NST) * stage_u4, s);
-  }
-  lds_barrier();     // the ring may be refilled afterwards
-}
-
-// Copy 64 rows (row r: byte offset row_off(r0, r) from Kb / Vb, r0 = first
-// row of the copy instruction, wave-uniform) into a stage: K rows at slots
-// [0, 64*CPR), V rows at [64*CPR, 128*CPR), CPR 16-byte chunks per row.
-template <int W, int FP8, class RowOff>
-__device__ __forceinline__ void copy_rows(uint4* st, const uint8_t* Kb, const uint8_t* Vb,
-                                          RowOff row_off) {
-  constexpr int CPR = FP8 ? 8 : 16;
-  constexpr int RPG = 64 / CPR;               // rows per 1 KiB copy
-  constexpr int PER = (kStep / RPG) / W;      // copy instructions per wave and tensor
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int pc = lane % CPR;
-  int64_t offs[PER];
-#pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const int r0 = RPG * (w + W * j);
-    offs[j] = row_off(r0, r0 + lane / CPR);
-  }
-#pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const int g = w + W * j;
-    const int r = RPG * g + lane / CPR;
-    const int kc = FP8 ? (pc ^ ((r >> 1) & 7)) : (pc ^ (r & 15));
-    const int vc = FP8 ? (pc ^ (2 * ((r >> 1) & 3))) : (pc ^ (4 * (r & 3)));
-    dma16(Kb + offs[j] + 16 * kc, st + g * 64);
-    dma16(Vb + offs[j] + 16 * vc, st + 64 * CPR + g * 64);
-  }
-}
-
-template <int W, int FP8> struct Copies {
-  static constexpr int CPR = FP8 ? 8 : 16;
-  static constexpr int per_step = 2 * ((kStep / (64 / CPR)) / W);   // per thread
-  static constexpr int stage_u4 = 2 * kStep * CPR;
-  static constexpr int nst = kRingU4 / stage_u4;
+// Copy plan of one 64-row step (K and V): copy instruction j of wave w moves
+// rows RPG*(w + W*j) .. +RPG-1, lane i taking 16-byte slot i % CPR of row
+// RPG*(w + W*j) + i / CPR.
+template <int W, int FP8>
+struct Plan {
+  static constexpr int CPR = FP8 ? 8 : 16;          // 16-byte chunks per row
+  static constexpr int RPG = 64 / CPR;              // rows per copy instruction
+  static constexpr int PER = kStep / RPG / W;       // copies per wave and tensor
+  static constexpr int D = 2 * PER;                 // copies per thread and step
+  static constexpr int STAGE = 2 * kStep * CPR;     // 16-byte slots per stage
+  static constexpr int NST = kRingU4 / STAGE;       // ring depth
+  __device__ static int row(int j, int tid) { return RPG * ((tid >> 6) + W * j) + (tid & 63) / CPR; }
 };
 
-// Online-softmax update of one 32-row tile over NU 32-key subtiles. On entry
-// s holds raw scores (-inf where masked); the logits are x = cs * s + shift
-// (log2 units). On return s holds 2^(x - m + off), their row sum has been
-// added to l_i, and o / l_i have been rescaled to the new running maximum.
-template <int NU>
-__device__ __forceinline__ void softmax_update(f32x16_t (&s)[NU], f32x16_t (&o)[4], float& m_i,
-                                               float& l_i, float cs, float shift, float off) {
+// Start the copies of one step: row row(j) of K / V lies at byte offset
+// off[j] from Kb / Vb.
+template <int W, int FP8>
+__device__ __forceinline__ void issue_copies(uint4* st, const uint8_t* Kb, const uint8_t* Vb,
+                                             const int64_t (&off)[Plan<W, FP8>::PER], int tid) {
+  using P = Plan<W, FP8>;
+  const int w = tid >> 6, lane = tid & 63;
+  const int pc = lane % P::CPR;
+#pragma unroll
+  for (int j = 0; j < P::PER; ++j) {
+    const int g = w + W * j;
+    const int r = P::RPG * g + lane / P::CPR;
+    const int kc = FP8 ? (pc ^ ((r >> 1) & 7)) : (pc ^ (r & 15));
+    const int vc = FP8 ? (pc ^ (2 * ((r >> 1) & 3))) : (pc ^ (4 * (r & 3)));
+    dma16(Kb + off[j] + 16 * kc, st + g * 64);
+    dma16(Vb + off[j] + 16 * vc, st + 64 * P::CPR + g * 64);
+  }
+}
+
+// Ring over steps 0 .. n-1 without cross-step overlap of the compute:
+// offs(s, r) gives the byte offset of row r of step s, body(stage, s)
+// consumes step s. Ends with a barrier (the ring may be refilled).
+template <int W, int FP8, class Offs, class Body>
+__device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
+                                          Offs offs, Body body, int tid) {
+  using P = Plan<W, FP8>;
+  int64_t nxt[P::PER];
+  auto load = [&](int s) {
+#pragma unroll
+    for (int j = 0; j < P::PER; ++j) nxt[j] = offs(s, P::row(j, tid));
+  };
+  int ni = 0;
+#pragma unroll 1
+  for (; ni < P::NST - 1 && ni < n; ++ni) {
+    load(ni);
+    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, nxt, tid);
+  }
+  if (ni < n) load(ni);
+#pragma unroll 1
+  for (int s = 0; s < n; ++s) {
+    wait_ahead<P::D>(ni - 1 - s);
+    lds_barrier();   // step s visible to all; every wave is done with step s-1
+    const bool more = ni < n;
+    if (more) issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, nxt, tid);
+    body(ring + (s % P::NST) * P::STAGE, s);
+    if (more && ni < n) load(ni);   // table reads overlap the matrix cores
+  }
+  lds_barrier();
+}
+
+// Larger of a lane's value and that of lane l^32.
+__device__ __forceinline__ float xhalf_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  const float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+  return a > b ? a : b;
+}
+
+// Running state of the RT 32-row tiles of one wave.
+template <int RT>
+struct RowState {
+  f32x16_t o[RT][4];   // O^T accumulators: o[rt][dt][4i+j] = O[row][32dt + 8i + 4*half + j]
+  f32x16_t ls[RT];     // fp8 kept keys: row sums of P~ from the matrix cores (element 0);
+                       // folded into l once the kept blocks are done
+  float m[RT];         // running maximum (log2 units)
+  float l[RT];         // row-sum part summed on the vector ALUs (this lane's keys)
+};
+
+// Online-softmax rescale of row tile rt to the new running maximum of the
+// raw scores s (-inf where masked); the logits are x = cs * s + shift (log2
+// units, cs > 0). Returns the bias b with x - m + off = cs * s + b.
+template <int NU, bool LS, int RT>
+__device__ __forceinline__ float softmax_rescale(const f32x16_t (&s)[NU], RowState<RT>& rs, int rt,
+                                                 float cs, float shift, float off) {
   float mr = -INFINITY;
 #pragma unroll
   for (int u = 0; u < NU; ++u)
 #pragma unroll
     for (int e = 0; e < 16; ++e) mr = fmaxf(mr, s[u][e]);
-  mr = fmaxf(mr, __shfl_xor(mr, 32, 64));
+  mr = xhalf_max(mr);
   const float mx = mr == -INFINITY ? -INFINITY : fmaf(mr, cs, shift);
   // m_new stays -inf only while no key of this row has been visible; the
-  // update is then the identity (alpha = 1, p = 0), without branching the
+  // update is then the identity (scale 1, p = 0), without branching the
   // wave away from the MFMAs that follow.
-  const float m_new = fmaxf(m_i, mx);
+  const float m_new = fmaxf(rs.m[rt], mx);
   const float m_use = m_new == -INFINITY ? 0.f : m_new;
-  if (__any(m_new != m_i)) {
-    const float alpha = fast_exp2(m_i - m_use);
-    l_i *= alpha;
+  if (__any(m_new != rs.m[rt])) {
+    const float a = fast_exp2(rs.m[rt] - m_use);
+    rs.l[rt] *= a;
+    if (LS) rs.ls[rt][0] *= a;   // the only element of the row-sum tile that is read
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) o[dt][e] *= alpha;
+      for (int e = 0; e < 16; ++e) rs.o[rt][dt][e] *= a;
   }
-  m_i = m_new;
-  const float bias = shift + off - m_use;
-  float ls = 0.f;
-#pragma unroll
-  for (int u = 0; u < NU; ++u)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const float pv = fast_exp2(fmaf(s[u][e], cs, bias));
-      s[u][e] = pv;
-      ls += pv;
-    }
-  l_i += ls;
+  rs.m[rt] = m_new;
+  return shift + off - m_use;
 }
 
-// Running state of the RT query-row tiles of one wave.
-template <int RT>
-struct RowState {
-  f32x16_t o[RT][4];   // O^T accumulators: o[rt][dt][4i+j] = O[row][32dt + 8i + 4*half + j]
-  float m[RT], l[RT];  // running maximum (log2 units) and row sum
-};
+// Pairwise sum of 16 values.
+__device__ __forceinline__ float sum16(const float (&x)[16]) {
+  float a[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] = x[2 * i] + x[2 * i + 1];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[i] = a[2 * i] + a[2 * i + 1];
+  return (a[0] + a[1]) + (a[2] + a[3]);
+}
 
-// One bf16 step of 64 keys for all RT row tiles of the wave; every LDS
-// fragment read feeds RT MFMAs. KIND 0: kept keys key0 .. key0+63 (diag:
-// causal mask against pos[rt]). KIND 1: correction, column k is used iff
-// k < nv and todo[k] (logit shift +7, PV weights x pv_scale).
+// ---------------------------------------------------------------------------
+// bf16 step: 64 keys, QK + softmax + PV for the RT row tiles of the wave;
+// every LDS operand read feeds RT MFMAs. KIND 0: kept keys key0 .. key0+63
+// (diag: causal mask against pos). KIND 1: correction, column k is used iff
+// k < nv (logit shift +7, PV weights x pv_scale).
+// ---------------------------------------------------------------------------
 template <int KIND, int RT>
-__device__ __forceinline__ void step_bf16(const uint4* st, const uint8_t* todo, int nv,
-                                          const bf16x8_t (&qb)[RT][8], RowState<RT>& rs,
-                                          float cs, float off, float pv_scale, int key0,
-                                          const int (&pos)[RT], bool diag) {
-  const int lane = threadIdx.x & 63;
-  const int half = lane >> 5, l32 = lane & 31;
-  const int g16 = lane >> 4, i16 = lane & 15;
-  const int sidx = i16 >> 2, r4 = i16 & 3;
-  const uint4* vt = st + kStep * 16;
-#pragma unroll 1
-  for (int u = 0; u < 2; ++u) {          // 32 keys at a time
-    f32x16_t s[RT][1];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) s[rt][0] = f32x16_t{};
-    const int r = 32 * u + l32;
-#pragma unroll
-    for (int ds = 0; ds < 8; ++ds) {
-      const bf16x8_t a = __builtin_bit_cast(bf16x8_t, st[kslot16(r, 2 * ds + half)]);
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-        s[rt][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb[rt][ds], s[rt][0], 0, 0, 0);
-    }
-    // key of s[rt][0][4i+j] is 32u + 8i + 4*half + j
-    if (KIND == 1 || diag) {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int key = 32 * u + 8 * i + 4 * half + j;
-            const bool drop = KIND == 1 ? !(key < nv && todo[key]) : (key0 + key > pos[rt]);
-            s[rt][0][4 * i + j] = drop ? -INFINITY : s[rt][0][4 * i + j];
-          }
-    }
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-      softmax_update<1>(s[rt], rs.o[rt], rs.m[rt], rs.l[rt], cs, KIND == 1 ? 7.0f : 0.0f, off);
-
-    // O^T += V^T P^T, 16 keys per MFMA: slot i' of lane half H is key
-    // 32u + 16a + 8(i'/4) + 4H + i'%4, i.e. s[rt][0][8a + i'].
-#pragma unroll
-    for (int a = 0; a < 2; ++a) {
-      bf16x8_t pb[RT];
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        uint32_t pw[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float x0 = s[rt][0][8 * a + 2 * q], x1 = s[rt][0][8 * a + 2 * q + 1];
-          pw[q] = KIND == 1 ? pack_bf16x2(x0 * pv_scale, x1 * pv_scale) : pack_bf16x2(x0, x1);
-        }
-        pb[rt] = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
-      }
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        i16x4_t rd[2];
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt) {
-          const int key = 32 * u + 16 * a + 8 * tt + 4 * (g16 >> 1) + sidx;
-          const int d = 32 * dt + 16 * (g16 & 1) + 4 * r4;
-          const int byte = vslot16(key, d >> 3) * 16 + (d & 7) * 2;
-          rd[tt] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)((lds_char_t*)vt + byte));
-        }
-        const i32x2_t r0 = __builtin_bit_cast(i32x2_t, rd[0]);
-        const i32x2_t r1 = __builtin_bit_cast(i32x2_t, rd[1]);
-        const bf16x8_t va = __builtin_bit_cast(bf16x8_t, (i32x4_t){r0[0], r0[1], r1[0], r1[1]});
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-          rs.o[rt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[rt], rs.o[rt][dt], 0, 0, 0);
-      }
-    }
-  }
-}
-
-// Four e4m3 codes (round to nearest even) of four non-negative floats <= 448.
-__device__ __forceinline__ int pack_e4m3x4(float a, float b, float c, float d) {
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
-  return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
-}
-
-// One fp8 step of 64 kept keys key0 .. key0+63 for all RT row tiles.
-template <int RT>
-__device__ __forceinline__ void step_fp8(const uint4* st, const i32x8_t (&qf)[RT][2],
-                                         RowState<RT>& rs, float cs, int key0,
-                                         const int (&pos)[RT], bool diag) {
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ void step_bf16(const uint4* st, const bf16x8_t (&qb)[RT][8],
+                                          RowState<RT>& rs, float cs, float off, float pv_scale,
+                                          int key0, const int (&pos)[RT], bool diag, int nv,
+                                          int lane) {
   const int half = lane >> 5, l32 = lane & 31;
   f32x16_t s[RT][2];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) s[rt][0] = s[rt][1] = f32x16_t{};
-#pragma unroll
   for (int u = 0; u < 2; ++u) {
-    const int r = 32 * u + l32;
+    bf16x8_t a[8];
 #pragma unroll
-    for (int ds = 0; ds < 2; ++ds) {
-      const uint4 c0 = st[kslot8(r, 4 * ds + 2 * half)];
-      const uint4 c1 = st[kslot8(r, 4 * ds + 2 * half + 1)];
-      const i32x8_t av = {(int)c0.x, (int)c0.y, (int)c0.z, (int)c0.w,
-                          (int)c1.x, (int)c1.y, (int)c1.z, (int)c1.w};
+    for (int ds = 0; ds < 8; ++ds)
+      a[ds] = __builtin_bit_cast(bf16x8_t, st[kslot16(32 * u + l32, 2 * ds + half)]);
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-        s[rt][u] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, qf[rt][ds], s[rt][u], 0, 0, 0,
-                                                                   0, 0, 0);
+    for (int rt = 0; rt < RT; ++rt) {
+      s[rt][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qb[rt][0], f32x16_t{}, 0, 0, 0);
+#pragma unroll
+      for (int ds = 1; ds < 8; ++ds)
+        s[rt][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ds], qb[rt][ds], s[rt][u], 0, 0, 0);
     }
   }
-  if (diag) {
+  // V^T fragment of key group kg (16 keys) and output tile dt: slot i' of
+  // lane half H is key 16kg + 8(i'/4) + 4H + i'%4.
+  const int g16 = lane >> 4, i16 = lane & 15;
+  const int sidx = i16 >> 2, r4 = i16 & 3;
+  const uint4* vt = st + kStep * 16;
+  auto vread = [&](int kg, int dt) -> bf16x8_t {
+    i16x4_t rd[2];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+    for (int tt = 0; tt < 2; ++tt) {
+      const int key = 16 * kg + 8 * tt + 4 * (g16 >> 1) + sidx;
+      const int d = 32 * dt + 16 * (g16 & 1) + 4 * r4;
+      const int byte = vslot16(key, d >> 3) * 16 + (d & 7) * 2;
+      rd[tt] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)((lds_char_t*)vt + byte));
+    }
+    const i32x2_t r0 = __builtin_bit_cast(i32x2_t, rd[0]);
+    const i32x2_t r1 = __builtin_bit_cast(i32x2_t, rd[1]);
+    return __builtin_bit_cast(bf16x8_t, (i32x4_t){r0[0], r0[1], r1[0], r1[1]});
+  };
+
+  // V^T fragments are read once for all row tiles (held when RT > 1)
+  bf16x8_t va[RT > 1 ? 4 : 1][4];
+  if (RT > 1) {
+#pragma unroll
+    for (int kg = 0; kg < 4; ++kg)
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) va[RT > 1 ? kg : 0][dt] = vread(kg, dt);
+  }
+
+  // key of s[rt][u][4i+j] is 32u + 8i + 4*half + j. Per tile: softmax, then
+  // its PV MFMAs, which run while the next tile's softmax is computed.
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    if (KIND == 1 || diag) {
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -326,24 +298,69 @@ __device__ __forceinline__ void step_fp8(const uint4* st, const i32x8_t (&qf)[RT
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int key = 32 * u + 8 * i + 4 * half + j;
-            s[rt][u][4 * i + j] = (key0 + key > pos[rt]) ? -INFINITY : s[rt][u][4 * i + j];
+            const bool drop = KIND == 1 ? key >= nv : key0 + key > pos[rt];
+            s[rt][u][4 * i + j] = drop ? -INFINITY : s[rt][u][4 * i + j];
           }
-  }
-  // O^T += V^T P^T over the 64 keys: byte b of lane half H is the key of
-  // s[b/16][b%16], i.e. 16(b/8) + 8((b%8)/4) + 4H + b%4.
-  i32x8_t pb[RT];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    softmax_update<2>(s[rt], rs.o[rt], rs.m[rt], rs.l[rt], cs, 0.0f, 8.0f);
-    int pk[2][4];
+    }
+    const float bias = softmax_rescale<2, false>(s[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off);
+    float pv[2][16];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        pk[u][q] = pack_e4m3x4(s[rt][u][4 * q], s[rt][u][4 * q + 1], s[rt][u][4 * q + 2],
-                               s[rt][u][4 * q + 3]);
-    pb[rt] = (i32x8_t){pk[0][0], pk[0][1], pk[0][2], pk[0][3], pk[1][0], pk[1][1], pk[1][2], pk[1][3]};
+      for (int e = 0; e < 16; ++e) pv[u][e] = fast_exp2(fmaf(s[rt][u][e], cs, bias));
+    rs.l[rt] += sum16(pv[0]) + sum16(pv[1]);
+    // O^T += V^T P^T, 16 keys per MFMA; B operand of key group kg = 2u + a:
+    // slot i' of lane half H is s[u][8a + i']
+#pragma unroll
+    for (int kg = 0; kg < 4; ++kg) {
+      uint32_t pw[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float x0 = pv[kg >> 1][8 * (kg & 1) + 2 * q], x1 = pv[kg >> 1][8 * (kg & 1) + 2 * q + 1];
+        pw[q] = KIND == 1 ? pack_bf16x2(x0 * pv_scale, x1 * pv_scale) : pack_bf16x2(x0, x1);
+      }
+      const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        const bf16x8_t v = RT > 1 ? va[RT > 1 ? kg : 0][dt] : vread(kg, dt);
+        rs.o[rt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, pb, rs.o[rt][dt], 0, 0, 0);
+      }
+    }
   }
+}
+
+// ---------------------------------------------------------------------------
+// fp8 pieces: the scores of one 64-key step, then softmax + PV.
+// ---------------------------------------------------------------------------
+template <int RT>
+__device__ __forceinline__ void qk_fp8(const uint4* st, const i32x8_t (&qf)[RT][2],
+                                       f32x16_t (&s)[RT][2], int lane) {
+  const int half = lane >> 5, l32 = lane & 31;
+  i32x8_t a[2][2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int ds = 0; ds < 2; ++ds) {
+      const int r = 32 * u + l32;
+      const uint4 c0 = st[kslot8(r, 4 * ds + 2 * half)];
+      const uint4 c1 = st[kslot8(r, 4 * ds + 2 * half + 1)];
+      a[u][ds] = (i32x8_t){(int)c0.x, (int)c0.y, (int)c0.z, (int)c0.w,
+                           (int)c1.x, (int)c1.y, (int)c1.z, (int)c1.w};
+    }
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      s[rt][u] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[u][0], qf[rt][0], f32x16_t{}, 0, 0,
+                                                                  0, 0, 0, 0);
+      s[rt][u] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[u][1], qf[rt][1], s[rt][u], 0, 0,
+                                                                  0, 0, 0, 0);
+    }
+}
+
+// V^T fragments of a 64-key fp8 step: byte b of lane half H is key
+// 16(b/8) + 8((b%8)/4) + 4H + b%4.
+__device__ __forceinline__ void vread_fp8(const uint4* st, i32x8_t (&va)[4], int lane) {
   const int g16 = lane >> 4, i16 = lane & 15;
   const int sidx = i16 >> 1, r2 = i16 & 1;
   const int H = g16 >> 1;
@@ -358,177 +375,255 @@ __device__ __forceinline__ void step_fp8(const uint4* st, const i32x8_t (&qf)[RT
       const int byte = vslot8(key, c) * 16 + 8 * r2;
       rd[t] = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2_t*)((lds_char_t*)vt + byte));
     }
-    const i32x8_t va = {rd[0][0], rd[0][1], rd[1][0], rd[1][1], rd[2][0], rd[2][1], rd[3][0], rd[3][1]};
+    va[dt] = (i32x8_t){rd[0][0], rd[0][1], rd[1][0], rd[1][1], rd[2][0], rd[2][1], rd[3][0], rd[3][1]};
+  }
+}
+
+// Four e4m3 codes (round to nearest even) of four non-negative floats <= 448.
+__device__ __forceinline__ int pack_e4m3x4(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
+}
+
+// One fp8 step of 64 kept keys key0 .. key0+63 for the RT row tiles of the
+// wave: S^T for all tiles, then per tile the softmax (diag: causal mask
+// against pos) and O^T += V^T P~^T with P~ = e4m3(2^8 exp(x - m)), so that
+// the softmax of one tile runs on the vector ALUs while the matrix cores work
+// on the other tile. The row sums of P~ come from the matrix cores as well:
+// an all-ones A operand (e4m3 1.0 = 0x38) times P~^T puts sum_k P~[row][k]
+// in every element of the lane's column.
+template <int RT>
+__device__ __forceinline__ void step_fp8(const uint4* st, const i32x8_t (&qf)[RT][2],
+                                         RowState<RT>& rs, float cs, int key0,
+                                         const int (&pos)[RT], bool diag, int lane) {
+  const int half = lane >> 5;
+  f32x16_t s[RT][2];
+  qk_fp8<RT>(st, qf, s, lane);
+  i32x8_t va[4];
+  vread_fp8(st, va, lane);
+  const int one = 0x38383838;
+  const i32x8_t ones = {one, one, one, one, one, one, one, one};
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-      rs.o[rt][dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(va, pb[rt], rs.o[rt][dt], 0, 0,
-                                                                     0, 0, 0, 0);
+  for (int rt = 0; rt < RT; ++rt) {
+    if (diag) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int key = 32 * u + 8 * i + 4 * half + j;
+            s[rt][u][4 * i + j] = (key0 + key > pos[rt]) ? -INFINITY : s[rt][u][4 * i + j];
+          }
+    }
+    const float bias = softmax_rescale<2, true>(s[rt], rs, rt, cs, 0.0f, 8.0f);
+    int pk[8];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        pk[4 * u + q] = pack_e4m3x4(fast_exp2(fmaf(s[rt][u][4 * q], cs, bias)),
+                                    fast_exp2(fmaf(s[rt][u][4 * q + 1], cs, bias)),
+                                    fast_exp2(fmaf(s[rt][u][4 * q + 2], cs, bias)),
+                                    fast_exp2(fmaf(s[rt][u][4 * q + 3], cs, bias)));
+    const i32x8_t pb = {pk[0], pk[1], pk[2], pk[3], pk[4], pk[5], pk[6], pk[7]};
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+      rs.o[rt][dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(va[dt], pb, rs.o[rt][dt], 0, 0, 0,
+                                                                     0, 0, 0);
+    rs.ls[rt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones, pb, rs.ls[rt], 0, 0, 0, 0, 0, 0);
   }
 }
 
 template <int FP8, int W, int RT>
-__global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p, Pooled pooled,
-                                                                const uint8_t* __restrict__ mask,
-                                                                KeptLists kl,
-                                                                uint16_t* __restrict__ out,
-                                                                float* __restrict__ lse) {
+__global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled pooled,
+                                                           const uint8_t* __restrict__ mask,
+                                                           KeptLists kl,
+                                                           uint16_t* __restrict__ out,
+                                                           float* __restrict__ lse) {
   __shared__ uint4 ring[kRingU4];
-  __shared__ uint8_t todo[kMaxBlocks];      // correction: J < I not kept
-  __shared__ uint8_t cflag[kMaxBlocks / kBlock];
-  __shared__ int32_t clist[kMaxBlocks / kBlock];
-  __shared__ int ncl;
+  __shared__ int32_t aux[kAuxI32];          // kept: block list + page entries; correction: pruned list
+  __shared__ int32_t wtot[W];
+  __shared__ int32_t s_item;
 
-  constexpr int M = 32 * RT * W;            // packed rows per workgroup
-  const int wpu = p.g * kBlock / M;         // workgroups per unit
-  const int x = blockIdx.x;
-  const int xcd = x & 7, k = x >> 3;
-  const int u = 8 * (k / wpu) + xcd;
-  const int msub = k % wpu;
-  const int nbh = p.batch * p.hkv;
-  const int nunits = p.nbmax * nbh;
-  if (u >= nunits) return;
-  const int I = p.nbmax - 1 - u / nbh;
-  const int bh = u % nbh;
-  const int b = bh / p.hkv, h = bh % p.hkv;
-  const int64_t tok0 = p.cu[b];
-  const int L = p.cu[b + 1] - (int)tok0;
-  const int n = (L + kBlock - 1) / kBlock;
-  if (I >= n) return;
+  constexpr int M = 32 * RT * W;            // packed rows per work item
+  const int wpu = p0.g * kBlock / M;        // work items per unit
+  const int nbh = p0.batch * p0.hkv;
+  const int nitems = p0.nbmax * nbh * wpu;
+  const int tid0 = threadIdx.x;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int half = lane >> 5, l32 = lane & 31;
-  const int G = p.g;
-  const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
+  // Persistent workgroups: items (unit, row slice) are taken from a counter
+  // in order of decreasing query block, i.e. heaviest first; the loop ends
+  // for every wave once the counter passes the last item.
+#pragma unroll 1
+  for (;;) {
+    if (tid0 == 0) s_item = atomicAdd(kl.queue, 1);
+    __syncthreads();
+    const int item = s_item;
+    __syncthreads();   // every wave has read s_item before it is written again
+    if (item >= nitems) break;
+    // Opaque copies of the thread index and of the argument block: what is
+    // derived from them is recomputed per item instead of being held in
+    // registers across the whole loop. p0 is the first kernel argument, so it
+    // sits at offset 0 of the kernel argument segment; its fields are read
+    // back from there with scalar loads.
+    int tid = tid0;
+    asm volatile("" : "+v"(tid));
+    typedef const __attribute__((address_space(4))) Problem KProblem;
+    KProblem* pk = (KProblem*)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(pk));
+    KProblem& p = *pk;
 
-  // this lane's query rows (packed rows of Eq. packgqa): one per row tile;
-  // all of them belong to the same query head because G divides 32
-  int pos[RT];
-  bool qvalid[RT];
-  int64_t qoff[RT];
-  const int pr0 = msub * M + w * 32 * RT + l32;
-  const int hq = h * G + pr0 % G;
+    const int u = item / wpu;
+    const int msub = item - u * wpu;
+    const int I = p.nbmax - 1 - u / nbh;
+    const int bh = u % nbh;
+    const int b = bh / p.hkv, h = bh % p.hkv;
+    const int64_t tok0 = p.cu[b];
+    const int L = p.cu[b + 1] - (int)tok0;
+    const int n = (L + kBlock - 1) / kBlock;
+    if (I >= n) continue;
+
+    const int lane = tid & 63, w = tid >> 6;
+    const int half = lane >> 5, l32 = lane & 31;
+    const int G = p.g;
+    const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
+
+    // this lane's query rows (packed rows of Eq. packgqa), one per row tile;
+    // G divides 32, so a lane column keeps one query head
+    const int pr0 = msub * M + w * 32 * RT + l32;
+    const int hq = h * G + pr0 % G;
+    int pos[RT];
+    bool qvalid[RT];
+    int64_t qoff[RT];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int pr = pr0 + 32 * rt;
-    pos[rt] = I * kBlock + pr / G;
-    qvalid[rt] = pos[rt] < L;
-    qoff[rt] = ((tok0 + pos[rt]) * p.hq + hq) * kHeadDim;   // element index
-  }
+    for (int rt = 0; rt < RT; ++rt) {
+      pos[rt] = I * kBlock + (pr0 + 32 * rt) / G;
+      qvalid[rt] = pos[rt] < L;
+      qoff[rt] = ((tok0 + pos[rt]) * p.hq + hq) * kHeadDim;   // element index
+    }
 
-  RowState<RT> rs;
+    RowState<RT> rs;
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) rs.o[rt][dt] = f32x16_t{};
-    rs.m[rt] = -INFINITY;
-    rs.l[rt] = 0.f;
-  }
-  float qsc = FP8 ? p.q_scale[hq] : 1.f;
-  float vsc = FP8 ? p.v_scale[h] : 1.f;
-  float ksc = FP8 ? p.k_scale[h] : 1.f;
-  const float off = FP8 ? 8.f : 0.f;        // log2 of the probability offset
-  asm volatile("" : "+v"(qsc), "+v"(vsc), "+v"(ksc));  // loads complete before the rings
+      for (int dt = 0; dt < 4; ++dt) rs.o[rt][dt] = f32x16_t{};
+      rs.ls[rt] = f32x16_t{};
+      rs.m[rt] = -INFINITY;
+      rs.l[rt] = 0.f;
+    }
+    float qsc = FP8 ? p.q_scale[hq] : 1.f;
+    float vsc = FP8 ? p.v_scale[h] : 1.f;
+    float ksc = FP8 ? p.k_scale[h] : 1.f;
+    const float off = FP8 ? 8.f : 0.f;        // log2 of the probability offset
+    asm volatile("" : "+v"(qsc), "+v"(vsc), "+v"(ksc));  // loads complete before the rings
 
-  // ---- kept blocks: steps s -> kept index cnt-1-s/2, half s%2
-  {
-    const uint8_t* K = (const uint8_t*)p.k;
-    const uint8_t* V = (const uint8_t*)p.v;
-    constexpr int esz = FP8 ? 1 : 2;
-    const int cnt = kl.cnt[row];
-    const int32_t* kidx = kl.idx + row * p.nbmax;
-    const int64_t rowbytes = (int64_t)p.hkv * kHeadDim * esz;     // one token slot of the pool
-    const int64_t hbytes = (int64_t)h * kHeadDim * esz;
-    constexpr int RPG = FP8 ? 8 : 4;
-    // a page holding whole copy groups lets one scalar table read serve a copy
-    const bool uniform_pages = p.pm.page == 0 || (p.pm.shift >= 0 && p.pm.page >= RPG);
-    const int32_t* ptab = p.pm.table + (int64_t)b * p.pm.stride;
+    using PK = Plan<W, FP8>;
+    int32_t* jtab = aux;
+    int32_t* tab = aux + kJtab;
 
-    bf16x8_t qb[FP8 ? 1 : RT][8];
-    i32x8_t qf[FP8 ? RT : 1][2];
-    if (!FP8) {
+    // ---- kept blocks: step s of a chunk -> its block list entry s/2, half s%2
+    {
+      const uint8_t* K = (const uint8_t*)p.k;
+      const uint8_t* V = (const uint8_t*)p.v;
+      constexpr int esz = FP8 ? 1 : 2;
+      const int cnt = kl.cnt[row];
+      const int32_t* kidx = kl.idx + row * p.nbmax;
+      const bool has_diag = cnt > 0 && kidx[cnt - 1] == I;
+      const int64_t rowbytes = (int64_t)p.hkv * kHeadDim * esz;     // one token slot of the pool
+      const int64_t hbytes = (int64_t)h * kHeadDim * esz;
+      const int page = p.pm.page, shift = p.pm.shift;
+      // page-table entries per block: the pages that block J's 128 tokens touch
+      const int epb = page == 0 ? 0 : shift >= 0 ? (page >= kBlock ? 1 : kBlock / page)
+                                                 : (kBlock - 1 + page - 1) / page + 1;
+      const int chunk = epb == 0 ? kJtab : min(kJtab, kTab / epb);
+      const int32_t* ptab = p.pm.table + (int64_t)b * p.pm.stride;
+
+      i32x8_t qf[FP8 ? RT : 1][2];
+      bf16x8_t qb[FP8 ? 1 : RT][8];
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
-        const uint16_t* qrow = (const uint16_t*)p.q + qoff[rt];
+        if constexpr (FP8) {
+          const uint8_t* qrow = (const uint8_t*)p.q + qoff[rt];
 #pragma unroll
-        for (int ds = 0; ds < 8; ++ds) {
-          uint4 v = make_uint4(0, 0, 0, 0);
-          if (qvalid[rt]) v = *(const uint4*)(qrow + 16 * ds + 8 * half);
-          qb[rt][ds] = __builtin_bit_cast(bf16x8_t, v);
-          asm volatile("" : "+v"(qb[rt][ds]));
-        }
-      }
-    } else {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        const uint8_t* qrow = (const uint8_t*)p.q + qoff[rt];
-#pragma unroll
-        for (int ds = 0; ds < 2; ++ds) {
-          uint4 c0 = make_uint4(0, 0, 0, 0), c1 = make_uint4(0, 0, 0, 0);
-          if (qvalid[rt]) {
-            c0 = *(const uint4*)(qrow + 64 * ds + 32 * half);
-            c1 = *(const uint4*)(qrow + 64 * ds + 32 * half + 16);
+          for (int ds = 0; ds < 2; ++ds) {
+            uint4 c0 = make_uint4(0, 0, 0, 0), c1 = make_uint4(0, 0, 0, 0);
+            if (qvalid[rt]) {
+              c0 = *(const uint4*)(qrow + 64 * ds + 32 * half);
+              c1 = *(const uint4*)(qrow + 64 * ds + 32 * half + 16);
+            }
+            qf[rt][ds] = (i32x8_t){(int)c0.x, (int)c0.y, (int)c0.z, (int)c0.w,
+                                   (int)c1.x, (int)c1.y, (int)c1.z, (int)c1.w};
+            asm volatile("" : "+v"(qf[rt][ds]));
           }
-          qf[rt][ds] = (i32x8_t){(int)c0.x, (int)c0.y, (int)c0.z, (int)c0.w,
-                                 (int)c1.x, (int)c1.y, (int)c1.z, (int)c1.w};
-          asm volatile("" : "+v"(qf[rt][ds]));
+        } else {
+          const uint16_t* qrow = (const uint16_t*)p.q + qoff[rt];
+#pragma unroll
+          for (int ds = 0; ds < 8; ++ds) {
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (qvalid[rt]) v = *(const uint4*)(qrow + 16 * ds + 8 * half);
+            qb[rt][ds] = __builtin_bit_cast(bf16x8_t, v);
+            asm volatile("" : "+v"(qb[rt][ds]));
+          }
+        }
+      }
+      const float cs = FP8 ? p.scale_log2 * qsc * ksc : p.scale_log2;
+
+#pragma unroll 1
+      for (int c0 = 0; c0 < cnt; c0 += chunk) {
+        const int nbc = min(chunk, cnt - c0);
+        // tables of this chunk: block index, and the page-table entries of the
+        // pages it touches (entries past the sequence are never read)
+        for (int i = tid; i < nbc; i += 64 * W) jtab[i] = kidx[cnt - 1 - (c0 + i)];
+        for (int t = tid; t < nbc * epb; t += 64 * W) {
+          const int i = t / epb, e = t - i * epb;
+          const int jb = kidx[cnt - 1 - (c0 + i)] * kBlock;
+          const int pi = (shift >= 0 ? jb >> shift : jb / page) + e;
+          tab[t] = (int64_t)pi * page < L ? ptab[pi] : 0;
+        }
+        __syncthreads();
+        // byte offset of row r of step s: rows past the sequence repeat its
+        // last token (finite data; those keys are masked)
+        auto offs = [&](int s, int r) -> int64_t {
+          const int i = s >> 1;
+          const int jb = jtab[i] * kBlock;
+          const int t = min(jb + kStep * (s & 1) + r, L - 1);
+          int64_t slot;
+          if (page == 0) {
+            slot = tok0 + t;
+          } else if (shift >= 0) {
+            const int e = (t >> shift) - (jb >> shift);
+            slot = (int64_t)tab[i * epb + e] * page + (t & (page - 1));
+          } else {
+            const int pi = t / page;
+            slot = (int64_t)tab[i * epb + pi - jb / page] * page + (t - pi * page);
+          }
+          return slot * rowbytes + hbytes;
+        };
+        const int nst = 2 * nbc;
+        const int ndiag = (c0 == 0 && has_diag) ? 2 : 0;   // the diagonal block comes first
+        if constexpr (FP8) {
+          ring_loop<W, 1>(ring, nst, K, V, offs, [&](const uint4* st, int s) {
+            step_fp8<RT>(st, qf, rs, cs, I * kBlock + kStep * (s & 1), pos, s < ndiag, lane);
+          }, tid);
+        } else {
+          ring_loop<W, 0>(ring, nst, K, V, offs, [&](const uint4* st, int s) {
+            step_bf16<0, RT>(st, qb, rs, cs, off, 1.f, I * kBlock + kStep * (s & 1), pos, s < ndiag,
+                             0, lane);
+          }, tid);
         }
       }
     }
-    const float cs = FP8 ? p.scale_log2 * qsc * ksc : p.scale_log2;
 
-    auto issue = [&](uint4* st, int s) {
-      const int J = sload_i32(kidx + (cnt - 1 - (s >> 1)));
-      const int key0 = J * kBlock + kStep * (s & 1);
-      const int nvalid = L - key0;                       // <= 0: the half lies past the sequence
-      // rows past the sequence repeat a valid row of the block (finite data)
-      const int t0 = nvalid > 0 ? key0 : J * kBlock;
-      copy_rows<W, FP8>(st, K, V, [&](int r0, int r) -> int64_t {
-        const int rg = nvalid > 0 && r0 < nvalid ? r0 : 0;
-        const int rr = nvalid > 0 && r < nvalid ? r : rg;
-        int64_t slot;
-        if (p.pm.page == 0) {
-          slot = tok0 + t0 + rr;
-        } else if (uniform_pages) {
-          const int pi = __builtin_amdgcn_readfirstlane((t0 + rg) >> p.pm.shift);
-          const int64_t pg = sload_i32(ptab + pi);
-          slot = pg * p.pm.page + ((t0 + rr) & (p.pm.page - 1));
-        } else {
-          slot = slot_of(p.pm, b, tok0, t0 + rr);
-        }
-        return slot * rowbytes + hbytes;
-      });
-    };
-    auto compute = [&](const uint4* st, int s) {
-      const int J = sload_i32(kidx + (cnt - 1 - (s >> 1)));
-      const int key0 = J * kBlock + kStep * (s & 1);
-      if constexpr (FP8) step_fp8<RT>(st, qf, rs, cs, key0, pos, J == I);
-      else step_bf16<0, RT>(st, nullptr, 0, qb, rs, cs, off, 1.f, key0, pos, J == I);
-    };
-    using C = Copies<W, FP8>;
-    run_ring<C::nst, C::per_step>(ring, C::stage_u4, 2 * cnt, issue, compute);
-  }
+    if constexpr (FP8) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) rs.l[rt] += half == 0 ? rs.ls[rt][0] : 0.f;
+    }
 
-  // ---- mean correction over the pruned blocks J < I
-  if (p.corr && I > 0) {
-    const uint8_t* mrow = mask + row * p.nbmax;
-    const int nch = (I + kBlock - 1) / kBlock;
-    for (int c = tid; c < nch; c += 64 * W) cflag[c] = 0;
-    __syncthreads();
-    for (int J = tid; J < I; J += 64 * W) {
-      const uint8_t f = !(mrow[J] & 1);
-      todo[J] = f;
-      if (f) cflag[J / kBlock] = 1;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      int c2 = 0;
-      for (int c = 0; c < nch; ++c)
-        if (cflag[c]) clist[c2++] = c;
-      ncl = c2;
-    }
-    __syncthreads();
-    const int nc = ncl;
-    if (nc > 0) {
+    // ---- mean correction over the pruned blocks J < I, compacted into a list
+    if (p.corr && I > 0) {
+      const uint8_t* mrow = mask + row * p.nbmax;
+      uint16_t* plist = (uint16_t*)aux;
       // Q as bf16 (fp8 codes widen exactly); the fp8 scale goes into cs.
       bf16x8_t qb[RT][8];
 #pragma unroll
@@ -541,7 +636,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p, Pooled poo
               v = *(const uint4*)((const uint16_t*)p.q + qoff[rt] + 16 * ds + 8 * half);
             } else {
               const uint2 cc = *(const uint2*)((const uint8_t*)p.q + qoff[rt] + 16 * ds + 8 * half);
-              uint32_t wv[2] = {cc.x, cc.y};
+              const uint32_t wv[2] = {cc.x, cc.y};
               uint32_t ow[4];
 #pragma unroll
               for (int i = 0; i < 4; ++i) {
@@ -561,64 +656,96 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p, Pooled poo
       const int64_t pbase = ((int64_t)b * p.hkv + h) * p.nbmax * kHeadDim;
       const uint8_t* Kh = (const uint8_t*)(pooled.khat + pbase);
       const uint8_t* Vh = (const uint8_t*)(pooled.vbar + pbase);
-      auto issue = [&](uint4* st, int s) {
-        const int c0 = clist[s >> 1] * kBlock;
-        const int j0 = c0 + kStep * (s & 1);
-        const int nv = I - j0;                           // <= 0: the half is all masked
-        copy_rows<W, 0>(st, Kh, Vh, [&](int r0, int r) -> int64_t {
-          (void)r0;
-          const int jr = r < nv ? j0 + r : c0;            // past I: repeat a valid row
-          return (int64_t)jr * kHeadDim * 2;
-        });
-      };
-      auto compute = [&](const uint4* st, int s) {
-        const int j0 = clist[s >> 1] * kBlock + kStep * (s & 1);
-        step_bf16<1, RT>(st, todo + j0, I - j0, qb, rs, cs, off, pv_scale, 0, pos, false);
-      };
-      using C = Copies<W, 0>;
-      run_ring<C::nst, C::per_step>(ring, C::stage_u4, 2 * nc, issue, compute);
+#pragma unroll 1
+      for (int j0 = 0; j0 < I; j0 += kPlist) {
+        const int j1 = min(I, j0 + kPlist);
+        // compaction of the pruned J in [j0, j1), in ascending order
+        int np = 0;
+#pragma unroll 1
+        for (int jb = j0; jb < j1; jb += 64 * W) {
+          const int J = jb + tid;
+          const bool f = J < j1 && !(mrow[J] & 1);
+          const uint64_t bal = __ballot(f);
+          const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+          if (lane == 0) wtot[w] = __popcll(bal);
+          __syncthreads();
+          int base = np, tot = 0;
+#pragma unroll
+          for (int v = 0; v < W; ++v) {
+            base += v < w ? wtot[v] : 0;
+            tot += wtot[v];
+          }
+          if (f) plist[base + before] = (uint16_t)J;
+          np += tot;
+          __syncthreads();
+        }
+        if (np == 0) continue;
+        auto offs = [&](int s, int r) -> int64_t {
+          const int i = min(kStep * s + r, np - 1);       // past the list: repeat a valid entry
+          return (int64_t)plist[i] * kHeadDim * 2;
+        };
+        ring_loop<W, 0>(ring, (np + kStep - 1) / kStep, Kh, Vh, offs, [&](const uint4* st, int s) {
+          step_bf16<1, RT>(st, qb, rs, cs, off, pv_scale, 0, pos, false, np - kStep * s, lane);
+        }, tid);
+      }
+    }
+
+    // epilogue: O = c_v O^T / l, LSE = (m + log2 l - off) ln 2
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const float l_tot = rs.l[rt] + __shfl_xor(rs.l[rt], 32, 64);
+      if (!qvalid[rt]) continue;
+      const float inv = vsc / l_tot;
+      uint16_t* orow = out + qoff[rt];
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d = 32 * dt + 8 * i + 4 * half;
+          uint2 v;
+          v.x = pack_bf16x2(rs.o[rt][dt][4 * i + 0] * inv, rs.o[rt][dt][4 * i + 1] * inv);
+          v.y = pack_bf16x2(rs.o[rt][dt][4 * i + 2] * inv, rs.o[rt][dt][4 * i + 3] * inv);
+          *(uint2*)(orow + d) = v;
+        }
+      if (lse && half == 0)
+        lse[(tok0 + pos[rt]) * p.hq + hq] = (rs.m[rt] + fast_log2(l_tot) - off) * kLn2;
     }
   }
+}
 
-  // epilogue: O = c_v O^T / l, LSE = (m + log2 l - off) ln 2
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const float l_tot = rs.l[rt] + __shfl_xor(rs.l[rt], 32, 64);
-    if (!qvalid[rt]) continue;
-    const float inv = vsc / l_tot;
-    uint16_t* orow = out + qoff[rt];
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d = 32 * dt + 8 * i + 4 * half;
-        uint2 v;
-        v.x = pack_bf16x2(rs.o[rt][dt][4 * i + 0] * inv, rs.o[rt][dt][4 * i + 1] * inv);
-        v.y = pack_bf16x2(rs.o[rt][dt][4 * i + 2] * inv, rs.o[rt][dt][4 * i + 3] * inv);
-        *(uint2*)(orow + d) = v;
-      }
-    if (lse && half == 0)
-      lse[(tok0 + pos[rt]) * p.hq + hq] = (rs.m[rt] + fast_log2(l_tot) - off) * kLn2;
+// Compute units of the current device (one resident workgroup each: the
+// kernel's LDS use admits one per CU).
+int device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cus[dev] = n;
   }
+  return cus[dev];
 }
 
 template <int FP8, int W, int RT>
-void launch_cfg(const Problem& p, const Pooled& pooled, const uint8_t* mask, const KeptLists& kl,
-                void* out, float* lse, hipStream_t s) {
-  const int64_t nunits = (int64_t)p.nbmax * p.batch * p.hkv;
-  const int64_t units8 = (nunits + 7) / 8 * 8;
-  const int wpu = p.g * kBlock / (32 * RT * W);
-  const unsigned grid = (unsigned)(units8 * wpu);
+hipError_t launch_cfg(const Problem& p, const Pooled& pooled, const uint8_t* mask,
+                      const KeptLists& kl, void* out, float* lse, hipStream_t s) {
+  const int64_t nitems = (int64_t)p.nbmax * p.batch * p.hkv * (p.g * kBlock / (32 * RT * W));
+  const int cus = device_cus();
+  if (cus <= 0) return hipErrorInvalidDevice;
+  const unsigned grid = (unsigned)std::min<int64_t>(nitems, cus);
   attend_kernel<FP8, W, RT><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, (uint16_t*)out, lse);
+  return hipSuccess;
 }
 
 template <int FP8>
-void launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask, const KeptLists& kl,
-               void* out, float* lse, hipStream_t s) {
+hipError_t launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask,
+                     const KeptLists& kl, void* out, float* lse, hipStream_t s) {
   // 32 query rows per wave; 8 waves (two per SIMD) when the unit has at
   // least 256 packed rows, else 4
-  if (p.g == 1) launch_cfg<FP8, 4, 1>(p, pooled, mask, kl, out, lse, s);
-  else launch_cfg<FP8, 8, 1>(p, pooled, mask, kl, out, lse, s);
+  if (p.g == 1) return launch_cfg<FP8, 4, 1>(p, pooled, mask, kl, out, lse, s);
+  return launch_cfg<FP8, 8, 1>(p, pooled, mask, kl, out, lse, s);
 }
 
 }  // namespace
@@ -626,9 +753,9 @@ void launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask, cons
 hipError_t launch_attend(const Problem& p, const Pooled& pooled, const uint8_t* mask,
                          const KeptLists& kl, void* out, float* lse, hipStream_t s) {
   if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
-  if (p.fp8) launch_dt<1>(p, pooled, mask, kl, out, lse, s);
-  else launch_dt<0>(p, pooled, mask, kl, out, lse, s);
-  return hipGetLastError();
+  const hipError_t e = p.fp8 ? launch_dt<1>(p, pooled, mask, kl, out, lse, s)
+                             : launch_dt<0>(p, pooled, mask, kl, out, lse, s);
+  return e != hipSuccess ? e : hipGetLastError();
 }
 
 }  // namespace fp2

@@ -52,6 +52,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p, Pooled po
   const int n = (L + kBlock - 1) / kBlock;
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
   uint8_t* mrow = mask + row * p.nbmax;
+  if (blockIdx.x == 0 && tid == 0) *kl.queue = 0;
 
   if (I >= n) {
     for (int J = tid; J < p.nbmax; J += kThreads) mrow[J] = 0;
@@ -234,6 +235,7 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
   const int L = p.cu[b + 1] - p.cu[b];
   const int n = (L + kBlock - 1) / kBlock;
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
+  if (blockIdx.x == 0 && tid == 0) *kl.queue = 0;
   if (I >= n) {
     if (tid == 0) kl.cnt[row] = 0;
     return;

@@ -33,6 +33,8 @@ struct Pooled {
 struct KeptLists {
   int32_t* idx;             // [batch, Hkv, nbmax, nbmax] ascending kept blocks per row
   int32_t* cnt;             // [batch, Hkv, nbmax]
+  int32_t* queue;           // work counter of the attention kernel; the kernel that
+                            // builds the lists sets it to 0
 };
 
 hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s);

@@ -12,6 +12,11 @@ import synth
 
 TOL = {"bf16": 2e-2, "fp8": 6e-2}   # max-abs, attention output under the same mask
 BAND = 1e-4                         # relative distance of a block energy from the threshold
+# LSE (natural log). bf16: fp32 softmax arithmetic, far below 1e-2. fp8: the
+# denominator sums the e4m3-rounded probabilities of Eq. fp8; round to nearest
+# with 3 mantissa bits moves each term by at most 2^-4 of itself, so the sum,
+# and its log, by at most ln(1 + 2^-4) < 0.0625.
+LSE_TOL = {"bf16": 1e-2, "fp8": 0.0625}
 
 
 def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=0.0):
