@@ -54,6 +54,12 @@ constexpr int kJtab = 1024;          // kept blocks per table chunk
 constexpr int kTab = 2048;           // page-table entries per table chunk
 constexpr int kAuxI32 = kJtab + kTab;          // 12 KiB of tables
 constexpr int kPlist = 2 * kAuxI32;            // pruned blocks per correction chunk (u16)
+#ifndef ATT_W
+#define ATT_W 8
+#endif
+#ifndef ATT_PIPE
+#define ATT_PIPE 0
+#endif
 
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 typedef __attribute__((address_space(3))) i32x2_t lds_i32x2_t;
@@ -172,6 +178,45 @@ __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb,
   lds_barrier();
 }
 
+// Ring over steps 0 .. n-1 with the scores of step s+1 issued to the matrix
+// cores before the rest of step s runs: qk(stage, S) starts the score MFMAs
+// of a step, fin(stage, S, s) finishes step s from its scores. The vector
+// work of step s then overlaps the MFMAs of step s+1 within the wave.
+template <int W, int FP8, class SC, class Offs, class QK, class Fin>
+__device__ __forceinline__ void pipe_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
+                                          Offs offs, QK qk, Fin fin, int tid) {
+  using P = Plan<W, FP8>;
+  static_assert(P::NST >= 3, "the ring holds steps s-1 (refill), s and s+1");
+  int64_t nxt[P::PER];
+  auto load = [&](int s) {
+#pragma unroll
+    for (int j = 0; j < P::PER; ++j) nxt[j] = offs(s, P::row(j, tid));
+  };
+  int ni = 0;
+#pragma unroll 1
+  for (; ni < P::NST - 1 && ni < n; ++ni) {
+    load(ni);
+    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, nxt, tid);
+  }
+  if (ni < n) load(ni);
+  wait_ahead<P::D>(ni - 1);
+  lds_barrier();   // step 0 visible to all
+  SC sc, sn;
+  qk(ring, sc);
+#pragma unroll 1
+  for (int s = 0; s < n; ++s) {
+    if (s + 1 < n) wait_ahead<P::D>(ni - 2 - s);
+    lds_barrier();   // step s+1 visible; every wave is done with step s-1
+    const bool more = ni < n;
+    if (more) issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, nxt, tid);
+    if (s + 1 < n) qk(ring + ((s + 1) % P::NST) * P::STAGE, sn);
+    fin(ring + (s % P::NST) * P::STAGE, sc, s);
+    if (more && ni < n) load(ni);
+    sc = sn;
+  }
+  lds_barrier();
+}
+
 // Larger of a lane's value and that of lane l^32.
 __device__ __forceinline__ float xhalf_max(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
@@ -188,6 +233,13 @@ struct RowState {
                        // folded into l once the kept blocks are done
   float m[RT];         // running maximum (log2 units)
   float l[RT];         // row-sum part summed on the vector ALUs (this lane's keys)
+};
+
+// Raw scores S^T of one 64-key step for the RT row tiles: v[rt][u][4i+j] is
+// key 32u + 8i + 4*half + j of the lane's query row.
+template <int RT>
+struct Scores {
+  f32x16_t v[RT][2];
 };
 
 // Online-softmax rescale of row tile rt to the new running maximum of the
@@ -232,18 +284,13 @@ __device__ __forceinline__ float sum16(const float (&x)[16]) {
 }
 
 // ---------------------------------------------------------------------------
-// bf16 step: 64 keys, QK + softmax + PV for the RT row tiles of the wave;
-// every LDS operand read feeds RT MFMAs. KIND 0: kept keys key0 .. key0+63
-// (diag: causal mask against pos). KIND 1: correction, column k is used iff
-// k < nv (logit shift +7, PV weights x pv_scale).
+// bf16 steps of 64 keys for the RT row tiles of the wave; every LDS operand
+// read feeds RT MFMAs.
 // ---------------------------------------------------------------------------
-template <int KIND, int RT>
-__device__ __forceinline__ void step_bf16(const uint4* st, const bf16x8_t (&qb)[RT][8],
-                                          RowState<RT>& rs, float cs, float off, float pv_scale,
-                                          int key0, const int (&pos)[RT], bool diag, int nv,
-                                          int lane) {
+template <int RT>
+__device__ __forceinline__ void qk_bf16(const uint4* st, const bf16x8_t (&qb)[RT][8], Scores<RT>& S,
+                                        int lane) {
   const int half = lane >> 5, l32 = lane & 31;
-  f32x16_t s[RT][2];
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     bf16x8_t a[8];
@@ -252,12 +299,24 @@ __device__ __forceinline__ void step_bf16(const uint4* st, const bf16x8_t (&qb)[
       a[ds] = __builtin_bit_cast(bf16x8_t, st[kslot16(32 * u + l32, 2 * ds + half)]);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      s[rt][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qb[rt][0], f32x16_t{}, 0, 0, 0);
+      S.v[rt][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], qb[rt][0], f32x16_t{}, 0, 0, 0);
 #pragma unroll
       for (int ds = 1; ds < 8; ++ds)
-        s[rt][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ds], qb[rt][ds], s[rt][u], 0, 0, 0);
+        S.v[rt][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ds], qb[rt][ds], S.v[rt][u], 0, 0, 0);
     }
   }
+}
+
+// Softmax + PV of a bf16 step from its scores. KIND 0: kept keys key0 ..
+// key0+63 (diag: causal mask against pos). KIND 1: correction, column k is
+// used iff k < nv (logit shift +7, PV weights x pv_scale). NPRE of the four
+// 16-key groups of V^T are read before the softmax, the rest just before
+// their MFMAs.
+template <int KIND, int RT, int NPRE>
+__device__ __forceinline__ void fin_bf16(const uint4* st, Scores<RT>& S, RowState<RT>& rs, float cs,
+                                         float off, float pv_scale, int key0, const int (&pos)[RT],
+                                         bool diag, int nv, int lane) {
+  const int half = lane >> 5;
   // V^T fragment of key group kg (16 keys) and output tile dt: slot i' of
   // lane half H is key 16kg + 8(i'/4) + 4H + i'%4.
   const int g16 = lane >> 4, i16 = lane & 15;
@@ -276,17 +335,14 @@ __device__ __forceinline__ void step_bf16(const uint4* st, const bf16x8_t (&qb)[
     const i32x2_t r1 = __builtin_bit_cast(i32x2_t, rd[1]);
     return __builtin_bit_cast(bf16x8_t, (i32x4_t){r0[0], r0[1], r1[0], r1[1]});
   };
-
-  // V^T fragments are read once for all row tiles (held when RT > 1)
-  bf16x8_t va[RT > 1 ? 4 : 1][4];
-  if (RT > 1) {
+  constexpr int NV = RT > 1 ? 4 : NPRE;   // several row tiles share every fragment
+  bf16x8_t va[NV > 0 ? NV : 1][4];
 #pragma unroll
-    for (int kg = 0; kg < 4; ++kg)
+  for (int kg = 0; kg < NV; ++kg)
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt) va[RT > 1 ? kg : 0][dt] = vread(kg, dt);
-  }
+    for (int dt = 0; dt < 4; ++dt) va[kg][dt] = vread(kg, dt);
 
-  // key of s[rt][u][4i+j] is 32u + 8i + 4*half + j. Per tile: softmax, then
+  // key of S[rt][u][4i+j] is 32u + 8i + 4*half + j. Per tile: softmax, then
   // its PV MFMAs, which run while the next tile's softmax is computed.
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
@@ -299,18 +355,18 @@ __device__ __forceinline__ void step_bf16(const uint4* st, const bf16x8_t (&qb)[
           for (int j = 0; j < 4; ++j) {
             const int key = 32 * u + 8 * i + 4 * half + j;
             const bool drop = KIND == 1 ? key >= nv : key0 + key > pos[rt];
-            s[rt][u][4 * i + j] = drop ? -INFINITY : s[rt][u][4 * i + j];
+            S.v[rt][u][4 * i + j] = drop ? -INFINITY : S.v[rt][u][4 * i + j];
           }
     }
-    const float bias = softmax_rescale<2, false>(s[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off);
+    const float bias = softmax_rescale<2, false>(S.v[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off);
     float pv[2][16];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) pv[u][e] = fast_exp2(fmaf(s[rt][u][e], cs, bias));
+      for (int e = 0; e < 16; ++e) pv[u][e] = fast_exp2(fmaf(S.v[rt][u][e], cs, bias));
     rs.l[rt] += sum16(pv[0]) + sum16(pv[1]);
     // O^T += V^T P^T, 16 keys per MFMA; B operand of key group kg = 2u + a:
-    // slot i' of lane half H is s[u][8a + i']
+    // slot i' of lane half H is S[u][8a + i']
 #pragma unroll
     for (int kg = 0; kg < 4; ++kg) {
       uint32_t pw[4];
@@ -322,7 +378,7 @@ __device__ __forceinline__ void step_bf16(const uint4* st, const bf16x8_t (&qb)[
       const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
-        const bf16x8_t v = RT > 1 ? va[RT > 1 ? kg : 0][dt] : vread(kg, dt);
+        const bf16x8_t v = kg < NV ? va[kg < NV ? kg : 0][dt] : vread(kg, dt);
         rs.o[rt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v, pb, rs.o[rt][dt], 0, 0, 0);
       }
     }
@@ -333,8 +389,8 @@ __device__ __forceinline__ void step_bf16(const uint4* st, const bf16x8_t (&qb)[
 // fp8 pieces: the scores of one 64-key step, then softmax + PV.
 // ---------------------------------------------------------------------------
 template <int RT>
-__device__ __forceinline__ void qk_fp8(const uint4* st, const i32x8_t (&qf)[RT][2],
-                                       f32x16_t (&s)[RT][2], int lane) {
+__device__ __forceinline__ void qk_fp8(const uint4* st, const i32x8_t (&qf)[RT][2], Scores<RT>& S,
+                                       int lane) {
   const int half = lane >> 5, l32 = lane & 31;
   i32x8_t a[2][2];
 #pragma unroll
@@ -351,10 +407,10 @@ __device__ __forceinline__ void qk_fp8(const uint4* st, const i32x8_t (&qf)[RT][
   for (int u = 0; u < 2; ++u)
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      s[rt][u] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[u][0], qf[rt][0], f32x16_t{}, 0, 0,
-                                                                  0, 0, 0, 0);
-      s[rt][u] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[u][1], qf[rt][1], s[rt][u], 0, 0,
-                                                                  0, 0, 0, 0);
+      S.v[rt][u] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[u][0], qf[rt][0], f32x16_t{}, 0,
+                                                                    0, 0, 0, 0, 0);
+      S.v[rt][u] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[u][1], qf[rt][1], S.v[rt][u], 0,
+                                                                    0, 0, 0, 0, 0);
     }
 }
 
@@ -385,20 +441,17 @@ __device__ __forceinline__ int pack_e4m3x4(float a, float b, float c, float d) {
   return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
 }
 
-// One fp8 step of 64 kept keys key0 .. key0+63 for the RT row tiles of the
-// wave: S^T for all tiles, then per tile the softmax (diag: causal mask
-// against pos) and O^T += V^T P~^T with P~ = e4m3(2^8 exp(x - m)), so that
-// the softmax of one tile runs on the vector ALUs while the matrix cores work
-// on the other tile. The row sums of P~ come from the matrix cores as well:
+// Finish an fp8 step of 64 kept keys key0 .. key0+63 from its scores: per
+// row tile the softmax (diag: causal mask against pos) and
+// O^T += V^T P~^T with P~ = e4m3(2^8 exp(x - m)); the softmax of one tile
+// runs on the vector ALUs while the matrix cores work on the other tile. The row sums of P~ come from the matrix cores as well:
 // an all-ones A operand (e4m3 1.0 = 0x38) times P~^T puts sum_k P~[row][k]
 // in every element of the lane's column.
 template <int RT>
-__device__ __forceinline__ void step_fp8(const uint4* st, const i32x8_t (&qf)[RT][2],
-                                         RowState<RT>& rs, float cs, int key0,
-                                         const int (&pos)[RT], bool diag, int lane) {
+__device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState<RT>& rs, float cs,
+                                        int key0, const int (&pos)[RT], bool diag, int lane) {
   const int half = lane >> 5;
-  f32x16_t s[RT][2];
-  qk_fp8<RT>(st, qf, s, lane);
+  auto& s = S.v;
   i32x8_t va[4];
   vread_fp8(st, va, lane);
   const int one = 0x38383838;
@@ -435,7 +488,22 @@ __device__ __forceinline__ void step_fp8(const uint4* st, const i32x8_t (&qf)[RT
   }
 }
 
-template <int FP8, int W, int RT>
+// Steps 0 .. n-1 of a ring, with (PIPE) or without the cross-step overlap.
+template <int W, int FP8, int PIPE, int RT, class Offs, class QK, class Fin>
+__device__ __forceinline__ void run_steps(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
+                                          Offs offs, QK qk, Fin fin, int tid) {
+  if constexpr (PIPE) {
+    pipe_loop<W, FP8, Scores<RT>>(ring, n, Kb, Vb, offs, qk, fin, tid);
+  } else {
+    ring_loop<W, FP8>(ring, n, Kb, Vb, offs, [&](const uint4* st, int s) {
+      Scores<RT> S;
+      qk(st, S);
+      fin(st, S, s);
+    }, tid);
+  }
+}
+
+template <int FP8, int W, int RT, int PIPE>
 __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled pooled,
                                                            const uint8_t* __restrict__ mask,
                                                            KeptLists kl,
@@ -447,6 +515,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
   __shared__ int32_t s_item;
 
   constexpr int M = 32 * RT * W;            // packed rows per work item
+  constexpr int NPRE = W > 4 ? 2 : 4;       // V^T key groups read ahead of the softmax
   const int wpu = p0.g * kBlock / M;        // work items per unit
   const int nbh = p0.batch * p0.hkv;
   const int nitems = p0.nbmax * nbh * wpu;
@@ -603,14 +672,22 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
         const int nst = 2 * nbc;
         const int ndiag = (c0 == 0 && has_diag) ? 2 : 0;   // the diagonal block comes first
         if constexpr (FP8) {
-          ring_loop<W, 1>(ring, nst, K, V, offs, [&](const uint4* st, int s) {
-            step_fp8<RT>(st, qf, rs, cs, I * kBlock + kStep * (s & 1), pos, s < ndiag, lane);
-          }, tid);
+          run_steps<W, 1, PIPE, RT>(
+              ring, nst, K, V, offs,
+              [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
+              [&](const uint4* st, Scores<RT>& S, int s) {
+                fin_fp8<RT>(st, S, rs, cs, I * kBlock + kStep * (s & 1), pos, s < ndiag, lane);
+              },
+              tid);
         } else {
-          ring_loop<W, 0>(ring, nst, K, V, offs, [&](const uint4* st, int s) {
-            step_bf16<0, RT>(st, qb, rs, cs, off, 1.f, I * kBlock + kStep * (s & 1), pos, s < ndiag,
-                             0, lane);
-          }, tid);
+          run_steps<W, 0, PIPE, RT>(
+              ring, nst, K, V, offs,
+              [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
+              [&](const uint4* st, Scores<RT>& S, int s) {
+                fin_bf16<0, RT, NPRE>(st, S, rs, cs, off, 1.f, I * kBlock + kStep * (s & 1), pos,
+                                      s < ndiag, 0, lane);
+              },
+              tid);
         }
       }
     }
@@ -685,9 +762,14 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
           const int i = min(kStep * s + r, np - 1);       // past the list: repeat a valid entry
           return (int64_t)plist[i] * kHeadDim * 2;
         };
-        ring_loop<W, 0>(ring, (np + kStep - 1) / kStep, Kh, Vh, offs, [&](const uint4* st, int s) {
-          step_bf16<1, RT>(st, qb, rs, cs, off, pv_scale, 0, pos, false, np - kStep * s, lane);
-        }, tid);
+        run_steps<W, 0, PIPE, RT>(
+            ring, (np + kStep - 1) / kStep, Kh, Vh, offs,
+            [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
+            [&](const uint4* st, Scores<RT>& S, int s) {
+              fin_bf16<1, RT, NPRE>(st, S, rs, cs, off, pv_scale, 0, pos, false, np - kStep * s,
+                                    lane);
+            },
+            tid);
       }
     }
 
@@ -728,14 +810,14 @@ int device_cus() {
   return cus[dev];
 }
 
-template <int FP8, int W, int RT>
+template <int FP8, int W, int RT, int PIPE>
 hipError_t launch_cfg(const Problem& p, const Pooled& pooled, const uint8_t* mask,
                       const KeptLists& kl, void* out, float* lse, hipStream_t s) {
   const int64_t nitems = (int64_t)p.nbmax * p.batch * p.hkv * (p.g * kBlock / (32 * RT * W));
   const int cus = device_cus();
   if (cus <= 0) return hipErrorInvalidDevice;
   const unsigned grid = (unsigned)std::min<int64_t>(nitems, cus);
-  attend_kernel<FP8, W, RT><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, (uint16_t*)out, lse);
+  attend_kernel<FP8, W, RT, PIPE><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, (uint16_t*)out, lse);
   return hipSuccess;
 }
 
@@ -744,8 +826,8 @@ hipError_t launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask
                      const KeptLists& kl, void* out, float* lse, hipStream_t s) {
   // 32 query rows per wave; 8 waves (two per SIMD) when the unit has at
   // least 256 packed rows, else 4
-  if (p.g == 1) return launch_cfg<FP8, 4, 1>(p, pooled, mask, kl, out, lse, s);
-  return launch_cfg<FP8, 8, 1>(p, pooled, mask, kl, out, lse, s);
+  if (p.g == 1) return launch_cfg<FP8, 4, 1, ATT_PIPE>(p, pooled, mask, kl, out, lse, s);
+  return launch_cfg<FP8, ATT_W, 1, ATT_PIPE>(p, pooled, mask, kl, out, lse, s);
 }
 
 }  // namespace

@@ -1,10 +1,11 @@
 // Fused block scoring, max-based thresholding and kept-list compaction
 // (Sec. 3.1 Eq. (1)-(2), Eq. fused_score, Eq. select; Algorithm 1 steps 3-5).
 //
-// One workgroup (8 waves) per (sequence b, KV head h, query block I), heaviest
-// (largest I) first. The query rows of block I are the g*B packed rows of
-// Eq. packgqa (position I*B + r/g, head h*g + r%g). They stream through LDS in
-// 32-row tiles; each wave keeps up to four 32-wide chunks of pooled keys khat
+// A persistent grid (one 8-wave workgroup per compute unit) deals the units
+// (sequence b, KV head h, query block I) round-robin, heaviest (largest I)
+// first. The query rows of block I are the g*B packed rows of Eq. packgqa
+// (position I*B + r/g, head h*g + r%g). They stream through two LDS buffers
+// in 32-row tiles, the global loads running two tiles ahead; each wave keeps up to four 32-wide chunks of pooled keys khat
 // in registers (the MFMA B operand) and computes S = Q khat^T with
 // v_mfma_f32_32x32x16_bf16 (fp32 accumulation). Lane l of the accumulator
 // owns key block J = chunk + l%32 and 16 query rows, so the row sum of
@@ -21,6 +22,8 @@
 // Precision: fp8 queries are widened to bf16 exactly, the per-head fp8 scale
 // is applied in fp32 after the MFMA, and exponentials use the hardware
 // v_exp_f32; block energies match the fp64 definition to ~1e-6 relative.
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace fp2 {
@@ -33,31 +36,48 @@ constexpr int kChunksPerWave = 4;                          // 4 x 32 key blocks 
 constexpr int kGroup = kWaves * kChunksPerWave * 32;       // key blocks per pass (1024)
 
 template <int FP8, int G>
-__global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p, Pooled pooled,
+__global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled pooled,
                                                             uint8_t* __restrict__ mask,
                                                             KeptLists kl) {
   extern __shared__ float ell[];            // [nbmax] block log2-energies of this row
-  __shared__ uint4 qt[32 * 16];             // Q tile: 32 rows x 16 chunks of 8 bf16
+  __shared__ uint4 qt[2][32 * 16];          // Q tiles (double buffer): 32 rows x 16 chunks of 8 bf16
   __shared__ float redf[kWaves];
   __shared__ int redi[kWaves];
 
-  const int nbh = p.batch * p.hkv;
-  const int I = p.nbmax - 1 - (int)(blockIdx.x / nbh);
-  const int bh = blockIdx.x % nbh;
+  const int nbh = p0.batch * p0.hkv;
+  const int nitems = p0.nbmax * nbh;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *kl.queue = 0;
+
+  // Persistent workgroups, items dealt round-robin in order of decreasing
+  // query block: the cost of an item is proportional to (I + 1), so every
+  // workgroup gets an almost equal share.
+#pragma unroll 1
+  for (int item = blockIdx.x; item < nitems; item += gridDim.x) {
+  // Opaque copies of the thread index and of the argument block (the first
+  // kernel argument, at offset 0 of the argument segment): values derived
+  // from them are recomputed per item instead of living across the loop.
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  typedef const __attribute__((address_space(4))) Problem KProblem;
+  KProblem* pk = (KProblem*)__builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(pk));
+  KProblem& p = *pk;
+
+  const int I = p.nbmax - 1 - item / nbh;
+  const int bh = item % nbh;
   const int b = bh / p.hkv, h = bh % p.hkv;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lane = tid & 63, w = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
   const int64_t tok0 = p.cu[b];
   const int L = p.cu[b + 1] - (int)tok0;
   const int n = (L + kBlock - 1) / kBlock;
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
   uint8_t* mrow = mask + row * p.nbmax;
-  if (blockIdx.x == 0 && tid == 0) *kl.queue = 0;
 
   if (I >= n) {
     for (int J = tid; J < p.nbmax; J += kThreads) mrow[J] = 0;
     if (tid == 0) kl.cnt[row] = 0;
-    return;
+    continue;
   }
 
   const int npos = min(kBlock, L - I * kBlock);
@@ -73,6 +93,40 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p, Pooled po
   }
 
   const uint16_t* khat = pooled.khat + ((int64_t)b * p.hkv + h) * p.nbmax * kHeadDim;
+
+  // This thread's 16 bytes of Q tile t (bf16: row tid/16, chunk tid%16;
+  // fp8: threads < 256, row tid/8, 16 codes tid%8), zero past the block.
+  auto qload = [&](int t) -> uint4 {
+    uint4 v = make_uint4(0, 0, 0, 0);
+    const int r = FP8 ? tid >> 3 : tid >> 4;
+    const int pr = t * 32 + r;
+    if (t < ntiles && pr < nrows && (!FP8 || tid < 256)) {
+      const int pos = I * kBlock + pr / G, hq = h * G + pr % G;
+      if (FP8)
+        v = *(const uint4*)((const uint8_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + (tid & 7) * 16);
+      else
+        v = *(const uint4*)((const uint16_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + (tid & 15) * 8);
+    }
+    return v;
+  };
+  // Store it into LDS buffer qb (fp8 codes widened to bf16, exact).
+  auto qstore = [&](uint4* qb, uint4 v) {
+    if (!FP8) {
+      const int r = tid >> 4, c = tid & 15;
+      qb[r * 16 + (c ^ (r & 15))] = v;
+    } else if (tid < 256) {
+      const int r = tid >> 3, c8 = tid & 7;
+      uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+      uint32_t o[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        uint32_t src = wv[i >> 1] >> (16 * (i & 1));
+        o[i] = e4m3_to_bf16(src & 0xFF) | (e4m3_to_bf16((src >> 8) & 0xFF) << 16);
+      }
+      qb[r * 16 + ((2 * c8) ^ (r & 15))] = make_uint4(o[0], o[1], o[2], o[3]);
+      qb[r * 16 + ((2 * c8 + 1) ^ (r & 15))] = make_uint4(o[4], o[5], o[6], o[7]);
+    }
+  };
 
   for (int grp = 0; grp <= I; grp += kGroup) {
     bf16x8_t kf[kChunksPerWave][8];
@@ -93,42 +147,20 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p, Pooled po
       }
     }
 
+    // Q tiles stream through two LDS buffers; the global loads of tile t+2
+    // are in flight while tile t is scored.
+    uint4 qa_next = qload(0), qa_next2 = qload(1);
     for (int t = 0; t < ntiles; ++t) {
-      __syncthreads();
-      if (!FP8) {
-        const int r = tid >> 4, c = tid & 15;
-        const int pr = t * 32 + r;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (pr < nrows) {
-          const int pos = I * kBlock + pr / G, hq = h * G + pr % G;
-          v = *(const uint4*)((const uint16_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + c * 8);
-        }
-        qt[r * 16 + (c ^ (r & 15))] = v;
-      } else if (tid < 256) {
-        const int r = tid >> 3, c8 = tid & 7;
-        const int pr = t * 32 + r;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (pr < nrows) {
-          const int pos = I * kBlock + pr / G, hq = h * G + pr % G;
-          v = *(const uint4*)((const uint8_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + c8 * 16);
-        }
-        uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-        uint32_t o[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          uint32_t src = wv[i >> 1] >> (16 * (i & 1));
-          o[i] = e4m3_to_bf16(src & 0xFF) | (e4m3_to_bf16((src >> 8) & 0xFF) << 16);
-        }
-        qt[r * 16 + ((2 * c8) ^ (r & 15))] = make_uint4(o[0], o[1], o[2], o[3]);
-        qt[r * 16 + ((2 * c8 + 1) ^ (r & 15))] = make_uint4(o[4], o[5], o[6], o[7]);
-      }
-      __syncthreads();
+      qstore(qt[t & 1], qa_next);
+      __syncthreads();   // tile t visible; every wave is done with tile t-1
+      qa_next = qa_next2;
+      qa_next2 = qload(t + 2);
+      const uint4* qb = qt[t & 1];
 
       bf16x8_t qa[8];
 #pragma unroll
       for (int ds = 0; ds < 8; ++ds)
-        qa[ds] = __builtin_bit_cast(bf16x8_t, qt[l32 * 16 + ((2 * ds + half) ^ (l32 & 15))]);
-
+        qa[ds] = __builtin_bit_cast(bf16x8_t, qb[l32 * 16 + ((2 * ds + half) ^ (l32 & 15))]);
       // validity of this lane's 16 rows (only the last tile can be partial)
       const int rbase = t * 32 + 4 * half;
       const bool full = t * 32 + 32 <= nrows;
@@ -181,8 +213,8 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p, Pooled po
       const int J = grp + 32 * (w + kWaves * c) + l32;
       if (half == 0 && J <= I) ell[J] = M + fast_log2(e1 + e2);
     }
+    __syncthreads();   // every wave is done with the Q tile buffers and ell of this group
   }
-  __syncthreads();
 
   // ---- selection: max-based threshold plus forced blocks (Eq. select)
   float mu = -INFINITY;
@@ -221,6 +253,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p, Pooled po
     }
   }
   if (tid == 0) kl.cnt[row] = base;
+  }
 }
 
 // Kept lists from a caller-given mask (bit 0), ascending; one workgroup per row.
@@ -263,10 +296,25 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
   if (tid == 0) kl.cnt[row] = base;
 }
 
+// Compute units of the current device (one resident workgroup each).
+int est_device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
 template <int FP8>
 hipError_t launch_est_dt(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
                          hipStream_t s) {
-  const unsigned grid = (unsigned)p.nbmax * p.batch * p.hkv;
+  const int cus = est_device_cus();
+  if (cus <= 0) return hipErrorInvalidDevice;
+  const unsigned grid = (unsigned)std::min<int64_t>((int64_t)p.nbmax * p.batch * p.hkv, cus);
   const size_t smem = (size_t)p.nbmax * sizeof(float);
   switch (p.g) {
     case 1: estimate_kernel<FP8, 1><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
