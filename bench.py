@@ -9,8 +9,11 @@ per-head scales, threshold calibrated to ~5% kept blocks, correction on.
 
 Prints ONE JSON line with the dense-equivalent throughput, the latency, the
 kept-block ratio, a roofline entry for the attention kernel (the dominant
-kernel), the oracle timed on the host cores on a bounded sample, and the
-other 128K variants (kept ratio, correction off, bf16, GQA 8:1).
+kernel), and the oracle timed on the host cores on a bounded sample;
+--variants adds the other 128K variants (kept ratio, correction off, bf16,
+GQA 8:1). The roofline's HBM traffic comes from the committed rocprofv3
+counter summary of the attention kernel, and only while the kernel sources
+are the ones the counters were taken on (else null).
 """
 from __future__ import annotations
 
@@ -24,6 +27,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "128K prefill attn latency + dense-equiv TFLOP/s (bf16/fp8); kept-block ratio"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attend_kernel_llama128k_fp8_pmc.txt")
+KERNEL_SOURCES = ["paper_2608_19758_amd/csrc/attend.hip", "paper_2608_19758_amd/csrc/kernels.h",
+                  "paper_2608_19758_amd/csrc/common.h"]
 PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}
 PEAK_HBM_GBS = 8000.0
 
@@ -35,13 +41,59 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama128k_fp8")
     ap.add_argument("--target", default="0.05", help="kept-ratio target the alpha was calibrated for")
-    ap.add_argument("--no-variants", action="store_true")
+    ap.add_argument("--variants", action="store_true",
+                    help="also measure the other 128K variants (not part of the headline line)")
+    ap.add_argument("--no-variants", action="store_true", help="(default; kept for old scripts)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=64,
                     help="(sequence, KV head, query block) units the oracle runs for the CPU baseline")
     ap.add_argument("--profile-only", action="store_true",
                     help="only run the timed loop of the default workload (for rocprofv3)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 256 MiB device copy three times (scales the "
+                         "FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
+
+
+def kernel_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def committed_traffic():
+    """HBM bytes per attention launch from the committed counter summary:
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) times the factors a plain
+    copy of known size gives; None if the summary is missing or was taken on
+    other kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
+    except OSError:
+        return None
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("source_sha256") != kernel_sources_sha256():
+        return None
+    try:
+        return (float(kv["fetch_kib_per_dispatch"]) * 1024 * float(kv["fetch_scale"])
+                + float(kv["write_kib_per_dispatch"]) * 1024 * float(kv["write_scale"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration():
+    import torch
+    n = 256 << 20
+    x = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n, "copies": 3}), flush=True)
 
 
 def setup(name, target, correction=None):
@@ -172,12 +224,15 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on exactly one GPU: this operator build has no multi-GPU path "
-              "(sharding by KV head is described in DESIGN.md); got --gpus %d, WORLD_SIZE %d"
+              "(the path would shard by KV head); got --gpus %d, WORLD_SIZE %d"
               % (args.gpus, world), file=sys.stderr)
         sys.exit(2)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
 
+    if args.copy_calibration:
+        copy_calibration()
+        return
     cfg = setup(args.workload, args.target)
     if args.profile_only:
         t, _ = time_loop(cfg["run_prefill"], args.steps, args.warmup)
@@ -194,7 +249,7 @@ def main():
         print("[bench] cpu baseline: %s" % cpu["sample"], file=sys.stderr, flush=True)
 
     variants = []
-    if not args.no_variants:
+    if args.variants:
         vlist = [("llama128k_fp8", "0.10", None), ("llama128k_fp8", "0.02", None),
                  ("llama128k_fp8", "0.05", 0), ("llama128k_bf16", "0.05", None),
                  ("wide128k_bf16", "0.009", None), ("wide128k_fp8", "0.009", None)]
@@ -218,6 +273,7 @@ def main():
             torch.cuda.empty_cache()
 
     att = m["attention"]
+    traffic = committed_traffic() if (args.workload, args.target) == ("llama128k_fp8", "0.05") else None
     line = {
         "metric": METRIC,
         "value": round(m["dense_tflops"], 3),
@@ -244,13 +300,16 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "attend_kernel",
                      "achieved": round(att["achieved_tflops"], 2),
                      "peak": round(att["peak_tflops"], 1), "unit": "TFLOP/s",
-                     "frac": round(att["frac"], 4), "traffic": None},
+                     "frac": round(att["frac"], 4),
+                     "traffic": None if traffic is None else round(traffic / 1e9, 3),
+                     "traffic_unit": "GB per launch"},
         "estimation": {"hbm_gbs": round(m["estimation"]["gbs"], 1),
                        "hbm_frac": round(m["estimation"]["hbm_frac"], 4)},
         "cpu_baseline": None if cpu is None else {k: (round(v, 6) if isinstance(v, float) else v)
                                                   for k, v in cpu.items() if k != "seconds"},
-        "variants": variants,
     }
+    if variants:
+        line["variants"] = variants
     print(json.dumps(line), flush=True)
 
 

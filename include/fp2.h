@@ -68,6 +68,12 @@
  * |B_J| * exp(scale * q . kbar_J) * vbar_J to the softmax numerator and
  * |B_J| * exp(scale * q . kbar_J) to its denominator (Sec. 3.2 Eq.
  * correction); kbar/vbar are the block means (stored in bf16 on the GPU).
+ *
+ * fp8 (Sec. 3.3 Eq. fp8): scores are c_q c_k (q~ . k~) from the e4m3 codes;
+ * the probabilities of kept keys are rounded to e4m3 as P~ = e4m3(2^8 *
+ * exp(S - m)) before the value product, and the softmax denominator sums
+ * those rounded P~ (so out is a convex combination of values); the 2^8 is
+ * removed from lse. Scales must be positive and finite.
  */
 #ifndef FP2_H
 #define FP2_H
@@ -112,7 +118,8 @@ typedef struct {
 
 /* Bytes of workspace the entry points need for `params` (0 for a null or
  * invalid params). Covers the pooled key/value means, the kept-block lists
- * and their counts. */
+ * and their counts, and the work counter of the attention kernel (reset by
+ * the call itself, so a workspace can be reused without clearing). */
 size_t fp2_workspace_bytes(const fp2_params_t* params);
 
 /* Full prefill (Algorithm 1 of Sec. 3.4): block means, fused scoring and
@@ -141,11 +148,12 @@ fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32
 
 /* The attention stage alone (Sec. 3.2 Eq. correction, Sec. 3.3; Algorithm 1
  * steps 6-11) under a caller-given mask: bit 0 of block_mask_in[b][h][I][J]
- * selects key block J for query block I (entries with J > I are ignored;
- * the diagonal J == I must be selected for every valid block I, else
- * FP2_EINVAL is not detected and rows whose keys are all excluded produce
- * undefined values). Recomputes the block means and the kept lists from the
- * mask in the workspace. Arguments as for fp2_prefill. */
+ * selects key block J for query block I (entries with J > I are ignored).
+ * The caller should select the diagonal J == I of every valid block I: the
+ * mask is not checked, and a row whose keys are all excluded (no selected
+ * key at or before its position and no corrected block) gets an undefined
+ * output. Recomputes the block means and the kept lists from the mask in
+ * the workspace. Arguments as for fp2_prefill. */
 fp2_status_t fp2_attend(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
                         const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
                         const int32_t* block_table, const float* q_scale, const float* k_scale,

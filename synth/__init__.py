@@ -340,7 +340,7 @@ def generate(spec: Spec) -> Workload:
 # ---------------------------------------------------------------------------
 
 def named(name: str, seed: int = 0) -> Spec:
-    """Named workload specs (see the design doc for the recipe)."""
+    """Named workload specs: the synthetic layers the tests and the benchmark run."""
     if name == "tiny2k":
         return Spec(name, [2048], 4, 1, dtype="bf16", page_size=0, salient_frac=0.0,
                     salient_min=3, sink_blocks=1, window_blocks=1, seed=seed)
