@@ -165,39 +165,52 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       const int rbase = t * 32 + 4 * half;
       const bool full = t * 32 + 32 <= nrows;
 
-#pragma unroll
-      for (int c = 0; c < kChunksPerWave; ++c) {
-        if (!act[c]) continue;
+      // Scores of chunk c (the other wave of the SIMD runs its vector work
+      // while these MFMAs execute).
+      auto score = [&](int c) -> f32x16_t {
         f32x16_t acc = {};
 #pragma unroll
         for (int ds = 0; ds < 8; ++ds)
           acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[ds], kf[c][ds], acc, 0, 0, 0);
-        float mx = -INFINITY;
+        return acc;
+      };
+      // Fold one chunk's scores into its running (m, E): rows of head
+      // offset j carry the scale cs[j] (> 0), so the maximum of cs * s is
+      // taken per j on the raw scores. Rows past the block (last tile only)
+      // are set to -inf first: they add exp2(-inf) = 0.
+      auto fold = [&](int c, f32x16_t& acc) {
+        if (!full) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float g = -INFINITY;
+          for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            bool ok = full || (rbase + 8 * i + j < nrows);
-            g = ok ? fmaxf(g, acc[4 * i + j]) : g;
-          }
-          mx = fmaxf(mx, g * cs[j]);
+            for (int j = 0; j < 4; ++j)
+              acc[4 * i + j] = rbase + 8 * i + j < nrows ? acc[4 * i + j] : -INFINITY;
         }
+        float g[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          g[j] = fmaxf(fmaxf(acc[j], acc[4 + j]), fmaxf(acc[8 + j], acc[12 + j])) * cs[j];
+        const float mx = fmaxf(fmaxf(g[0], g[1]), fmaxf(g[2], g[3]));
         const float mn = fmaxf(m[c], mx);
         if (mn > m[c]) {
           E[c] *= fast_exp2(m[c] - mn);
           m[c] = mn;
         }
-        float s = 0.f;
+        const float nb = mn == -INFINITY ? 0.f : -mn;   // no valid row yet: every term is 0
+        float s4[4];                                    // four independent partial sums
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) s4[j] = fast_exp2(fmaf(acc[j], cs[j], nb));
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            bool ok = full || (rbase + 8 * i + j < nrows);
-            float e = fast_exp2(fmaf(acc[4 * i + j], cs[j], -mn));
-            s += ok ? e : 0.f;
-          }
-        E[c] += s;
+        for (int i = 1; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) s4[j] += fast_exp2(fmaf(acc[4 * i + j], cs[j], nb));
+        E[c] += (s4[0] + s4[1]) + (s4[2] + s4[3]);
+      };
+#pragma unroll
+      for (int c = 0; c < kChunksPerWave; ++c) {
+        if (!act[c]) continue;
+        f32x16_t acc = score(c);
+        fold(c, acc);
       }
     }
 
