@@ -40,6 +40,7 @@
 // dtypes), logits shifted by log2|B_J| = 7 (Sec. 3.2 implementation
 // paragraph).
 #include <algorithm>
+#include <utility>
 
 #include "kernels.h"
 
@@ -50,10 +51,8 @@ namespace {
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kStep = 64;            // keys per pipeline step
 constexpr int kRingU4 = 8192;        // LDS ring: 128 KiB in 16-byte slots
-constexpr int kJtab = 1024;          // kept blocks per table chunk
-constexpr int kTab = 2048;           // page-table entries per table chunk
-constexpr int kAuxI32 = kJtab + kTab;          // 12 KiB of tables
-constexpr int kPlist = 2 * kAuxI32;            // pruned blocks per correction chunk (u16)
+constexpr int kRec = 768;            // copy-address records per chunk of kept blocks (12 KiB)
+constexpr int kPlist = 8 * kRec;     // pruned blocks per correction chunk (u16, same 12 KiB)
 #ifndef ATT_W
 #define ATT_W 8
 #endif
@@ -147,33 +146,56 @@ __device__ __forceinline__ void issue_copies(uint4* st, const uint8_t* Kb, const
   }
 }
 
-// Ring over steps 0 .. n-1 without cross-step overlap of the compute:
-// offs(s, r) gives the byte offset of row r of step s, body(stage, s)
-// consumes step s. Ends with a barrier (the ring may be refilled).
-template <int W, int FP8, class Offs, class Body>
-__device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
-                                          Offs offs, Body body, int tid) {
+// Copy addresses of a step come in two parts: fetch(s, r) reads the table
+// entry of row r of step s from LDS, addr(entry, s, r) turns it into the byte
+// offset. The entries of the next step are fetched at the end of a step and
+// converted after the next barrier, so their LDS latency is never waited on.
+template <int W, int FP8, class Fetch, class Addr>
+struct Addresser {
   using P = Plan<W, FP8>;
-  int64_t nxt[P::PER];
-  auto load = [&](int s) {
+  using Raw = decltype(std::declval<Fetch>()(0, 0));
+  Fetch fetch;
+  Addr addr;
+  int tid;
+  Raw raw[P::PER];
+  int64_t off[P::PER];
+  __device__ __forceinline__ void get(int s) {
 #pragma unroll
-    for (int j = 0; j < P::PER; ++j) nxt[j] = offs(s, P::row(j, tid));
-  };
+    for (int j = 0; j < P::PER; ++j) raw[j] = fetch(s, P::row(j, tid));
+  }
+  __device__ __forceinline__ void convert(int s) {
+#pragma unroll
+    for (int j = 0; j < P::PER; ++j) off[j] = addr(raw[j], s, P::row(j, tid));
+  }
+};
+
+// Ring over steps 0 .. n-1 without cross-step overlap of the compute;
+// body(stage, s) consumes step s. Ends with a barrier (the ring may be
+// refilled).
+template <int W, int FP8, class Fetch, class Addr, class Body>
+__device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
+                                          Fetch fetch, Addr addr, Body body, int tid) {
+  using P = Plan<W, FP8>;
+  Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
   int ni = 0;
 #pragma unroll 1
   for (; ni < P::NST - 1 && ni < n; ++ni) {
-    load(ni);
-    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, nxt, tid);
+    ad.get(ni);
+    ad.convert(ni);
+    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, ad.off, tid);
   }
-  if (ni < n) load(ni);
+  if (ni < n) ad.get(ni);
 #pragma unroll 1
   for (int s = 0; s < n; ++s) {
     wait_ahead<P::D>(ni - 1 - s);
     lds_barrier();   // step s visible to all; every wave is done with step s-1
     const bool more = ni < n;
-    if (more) issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, nxt, tid);
+    if (more) {
+      ad.convert(ni);
+      issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, ad.off, tid);
+    }
     body(ring + (s % P::NST) * P::STAGE, s);
-    if (more && ni < n) load(ni);   // table reads overlap the matrix cores
+    if (more && ni < n) ad.get(ni);
   }
   lds_barrier();
 }
@@ -182,23 +204,20 @@ __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb,
 // cores before the rest of step s runs: qk(stage, S) starts the score MFMAs
 // of a step, fin(stage, S, s) finishes step s from its scores. The vector
 // work of step s then overlaps the MFMAs of step s+1 within the wave.
-template <int W, int FP8, class SC, class Offs, class QK, class Fin>
+template <int W, int FP8, class SC, class Fetch, class Addr, class QK, class Fin>
 __device__ __forceinline__ void pipe_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
-                                          Offs offs, QK qk, Fin fin, int tid) {
+                                          Fetch fetch, Addr addr, QK qk, Fin fin, int tid) {
   using P = Plan<W, FP8>;
   static_assert(P::NST >= 3, "the ring holds steps s-1 (refill), s and s+1");
-  int64_t nxt[P::PER];
-  auto load = [&](int s) {
-#pragma unroll
-    for (int j = 0; j < P::PER; ++j) nxt[j] = offs(s, P::row(j, tid));
-  };
+  Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
   int ni = 0;
 #pragma unroll 1
   for (; ni < P::NST - 1 && ni < n; ++ni) {
-    load(ni);
-    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, nxt, tid);
+    ad.get(ni);
+    ad.convert(ni);
+    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, ad.off, tid);
   }
-  if (ni < n) load(ni);
+  if (ni < n) ad.get(ni);
   wait_ahead<P::D>(ni - 1);
   lds_barrier();   // step 0 visible to all
   SC sc, sn;
@@ -208,10 +227,13 @@ __device__ __forceinline__ void pipe_loop(uint4* ring, int n, const uint8_t* Kb,
     if (s + 1 < n) wait_ahead<P::D>(ni - 2 - s);
     lds_barrier();   // step s+1 visible; every wave is done with step s-1
     const bool more = ni < n;
-    if (more) issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, nxt, tid);
+    if (more) {
+      ad.convert(ni);
+      issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, ad.off, tid);
+    }
     if (s + 1 < n) qk(ring + ((s + 1) % P::NST) * P::STAGE, sn);
     fin(ring + (s % P::NST) * P::STAGE, sc, s);
-    if (more && ni < n) load(ni);
+    if (more && ni < n) ad.get(ni);
     sc = sn;
   }
   lds_barrier();
@@ -489,13 +511,13 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
 }
 
 // Steps 0 .. n-1 of a ring, with (PIPE) or without the cross-step overlap.
-template <int W, int FP8, int PIPE, int RT, class Offs, class QK, class Fin>
+template <int W, int FP8, int PIPE, int RT, class Fetch, class Addr, class QK, class Fin>
 __device__ __forceinline__ void run_steps(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
-                                          Offs offs, QK qk, Fin fin, int tid) {
+                                          Fetch fetch, Addr addr, QK qk, Fin fin, int tid) {
   if constexpr (PIPE) {
-    pipe_loop<W, FP8, Scores<RT>>(ring, n, Kb, Vb, offs, qk, fin, tid);
+    pipe_loop<W, FP8, Scores<RT>>(ring, n, Kb, Vb, fetch, addr, qk, fin, tid);
   } else {
-    ring_loop<W, FP8>(ring, n, Kb, Vb, offs, [&](const uint4* st, int s) {
+    ring_loop<W, FP8>(ring, n, Kb, Vb, fetch, addr, [&](const uint4* st, int s) {
       Scores<RT> S;
       qk(st, S);
       fin(st, S, s);
@@ -510,7 +532,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
                                                            uint16_t* __restrict__ out,
                                                            float* __restrict__ lse) {
   __shared__ uint4 ring[kRingU4];
-  __shared__ int32_t aux[kAuxI32];          // kept: block list + page entries; correction: pruned list
+  __shared__ uint4 aux[kRec];               // kept: copy-address records; correction: pruned list
   __shared__ int32_t wtot[W];
   __shared__ int32_t s_item;
 
@@ -588,8 +610,6 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     asm volatile("" : "+v"(qsc), "+v"(vsc), "+v"(ksc));  // loads complete before the rings
 
     using PK = Plan<W, FP8>;
-    int32_t* jtab = aux;
-    int32_t* tab = aux + kJtab;
 
     // ---- kept blocks: step s of a chunk -> its block list entry s/2, half s%2
     {
@@ -602,11 +622,18 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       const int64_t rowbytes = (int64_t)p.hkv * kHeadDim * esz;     // one token slot of the pool
       const int64_t hbytes = (int64_t)h * kHeadDim * esz;
       const int page = p.pm.page, shift = p.pm.shift;
-      // page-table entries per block: the pages that block J's 128 tokens touch
-      const int epb = page == 0 ? 0 : shift >= 0 ? (page >= kBlock ? 1 : kBlock / page)
-                                                 : (kBlock - 1 + page - 1) / page + 1;
-      const int chunk = epb == 0 ? kJtab : min(kJtab, kTab / epb);
+      // Copy-address records: rows of a 64-key half come in groups of G that
+      // lie in one page (G = 64 contiguous, min(p, 64) for a power-of-two
+      // page, 1 otherwise); one record per (kept block, half, group).
+      const int gshift = page == 0 ? 6 : shift >= 0 ? min(shift, 6) : 0;
+      const int rph = kStep >> gshift;       // records per half
+      const int chunk = kRec / (2 * rph);    // kept blocks per table chunk
       const int32_t* ptab = p.pm.table + (int64_t)b * p.pm.stride;
+      auto slot_of = [&](int t) -> uint32_t {
+        if (page == 0) return (uint32_t)(tok0 + t);
+        const int pi = shift >= 0 ? t >> shift : t / page;
+        return (uint32_t)ptab[pi] * (uint32_t)page + (uint32_t)(t - pi * page);
+      };
 
       i32x8_t qf[FP8 ? RT : 1][2];
       bf16x8_t qb[FP8 ? 1 : RT][8];
@@ -641,39 +668,37 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
 #pragma unroll 1
       for (int c0 = 0; c0 < cnt; c0 += chunk) {
         const int nbc = min(chunk, cnt - c0);
-        // tables of this chunk: block index, and the page-table entries of the
-        // pages it touches (entries past the sequence are never read)
-        for (int i = tid; i < nbc; i += 64 * W) jtab[i] = kidx[cnt - 1 - (c0 + i)];
-        for (int t = tid; t < nbc * epb; t += 64 * W) {
-          const int i = t / epb, e = t - i * epb;
-          const int jb = kidx[cnt - 1 - (c0 + i)] * kBlock;
-          const int pi = (shift >= 0 ? jb >> shift : jb / page) + e;
-          tab[t] = (int64_t)pi * page < L ? ptab[pi] : 0;
+        // Record (block i, half hf, group e) = {slot of its first row, that
+        // row's index in the half, last valid row index}: row r of the half
+        // then lives at slot + min(r, last) - first. Rows past the sequence
+        // thus repeat its last token (finite data; those keys are masked); a
+        // group that starts past it points at that token directly.
+        for (int k = tid; k < nbc * 2 * rph; k += 64 * W) {
+          const int i = k / (2 * rph), hk = k - i * 2 * rph;
+          const int key0 = kidx[cnt - 1 - (c0 + i)] * kBlock + kStep * (hk >= rph);
+          const int last = L - 1 - key0;
+          int first = (hk % rph) << gshift;
+          uint32_t slot;
+          if (first <= last) {
+            slot = slot_of(key0 + first);
+          } else {
+            slot = slot_of(L - 1);
+            first = last;
+          }
+          aux[k] = make_uint4(slot, (uint32_t)first, (uint32_t)last, 0u);
         }
         __syncthreads();
-        // byte offset of row r of step s: rows past the sequence repeat its
-        // last token (finite data; those keys are masked)
-        auto offs = [&](int s, int r) -> int64_t {
-          const int i = s >> 1;
-          const int jb = jtab[i] * kBlock;
-          const int t = min(jb + kStep * (s & 1) + r, L - 1);
-          int64_t slot;
-          if (page == 0) {
-            slot = tok0 + t;
-          } else if (shift >= 0) {
-            const int e = (t >> shift) - (jb >> shift);
-            slot = (int64_t)tab[i * epb + e] * page + (t & (page - 1));
-          } else {
-            const int pi = t / page;
-            slot = (int64_t)tab[i * epb + pi - jb / page] * page + (t - pi * page);
-          }
-          return slot * rowbytes + hbytes;
+        auto fetch = [&](int s, int r) -> uint4 { return aux[(s * rph) + (r >> gshift)]; };
+        auto addr = [&](uint4 rec, int s, int r) -> int64_t {
+          (void)s;
+          const int64_t sl = (int64_t)rec.x + (min(r, (int)rec.z) - (int)rec.y);
+          return sl * rowbytes + hbytes;
         };
         const int nst = 2 * nbc;
         const int ndiag = (c0 == 0 && has_diag) ? 2 : 0;   // the diagonal block comes first
         if constexpr (FP8) {
           run_steps<W, 1, PIPE, RT>(
-              ring, nst, K, V, offs,
+              ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
                 fin_fp8<RT>(st, S, rs, cs, I * kBlock + kStep * (s & 1), pos, s < ndiag, lane);
@@ -681,7 +706,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
               tid);
         } else {
           run_steps<W, 0, PIPE, RT>(
-              ring, nst, K, V, offs,
+              ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
                 fin_bf16<0, RT, NPRE>(st, S, rs, cs, off, 1.f, I * kBlock + kStep * (s & 1), pos,
@@ -758,12 +783,15 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
           __syncthreads();
         }
         if (np == 0) continue;
-        auto offs = [&](int s, int r) -> int64_t {
-          const int i = min(kStep * s + r, np - 1);       // past the list: repeat a valid entry
-          return (int64_t)plist[i] * kHeadDim * 2;
+        // past the list: repeat a valid entry
+        auto fetch = [&](int s, int r) -> int { return plist[min(kStep * s + r, np - 1)]; };
+        auto addr = [&](int J, int s, int r) -> int64_t {
+          (void)s;
+          (void)r;
+          return (int64_t)J * kHeadDim * 2;
         };
         run_steps<W, 0, PIPE, RT>(
-            ring, (np + kStep - 1) / kStep, Kh, Vh, offs,
+            ring, (np + kStep - 1) / kStep, Kh, Vh, fetch, addr,
             [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
             [&](const uint4* st, Scores<RT>& S, int s) {
               fin_bf16<1, RT, NPRE>(st, S, rs, cs, off, pv_scale, 0, pos, false, np - kStep * s,
