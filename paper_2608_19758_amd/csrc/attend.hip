@@ -148,8 +148,9 @@ __device__ __forceinline__ void issue_copies(uint4* st, const uint8_t* Kb, const
 
 // Copy addresses of a step come in two parts: fetch(s, r) reads the table
 // entry of row r of step s from LDS, addr(entry, s, r) turns it into the byte
-// offset. The entries of the next step are fetched at the end of a step and
-// converted after the next barrier, so their LDS latency is never waited on.
+// offset. The entries of the next step are fetched before a step is computed
+// and converted after the next barrier, so their LDS latency is never waited
+// on.
 template <int W, int FP8, class Fetch, class Addr>
 struct Addresser {
   using P = Plan<W, FP8>;
@@ -189,13 +190,12 @@ __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb,
   for (int s = 0; s < n; ++s) {
     wait_ahead<P::D>(ni - 1 - s);
     lds_barrier();   // step s visible to all; every wave is done with step s-1
-    const bool more = ni < n;
-    if (more) {
+    if (ni < n) {
       ad.convert(ni);
       issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, ad.off, tid);
+      if (ni < n) ad.get(ni);   // lands while the step is computed
     }
     body(ring + (s % P::NST) * P::STAGE, s);
-    if (more && ni < n) ad.get(ni);
   }
   lds_barrier();
 }
@@ -458,8 +458,12 @@ __device__ __forceinline__ void vread_fp8(const uint4* st, i32x8_t (&va)[4], int
 }
 
 // Four e4m3 codes (round to nearest even) of four non-negative floats <= 448.
+// The first conversion writes the low half-word and the second the high one,
+// so the register's previous contents never matter (no zeroing move).
 __device__ __forceinline__ int pack_e4m3x4(float a, float b, float c, float d) {
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  int w;
+  asm volatile("" : "=v"(w));
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, w, false);
   return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
 }
 
@@ -471,13 +475,12 @@ __device__ __forceinline__ int pack_e4m3x4(float a, float b, float c, float d) {
 // in every element of the lane's column.
 template <int RT>
 __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState<RT>& rs, float cs,
-                                        int key0, const int (&pos)[RT], bool diag, int lane) {
+                                        int key0, const int (&pos)[RT], bool diag, int lane,
+                                        const i32x8_t& ones) {
   const int half = lane >> 5;
   auto& s = S.v;
   i32x8_t va[4];
   vread_fp8(st, va, lane);
-  const int one = 0x38383838;
-  const i32x8_t ones = {one, one, one, one, one, one, one, one};
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     if (diag) {
@@ -510,11 +513,59 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
   }
 }
 
-// Steps 0 .. n-1 of a ring, with (PIPE) or without the cross-step overlap.
+// Ring over steps 0 .. n-1 with the two waves of each SIMD half a step
+// apart: waves 0 .. W/2-1 run qk(s) then fin(s); waves W/2 .. W-1 run
+// fin(s-1), whose scores they started in the previous step, then qk(s). On
+// every SIMD one wave then works on the vector ALUs while the other keeps the
+// matrix cores busy. Step s-1 is still read in step s, so the ring refills the
+// stage of step s-2.
+template <int W, int FP8, class SC, class Fetch, class Addr, class QK, class Fin>
+__device__ __forceinline__ void pingpong_loop(uint4* ring, int n, const uint8_t* Kb,
+                                              const uint8_t* Vb, Fetch fetch, Addr addr, QK qk,
+                                              Fin fin, int tid) {
+  using P = Plan<W, FP8>;
+  static_assert(P::NST >= 3, "the ring holds steps s-2 (refill), s-1 and s");
+  Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
+  const bool late = (tid >> 6) >= W / 2;
+  int ni = 0;
+#pragma unroll 1
+  for (; ni < P::NST - 2 && ni < n; ++ni) {
+    ad.get(ni);
+    ad.convert(ni);
+    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, ad.off, tid);
+  }
+  if (ni < n) ad.get(ni);
+  SC sc;
+#pragma unroll 1
+  for (int s = 0; s < n; ++s) {
+    wait_ahead<P::D>(ni - 1 - s);
+    lds_barrier();   // step s visible; every wave is done with step s-2
+    const bool more = ni < n;
+    if (more) {
+      ad.convert(ni);
+      issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, ad.off, tid);
+    }
+    if (!late) {
+      qk(ring + (s % P::NST) * P::STAGE, sc);
+      fin(ring + (s % P::NST) * P::STAGE, sc, s);
+    } else {
+      if (s > 0) fin(ring + ((s - 1) % P::NST) * P::STAGE, sc, s - 1);
+      qk(ring + (s % P::NST) * P::STAGE, sc);
+    }
+    if (more && ni < n) ad.get(ni);
+  }
+  if (late && n > 0) fin(ring + ((n - 1) % P::NST) * P::STAGE, sc, n - 1);
+  lds_barrier();
+}
+
+// Steps 0 .. n-1 of a ring: PIPE 0 plain, 1 cross-step overlap within a
+// wave, 2 ping-pong between the two waves of a SIMD.
 template <int W, int FP8, int PIPE, int RT, class Fetch, class Addr, class QK, class Fin>
 __device__ __forceinline__ void run_steps(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
                                           Fetch fetch, Addr addr, QK qk, Fin fin, int tid) {
-  if constexpr (PIPE) {
+  if constexpr (PIPE == 2) {
+    pingpong_loop<W, FP8, Scores<RT>>(ring, n, Kb, Vb, fetch, addr, qk, fin, tid);
+  } else if constexpr (PIPE == 1) {
     pipe_loop<W, FP8, Scores<RT>>(ring, n, Kb, Vb, fetch, addr, qk, fin, tid);
   } else {
     ring_loop<W, FP8>(ring, n, Kb, Vb, fetch, addr, [&](const uint4* st, int s) {
@@ -697,11 +748,18 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
         const int nst = 2 * nbc;
         const int ndiag = (c0 == 0 && has_diag) ? 2 : 0;   // the diagonal block comes first
         if constexpr (FP8) {
+          // all-ones A operand of the row-sum MFMA (e4m3 1.0 = 0x38), opaque so
+          // that it stays in registers instead of being rebuilt every step
+          i32x8_t ones;
+#pragma unroll
+          for (int k = 0; k < 8; ++k) ones[k] = 0x38383838;
+          asm volatile("" : "+v"(ones));
           run_steps<W, 1, PIPE, RT>(
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
-                fin_fp8<RT>(st, S, rs, cs, I * kBlock + kStep * (s & 1), pos, s < ndiag, lane);
+                fin_fp8<RT>(st, S, rs, cs, I * kBlock + kStep * (s & 1), pos, s < ndiag, lane,
+                            ones);
               },
               tid);
         } else {
@@ -854,7 +912,7 @@ hipError_t launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask
                      const KeptLists& kl, void* out, float* lse, hipStream_t s) {
   // 32 query rows per wave; 8 waves (two per SIMD) when the unit has at
   // least 256 packed rows, else 4
-  if (p.g == 1) return launch_cfg<FP8, 4, 1, ATT_PIPE>(p, pooled, mask, kl, out, lse, s);
+  if (p.g == 1) return launch_cfg<FP8, 4, 1, 0>(p, pooled, mask, kl, out, lse, s);
   return launch_cfg<FP8, ATT_W, 1, ATT_PIPE>(p, pooled, mask, kl, out, lse, s);
 }
 
