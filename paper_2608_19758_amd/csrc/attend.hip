@@ -339,6 +339,8 @@ __device__ __forceinline__ void fin_bf16(const uint4* st, Scores<RT>& S, RowStat
                                          float off, float pv_scale, int key0, const int (&pos)[RT],
                                          bool diag, int nv, int lane) {
   const int half = lane >> 5;
+  const float lg_pv = KIND == 1 ? fast_log2(pv_scale) : 0.f;
+  const float inv_pv = KIND == 1 ? 1.f / pv_scale : 1.f;
   // V^T fragment of key group kg (16 keys) and output tile dt: slot i' of
   // lane half H is key 16kg + 8(i'/4) + 4H + i'%4.
   const int g16 = lane >> 4, i16 = lane & 15;
@@ -380,23 +382,25 @@ __device__ __forceinline__ void fin_bf16(const uint4* st, Scores<RT>& S, RowStat
             S.v[rt][u][4 * i + j] = drop ? -INFINITY : S.v[rt][u][4 * i + j];
           }
     }
-    const float bias = softmax_rescale<2, false>(S.v[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off);
+    // KIND 1: the PV weight pv_scale (> 0) enters the exponent as log2
+    // pv_scale, and the row sum divides it out once.
+    const float bias = softmax_rescale<2, false>(S.v[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off) +
+                       (KIND == 1 ? lg_pv : 0.f);
     float pv[2][16];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int e = 0; e < 16; ++e) pv[u][e] = fast_exp2(fmaf(S.v[rt][u][e], cs, bias));
-    rs.l[rt] += sum16(pv[0]) + sum16(pv[1]);
+    const float psum = sum16(pv[0]) + sum16(pv[1]);
+    rs.l[rt] += KIND == 1 ? psum * inv_pv : psum;
     // O^T += V^T P^T, 16 keys per MFMA; B operand of key group kg = 2u + a:
     // slot i' of lane half H is S[u][8a + i']
 #pragma unroll
     for (int kg = 0; kg < 4; ++kg) {
       uint32_t pw[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float x0 = pv[kg >> 1][8 * (kg & 1) + 2 * q], x1 = pv[kg >> 1][8 * (kg & 1) + 2 * q + 1];
-        pw[q] = KIND == 1 ? pack_bf16x2(x0 * pv_scale, x1 * pv_scale) : pack_bf16x2(x0, x1);
-      }
+      for (int q = 0; q < 4; ++q)
+        pw[q] = pack_bf16x2(pv[kg >> 1][8 * (kg & 1) + 2 * q], pv[kg >> 1][8 * (kg & 1) + 2 * q + 1]);
       const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
