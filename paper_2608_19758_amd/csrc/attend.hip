@@ -368,9 +368,12 @@ __device__ __forceinline__ void fin_bf16(const uint4* st, Scores<RT>& S, RowStat
 
   // key of S[rt][u][4i+j] is 32u + 8i + 4*half + j. Per tile: softmax, then
   // its PV MFMAs, which run while the next tile's softmax is computed.
+  // only the diagonal step (kept keys) or the last step of the list
+  // (correction) has columns to drop
+  const bool masked = KIND == 1 ? nv < kStep : diag;
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
-    if (KIND == 1 || diag) {
+    if (masked) {
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
