@@ -176,6 +176,7 @@ def measure(cfg, steps, warmup):
     achieved = (fk + fc) / (t_attn * 1e-3) / 1e12
     est_bytes = acc.estimation_bytes(sp.seqlens, sp.num_q_heads, sp.num_kv_heads,
                                      elem=1 if sp.dtype == "fp8" else 2)
+    sflop = acc.scoring_flops(sp.seqlens, sp.num_q_heads)   # bf16 MFMA (scoring key in bf16)
     return dict(
         ms_per_step=t_pre, wall_ms_per_step=wall, estimate_ms=t_est, attention_ms=t_attn,
         dense_tflops=dense / (t_pre * 1e-3) / 1e12, kept_ratio=kept_ratio,
@@ -183,7 +184,9 @@ def measure(cfg, steps, warmup):
                        achieved_tflops=achieved, peak_tflops=peak, frac=achieved / peak),
         estimation=dict(alg_bytes=est_bytes, gbs=est_bytes / (t_est * 1e-3) / 1e9,
                         hbm_frac=est_bytes / (t_est * 1e-3) / 1e9 / PEAK_HBM_GBS,
-                        scoring_tflop=acc.scoring_flops(sp.seqlens, sp.num_q_heads) / 1e12),
+                        scoring_tflop=sflop / 1e12,
+                        mfma_frac=sflop / (t_est * 1e-3) / 1e12 / PEAK_TFLOPS["bf16"],
+                        exps_per_s=sflop / (2 * sp.head_dim) / (t_est * 1e-3)),
     )
 
 
@@ -303,8 +306,14 @@ def main():
                      "frac": round(att["frac"], 4),
                      "traffic": None if traffic is None else round(traffic / 1e9, 3),
                      "traffic_unit": "GB per launch"},
-        "estimation": {"hbm_gbs": round(m["estimation"]["gbs"], 1),
-                       "hbm_frac": round(m["estimation"]["hbm_frac"], 4)},
+        # the index stage (pooling + scoring + selection): its HBM fraction, and
+        # the fractions of the resources that bind it at 128K (bf16 MFMA for
+        # the scores, one exponential per (query row, pooled key))
+        "estimation": {"ms": round(m["estimate_ms"], 4),
+                       "hbm_gbs": round(m["estimation"]["gbs"], 1),
+                       "hbm_frac": round(m["estimation"]["hbm_frac"], 4),
+                       "scoring_mfma_frac": round(m["estimation"]["mfma_frac"], 4),
+                       "exps_per_s": float("%.4g" % m["estimation"]["exps_per_s"])},
         "cpu_baseline": None if cpu is None else {k: (round(v, 6) if isinstance(v, float) else v)
                                                   for k, v in cpu.items() if k != "seconds"},
     }

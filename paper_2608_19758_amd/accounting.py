@@ -42,14 +42,16 @@ def attention_flops(mask, seqlens, num_q_heads, num_kv_heads, head_dim=128, bloc
 
 def estimation_bytes(seqlens, num_q_heads, num_kv_heads, head_dim=128, block_size=128, elem=2):
     """Algorithmic bytes of the index stage: Q, K, V read once; pooled means
-    (bf16) written and re-read once; mask bytes and kept lists written."""
+    (bf16) written and re-read once; the mask rows and the int32 kept lists
+    (bounded by every causal block) written."""
     tot = 0.0
     for L in seqlens:
         n = (L + block_size - 1) // block_size
         tot += L * num_q_heads * head_dim * elem                 # Q
         tot += 2 * L * num_kv_heads * head_dim * elem            # K, V
         tot += 2 * 2 * n * num_kv_heads * head_dim * 2           # khat, vbar write + read
-        tot += num_kv_heads * n * n * (1 + 2)                    # mask bytes + int16 list
+        tot += num_kv_heads * n * n                              # mask rows
+        tot += num_kv_heads * n * (n + 1) // 2 * 4               # kept lists (upper bound)
     return tot
 
 
