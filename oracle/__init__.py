@@ -45,6 +45,7 @@ class Params(ctypes.Structure):
         ("recent_blocks", ctypes.c_int32), ("mean_correction", ctypes.c_int32),
         ("softmax_scale", ctypes.c_double),
         ("dtype", ctypes.c_int32), ("nthreads", ctypes.c_int32),
+        ("max_kv_len", ctypes.c_int32),
     ]
 
 
@@ -63,8 +64,8 @@ def _load():
         lib.oracle_e4m3_decode.argtypes = [ctypes.c_uint8]
         P = ctypes.POINTER(Params)
         lib.oracle_pool.argtypes = [P] + [vp] * 9
-        lib.oracle_estimate.argtypes = [P] + [vp] * 8 + [vp, ctypes.c_int, vp, vp, vp]
-        lib.oracle_attend.argtypes = [P] + [vp] * 8 + [vp, vp, ctypes.c_int, vp, vp]
+        lib.oracle_estimate.argtypes = [P] + [vp] * 9 + [vp, ctypes.c_int, vp, vp, vp]
+        lib.oracle_attend.argtypes = [P] + [vp] * 9 + [vp, vp, ctypes.c_int, vp, vp]
         for f in (lib.oracle_pool, lib.oracle_estimate, lib.oracle_attend):
             f.restype = ctypes.c_int
         _lib = lib
@@ -108,6 +109,7 @@ class Inputs:
         self.v = np.ascontiguousarray(v)
         self.bt = np.ascontiguousarray(bt, dtype=np.int32)
         self.cu = np.ascontiguousarray(wl.cu_seqlens, dtype=np.int32)
+        self.cu_k = np.ascontiguousarray(wl.cu_seqlens_k, dtype=np.int32)
         self.qs = np.ascontiguousarray(wl.q_scale, dtype=np.float32)
         self.ks = np.ascontiguousarray(wl.k_scale, dtype=np.float32)
         self.vs = np.ascontiguousarray(wl.v_scale, dtype=np.float32)
@@ -126,16 +128,24 @@ class Inputs:
             mean_correction=sp.mean_correction if correction is None else int(correction),
             softmax_scale=float(softmax_scale),
             dtype=1 if sp.dtype == "fp8" else 0,
-            nthreads=nthreads_default() if nthreads is None else nthreads)
+            nthreads=nthreads_default() if nthreads is None else nthreads,
+            max_kv_len=sp.max_kv_len)
 
     @property
     def nbmax(self):
+        """Query blocks (mask rows)."""
         sp = self.spec
         return (sp.max_seq_len + sp.block_size - 1) // sp.block_size
 
+    @property
+    def nbk(self):
+        """Key blocks (mask columns, pooled rows)."""
+        sp = self.spec
+        return (sp.max_kv_len + sp.block_size - 1) // sp.block_size
+
     def _args(self):
-        return [_ptr(self.q), _ptr(self.cu), _ptr(self.k), _ptr(self.v), _ptr(self.bt),
-                _ptr(self.qs), _ptr(self.ks), _ptr(self.vs)]
+        return [_ptr(self.q), _ptr(self.cu), _ptr(self.cu_k), _ptr(self.k), _ptr(self.v),
+                _ptr(self.bt), _ptr(self.qs), _ptr(self.ks), _ptr(self.vs)]
 
 
 def _units_arr(units):
@@ -148,25 +158,25 @@ def _units_arr(units):
 def pool(inp: Inputs, p: Params):
     """Block means kbar, vbar (fp64) and the bf16 scoring key bits khat."""
     sp = inp.spec
-    shape = (sp.batch, sp.num_kv_heads, max(1, inp.nbmax), sp.head_dim)
+    shape = (sp.batch, sp.num_kv_heads, max(1, inp.nbk), sp.head_dim)
     kbar = np.zeros(shape, np.float64)
     vbar = np.zeros(shape, np.float64)
     khat = np.zeros(shape, np.uint16)
     rc = _load().oracle_pool(ctypes.byref(p), _ptr(inp.k), _ptr(inp.v), _ptr(inp.bt),
-                             _ptr(inp.cu), _ptr(inp.ks), _ptr(inp.vs), _ptr(kbar), _ptr(vbar),
+                             _ptr(inp.cu_k), _ptr(inp.ks), _ptr(inp.vs), _ptr(kbar), _ptr(vbar),
                              _ptr(khat))
     assert rc == 0
     return kbar, vbar, khat
 
 
 def estimate(inp: Inputs, p: Params, units=None, want_scores=False):
-    """Mask [b, Hkv, nb, nb] (uint8: bit0 kept, bit1 forced) and optionally
-    ell [b, Hkv, nb, nb] (block log-energies, NaN above the diagonal) and
-    mu [b, Hkv, nb] (row maxima)."""
+    """Mask [b, Hkv, nbq, nbk] (uint8: bit0 kept, bit1 forced) and optionally
+    ell [b, Hkv, nbq, nbk] (block log-energies, NaN past the diagonal) and
+    mu [b, Hkv, nbq] (row maxima). Without a prefix nbq == nbk."""
     sp = inp.spec
-    nb = max(1, inp.nbmax)
-    mask = np.zeros((sp.batch, sp.num_kv_heads, nb, nb), np.uint8)
-    ell = np.full((sp.batch, sp.num_kv_heads, nb, nb), np.nan) if want_scores else None
+    nb, nk = max(1, inp.nbmax), max(1, inp.nbk)
+    mask = np.zeros((sp.batch, sp.num_kv_heads, nb, nk), np.uint8)
+    ell = np.full((sp.batch, sp.num_kv_heads, nb, nk), np.nan) if want_scores else None
     mu = np.full((sp.batch, sp.num_kv_heads, nb), np.nan) if want_scores else None
     u, nu = _units_arr(units)
     rc = _load().oracle_estimate(ctypes.byref(p), *inp._args(), _ptr(u), nu, _ptr(mask),
@@ -195,12 +205,14 @@ def margins(ell, mu, alpha):
     return np.expm1(ell - np.log(alpha) - mu[..., None])
 
 
-def kept_ratio(mask, seqlens, block_size):
-    """Kept blocks over block-causal pairs (J <= I), over all (b, h)."""
+def kept_ratio(mask, seqlens, block_size, prefix=None):
+    """Kept blocks over block-causal pairs (J <= absolute query block), over
+    all (b, h)."""
     kept = 0
     tot = 0
     for b, L in enumerate(seqlens):
         n = (L + block_size - 1) // block_size
-        kept += int((mask[b, :, :n, :n] & 1).sum())
-        tot += mask.shape[1] * n * (n + 1) // 2
+        off = 0 if prefix is None else prefix[b] // block_size
+        kept += int((mask[b, :, :n, :] & 1).sum())
+        tot += mask.shape[1] * sum(off + I + 1 for I in range(n))
     return kept / max(1, tot)

@@ -10,7 +10,15 @@
  * T_J = [J*B, min((J+1)*B, L))), per KV head h (group size g = Hq/Hkv) and
  * scale = softmax_scale (1/sqrt(d) by default):
  *
- *  1. Gather k_t, v_t (t < L) through the page table:
+ * Prefix KV (chunked prefill): a sequence may hold L_kv >= L keys, of which
+ * the L queries are the last ones (query i sits at absolute position
+ * P0 + i, P0 = L_kv - L, a multiple of B). Key blocks are then those of the
+ * L_kv keys, query block I sits at absolute block Ia = I + P0/B, and every
+ * "J <= I" / "J == I" / "J < I" / "t <= p" below reads with Ia and absolute
+ * positions; without a prefix P0 = 0 and Ia = I (Sec. 3.3 Eq. page, the
+ * request's KV length; Sec. 4 chunked prefill).
+ *
+ *  1. Gather k_t, v_t (t < L_kv) through the page table:
  *     slot(b, t) = page_table[b][t / p] * p + t mod p            (Sec. 3.3, Eq. page)
  *  2. Block means kbar_J, vbar_J over T_J in exact fp64          (Sec. 3.2, the
  *     pooled statistics beside Eq. correction).
@@ -53,6 +61,7 @@ typedef struct {
   double softmax_scale;     /* <= 0: 1/sqrt(head_dim) */
   int32_t dtype;            /* 0: bf16, 1: fp8 e4m3fn */
   int32_t nthreads;         /* <= 0: 1 */
+  int32_t max_kv_len;       /* bound of the KV lengths (<= 0: max_seq_len) */
 } oracle_params;
 
 /* ---------------- codecs ---------------- */
@@ -105,16 +114,18 @@ double oracle_e4m3_decode(uint8_t bits) {
 typedef struct {
   const oracle_params* P;
   const void* q;
-  const int32_t* cu;
+  const int32_t* cu;        /* query tokens per sequence */
+  const int32_t* cuk;       /* KV tokens per sequence (== cu without a prefix) */
   const void* k;
   const void* v;
   const int32_t* bt;
   const float* qs;
   const float* ks;
   const float* vs;
-  int g, d, B, nbmax;
+  int g, d, B, nbmax;       /* nbmax: query blocks (mask rows) */
+  int nbk;                  /* key blocks (mask columns, pooled rows) */
   double scale;
-  /* pooled statistics [b][Hkv][nbmax][d] */
+  /* pooled statistics [b][Hkv][nbk][d] */
   double* kbar;
   double* vbar;
   double* khat;
@@ -124,9 +135,9 @@ typedef struct {
   int next;                 /* atomic cursor */
   pthread_mutex_t lock;
   /* outputs / inputs of the stages */
-  uint8_t* mask;            /* [b][Hkv][nbmax][nbmax] */
+  uint8_t* mask;            /* [b][Hkv][nbmax][nbk] */
   const uint8_t* mask_in;
-  double* ell;              /* [b][Hkv][nbmax][nbmax], may be NULL */
+  double* ell;              /* [b][Hkv][nbmax][nbk], may be NULL */
   double* mu;               /* [b][Hkv][nbmax], may be NULL */
   double* out;              /* [total][Hq][d] */
   double* lse;              /* [total][Hq], may be NULL */
@@ -141,7 +152,7 @@ static double elem(const ctx_t* c, const void* base, size_t idx, double scale) {
 /* pool slot of token t of sequence b (Sec. 3.3, Eq. page) */
 static size_t slot_of(const ctx_t* c, int b, int t) {
   int p = c->P->page_size;
-  if (p == 0) return (size_t)c->cu[b] + (size_t)t;
+  if (p == 0) return (size_t)c->cuk[b] + (size_t)t;
   int page = c->bt[(size_t)b * c->P->max_pages_per_seq + t / p];
   return (size_t)page * p + (size_t)(t % p);
 }
@@ -166,15 +177,18 @@ static double dot(const double* a, const double* b, int d) {
 }
 
 static int seq_len(const ctx_t* c, int b) { return c->cu[b + 1] - c->cu[b]; }
+static int kv_len(const ctx_t* c, int b) { return c->cuk[b + 1] - c->cuk[b]; }
+/* absolute position of query 0 of sequence b */
+static int prefix_of(const ctx_t* c, int b) { return kv_len(c, b) - seq_len(c, b); }
 
 static size_t pool_index(const ctx_t* c, int b, int h, int J) {
-  return (((size_t)b * c->P->num_kv_heads + h) * c->nbmax + J) * c->d;
+  return (((size_t)b * c->P->num_kv_heads + h) * c->nbk + J) * c->d;
 }
 
 /* ---------------- step 2: block means ---------------- */
 
 static void pool_bh(ctx_t* c, int b, int h) {
-  int L = seq_len(c, b), d = c->d, B = c->B;
+  int L = kv_len(c, b), d = c->d, B = c->B;
   int n = (L + B - 1) / B;
   double* tmp = malloc(sizeof(double) * d);
   for (int J = 0; J < n; ++J) {
@@ -211,15 +225,17 @@ static void estimate_unit(ctx_t* c, int b, int h, int I) {
   int L = seq_len(c, b), d = c->d, B = c->B, g = c->g;
   int n = (L + B - 1) / B;
   if (I >= n) return;
+  int nk = (kv_len(c, b) + B - 1) / B;
+  int Ia = I + prefix_of(c, b) / B;          /* absolute query block */
   int p0 = I * B, p1 = p0 + B < L ? p0 + B : L;
   int rows = (p1 - p0) * g;
   double* qrows = malloc(sizeof(double) * (size_t)rows * d);
   double* x = malloc(sizeof(double) * rows);
-  double* ell = malloc(sizeof(double) * (I + 1));
+  double* ell = malloc(sizeof(double) * (Ia + 1));
   for (int p = p0; p < p1; ++p)
     for (int j = 0; j < g; ++j) load_q(c, b, p, h * g + j, qrows + ((size_t)(p - p0) * g + j) * d);
   double mu = -INFINITY;
-  for (int J = 0; J <= I; ++J) {
+  for (int J = 0; J <= Ia; ++J) {
     const double* kh = c->khat + pool_index(c, b, h, J);
     double m = -INFINITY;
     for (int r = 0; r < rows; ++r) {
@@ -231,13 +247,13 @@ static void estimate_unit(ctx_t* c, int b, int h, int I) {
     ell[J] = m + log(s);
     if (ell[J] > mu) mu = ell[J];
   }
-  size_t row = (((size_t)b * P->num_kv_heads + h) * c->nbmax + I) * c->nbmax;
+  size_t row = (((size_t)b * P->num_kv_heads + h) * c->nbmax + I) * c->nbk;
   double la = P->alpha > 0 ? log(P->alpha) : 0.0;
-  for (int J = 0; J < c->nbmax; ++J) {
+  for (int J = 0; J < c->nbk; ++J) {
     uint8_t byte = 0;
-    if (J <= I) {
+    if (J <= Ia) {
       int thr = P->alpha == 0.0 ? 1 : (ell[J] >= la + mu);
-      int f = forced_block(c, n, I, J);
+      int f = forced_block(c, nk, Ia, J);
       byte = (uint8_t)((thr || f) | (f << 1));
       if (c->ell) c->ell[row + J] = ell[J];
     } else if (c->ell) {
@@ -255,20 +271,22 @@ static void estimate_unit(ctx_t* c, int b, int h, int I) {
 
 static void attend_unit(ctx_t* c, int b, int h, int I) {
   const oracle_params* P = c->P;
-  int L = seq_len(c, b), d = c->d, B = c->B, g = c->g;
-  int n = (L + B - 1) / B;
+  int Lq = seq_len(c, b), d = c->d, B = c->B, g = c->g;
+  int n = (Lq + B - 1) / B;
   if (I >= n) return;
-  const uint8_t* mrow = c->mask_in + (((size_t)b * P->num_kv_heads + h) * c->nbmax + I) * c->nbmax;
-  int p0 = I * B, p1 = p0 + B < L ? p0 + B : L;
+  int L = kv_len(c, b), P0 = prefix_of(c, b);
+  int Ia = I + P0 / B;                       /* absolute query block */
+  const uint8_t* mrow = c->mask_in + (((size_t)b * P->num_kv_heads + h) * c->nbmax + I) * c->nbk;
+  int p0 = I * B, p1 = p0 + B < Lq ? p0 + B : Lq;
   /* keys of the kept blocks, gathered once per unit */
   int nkeys = 0;
-  for (int J = 0; J <= I; ++J)
+  for (int J = 0; J <= Ia; ++J)
     if (mrow[J] & 1) nkeys += (J * B + B < L ? B : L - J * B);
   int* kt = malloc(sizeof(int) * (nkeys + 1));
   double* kk = malloc(sizeof(double) * ((size_t)nkeys + 1) * d);
   double* vv = malloc(sizeof(double) * ((size_t)nkeys + 1) * d);
   int idx = 0;
-  for (int J = 0; J <= I; ++J) {
+  for (int J = 0; J <= Ia; ++J) {
     if (!(mrow[J] & 1)) continue;
     int t1 = J * B + B < L ? J * B + B : L;
     for (int t = J * B; t < t1; ++t, ++idx) {
@@ -277,11 +295,11 @@ static void attend_unit(ctx_t* c, int b, int h, int I) {
       load_kv(c, c->v, c->vs, b, h, t, vv + (size_t)idx * d);
     }
   }
-  /* corrected blocks: J < I, not kept */
+  /* corrected blocks: J < Ia, not kept */
   int ncorr = 0;
-  int* cj = malloc(sizeof(int) * (I + 1));
+  int* cj = malloc(sizeof(int) * (Ia + 1));
   if (P->mean_correction)
-    for (int J = 0; J < I; ++J)
+    for (int J = 0; J < Ia; ++J)
       if (!(mrow[J] & 1)) cj[ncorr++] = J;
   double* q = malloc(sizeof(double) * d);
   double* lg = malloc(sizeof(double) * ((size_t)nkeys + ncorr + 1));
@@ -292,7 +310,7 @@ static void attend_unit(ctx_t* c, int b, int h, int I) {
       load_q(c, b, p, hq, q);
       double m = -INFINITY;
       for (int i = 0; i < nkeys; ++i) {
-        lg[i] = kt[i] <= p ? c->scale * dot(q, kk + (size_t)i * d, d) : -INFINITY;
+        lg[i] = kt[i] <= P0 + p ? c->scale * dot(q, kk + (size_t)i * d, d) : -INFINITY;
         if (lg[i] > m) m = lg[i];
       }
       for (int i = 0; i < ncorr; ++i) {
@@ -350,20 +368,27 @@ static void run_units(ctx_t* c, unit_fn fn) {
 
 static void pool_worker_fn(ctx_t* c, int b, int h, int unused) { (void)unused; pool_bh(c, b, h); }
 
-static int setup(ctx_t* c, const oracle_params* P, const void* q, const int32_t* cu, const void* k,
-                 const void* v, const int32_t* bt, const float* qs, const float* ks, const float* vs) {
+static int setup(ctx_t* c, const oracle_params* P, const void* q, const int32_t* cu,
+                 const int32_t* cuk, const void* k, const void* v, const int32_t* bt,
+                 const float* qs, const float* ks, const float* vs) {
   memset(c, 0, sizeof(*c));
   if (P->head_dim <= 0 || P->block_size <= 0 || P->num_kv_heads <= 0 ||
       P->num_q_heads % P->num_kv_heads != 0 || P->batch < 0)
     return 1;
-  c->P = P; c->q = q; c->cu = cu; c->k = k; c->v = v; c->bt = bt;
+  c->P = P; c->q = q; c->cu = cu; c->cuk = cuk ? cuk : cu; c->k = k; c->v = v; c->bt = bt;
+  for (int b = 0; b < P->batch; ++b) {       /* block-aligned prefixes only */
+    int pre = c->cuk[b + 1] - c->cuk[b] - (c->cu ? c->cu[b + 1] - c->cu[b] : 0);
+    if (c->cu && (pre < 0 || pre % P->block_size != 0)) return 1;
+  }
   c->qs = qs; c->ks = ks; c->vs = vs;
   c->g = P->num_q_heads / P->num_kv_heads;
   c->d = P->head_dim;
   c->B = P->block_size;
   c->nbmax = (P->max_seq_len + P->block_size - 1) / P->block_size;
+  int maxkv = P->max_kv_len > 0 ? P->max_kv_len : P->max_seq_len;
+  c->nbk = (maxkv + P->block_size - 1) / P->block_size;
   c->scale = P->softmax_scale > 0 ? P->softmax_scale : 1.0 / sqrt((double)P->head_dim);
-  size_t np = (size_t)P->batch * P->num_kv_heads * (c->nbmax > 0 ? c->nbmax : 1) * c->d;
+  size_t np = (size_t)P->batch * P->num_kv_heads * (c->nbk > 0 ? c->nbk : 1) * c->d;
   c->kbar = calloc(np, sizeof(double));
   c->vbar = calloc(np, sizeof(double));
   c->khat = calloc(np, sizeof(double));
@@ -410,14 +435,15 @@ static int32_t* all_units(const ctx_t* c, int* count) {
 
 /* ---------------- entry points ---------------- */
 
-/* Block means: kbar, vbar (fp64) and the bf16 scoring key khat (bit patterns),
- * each [batch][Hkv][nbmax][d]; blocks beyond a sequence stay zero. */
+/* Block means of the KV tokens (cuk: KV lengths): kbar, vbar (fp64) and the
+ * bf16 scoring key khat (bit patterns), each [batch][Hkv][nbk][d]; blocks
+ * beyond a sequence stay zero. */
 int oracle_pool(const oracle_params* P, const void* k, const void* v, const int32_t* bt,
-                const int32_t* cu, const float* ks, const float* vs, double* kbar, double* vbar,
+                const int32_t* cuk, const float* ks, const float* vs, double* kbar, double* vbar,
                 uint16_t* khat_bits) {
   ctx_t c;
-  if (setup(&c, P, NULL, cu, k, v, bt, NULL, ks, vs)) return 1;
-  size_t np = (size_t)P->batch * P->num_kv_heads * c.nbmax * c.d;
+  if (setup(&c, P, NULL, NULL, cuk, k, v, bt, NULL, ks, vs)) return 1;
+  size_t np = (size_t)P->batch * P->num_kv_heads * c.nbk * c.d;
   if (kbar) memcpy(kbar, c.kbar, np * sizeof(double));
   if (vbar) memcpy(vbar, c.vbar, np * sizeof(double));
   if (khat_bits)
@@ -428,12 +454,12 @@ int oracle_pool(const oracle_params* P, const void* k, const void* v, const int3
 
 /* Steps 1-5 for the given units (NULL: all). Writes mask rows of those units;
  * ell/mu (optional) receive the block scores and row maxima. */
-int oracle_estimate(const oracle_params* P, const void* q, const int32_t* cu, const void* k,
-                    const void* v, const int32_t* bt, const float* qs, const float* ks,
-                    const float* vs, const int32_t* units, int nunits, uint8_t* mask, double* ell,
-                    double* mu) {
+int oracle_estimate(const oracle_params* P, const void* q, const int32_t* cu, const int32_t* cuk,
+                    const void* k, const void* v, const int32_t* bt, const float* qs,
+                    const float* ks, const float* vs, const int32_t* units, int nunits,
+                    uint8_t* mask, double* ell, double* mu) {
   ctx_t c;
-  if (setup(&c, P, q, cu, k, v, bt, qs, ks, vs)) return 1;
+  if (setup(&c, P, q, cu, cuk, k, v, bt, qs, ks, vs)) return 1;
   int32_t* own = NULL;
   if (!units) units = own = all_units(&c, &nunits);
   c.units = units; c.nunits = nunits;
@@ -446,12 +472,12 @@ int oracle_estimate(const oracle_params* P, const void* q, const int32_t* cu, co
 
 /* Step 6 for the given units under an external mask (bit 0 = kept). Writes the
  * fp64 output rows [total][Hq][d] and LSE [total][Hq] of those units. */
-int oracle_attend(const oracle_params* P, const void* q, const int32_t* cu, const void* k,
-                  const void* v, const int32_t* bt, const float* qs, const float* ks,
-                  const float* vs, const uint8_t* mask_in, const int32_t* units, int nunits,
-                  double* out, double* lse) {
+int oracle_attend(const oracle_params* P, const void* q, const int32_t* cu, const int32_t* cuk,
+                  const void* k, const void* v, const int32_t* bt, const float* qs,
+                  const float* ks, const float* vs, const uint8_t* mask_in, const int32_t* units,
+                  int nunits, double* out, double* lse) {
   ctx_t c;
-  if (setup(&c, P, q, cu, k, v, bt, qs, ks, vs)) return 1;
+  if (setup(&c, P, q, cu, cuk, k, v, bt, qs, ks, vs)) return 1;
   int32_t* own = NULL;
   if (!units) units = own = all_units(&c, &nunits);
   c.units = units; c.nunits = nunits;

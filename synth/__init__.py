@@ -71,6 +71,10 @@ class Spec:
     recent_blocks: int = 0
     mean_correction: int = 1
     seed: int = 0
+    # KV tokens before the queries of each sequence (chunked prefill): the
+    # queries are the last seqlens[b] of prefix[b] + seqlens[b] KV tokens.
+    # Multiples of block_size; None = no prefix.
+    prefix: Optional[List[int]] = None
 
     @property
     def batch(self) -> int:
@@ -83,6 +87,22 @@ class Spec:
     @property
     def max_seq_len(self) -> int:
         return int(max(self.seqlens)) if self.seqlens else 0
+
+    @property
+    def prefixes(self) -> List[int]:
+        return list(self.prefix) if self.prefix is not None else [0] * self.batch
+
+    @property
+    def kvlens(self) -> List[int]:
+        return [int(p + L) for p, L in zip(self.prefixes, self.seqlens)]
+
+    @property
+    def total_kv_tokens(self) -> int:
+        return int(sum(self.kvlens))
+
+    @property
+    def max_kv_len(self) -> int:
+        return int(max(self.kvlens)) if self.seqlens else 0
 
     def replace(self, **kw) -> "Spec":
         return dataclasses.replace(self, **kw)
@@ -130,8 +150,9 @@ def _to_e4m3_bits(x: np.ndarray) -> np.ndarray:
 class Workload:
     """Host arrays of one generated workload (storage-dtype bit patterns).
 
-    q: [total, Hq, d]; k_tok/v_tok: [total, Hkv, d] (token-major, sequence b
-    at rows cu[b]..cu[b+1]); scales are float32 per head (all ones for bf16).
+    q: [total, Hq, d] (the query tokens, sequence b at rows cu[b]..cu[b+1]);
+    k_tok/v_tok: [total_kv, Hkv, d] (the KV tokens, sequence b at rows
+    cu_k[b]..cu_k[b+1]); scales are float32 per head (all ones for bf16).
     block_table: int32 [batch, max_pages] giving, for page j of sequence b, its
     index in a pool of ``num_pages`` pages of ``page_size`` tokens.
     """
@@ -146,6 +167,11 @@ class Workload:
     block_table: np.ndarray
     num_pages: int
     salient: List[List[np.ndarray]]
+    cu_seqlens_k: Optional[np.ndarray] = None
+
+    def __post_init__(self):
+        if self.cu_seqlens_k is None:
+            self.cu_seqlens_k = self.cu_seqlens
 
     @property
     def max_pages(self) -> int:
@@ -156,11 +182,11 @@ class Workload:
         return _E4M3_NAN if self.spec.dtype == "fp8" else _BF16_NAN
 
     def slots(self) -> np.ndarray:
-        """Pool slot of every token (Eq. page addressing), int64 [total]."""
+        """Pool slot of every KV token (Eq. page addressing), int64 [total_kv]."""
         sp = self.spec
-        cu = self.cu_seqlens
-        out = np.empty(sp.total_tokens, dtype=np.int64)
-        for b, L in enumerate(sp.seqlens):
+        cu = self.cu_seqlens_k
+        out = np.empty(sp.total_kv_tokens, dtype=np.int64)
+        for b, L in enumerate(sp.kvlens):
             j = np.arange(L, dtype=np.int64)
             if sp.page_size == 0:
                 out[cu[b]:cu[b + 1]] = cu[b] + j
@@ -183,20 +209,20 @@ class Workload:
         bt = self.block_table
         if compact:
             used = []
-            for b, L in enumerate(sp.seqlens):
+            for b, L in enumerate(sp.kvlens):
                 used.extend(bt[b, : (L + sp.page_size - 1) // sp.page_size].tolist())
             remap = {pg: i for i, pg in enumerate(dict.fromkeys(used))}
             bt2 = np.zeros_like(bt)
-            for b, L in enumerate(sp.seqlens):
+            for b, L in enumerate(sp.kvlens):
                 n = (L + sp.page_size - 1) // sp.page_size
                 bt2[b, :n] = [remap[x] for x in bt[b, :n]]
             npages = max(1, len(remap))
         else:
             bt2, npages = bt, self.num_pages
         pool = np.full((npages * sp.page_size,) + tok.shape[1:], self.nan_bits, dtype=tok.dtype)
-        sl = np.empty(sp.total_tokens, dtype=np.int64)
-        cu = self.cu_seqlens
-        for b, L in enumerate(sp.seqlens):
+        sl = np.empty(sp.total_kv_tokens, dtype=np.int64)
+        cu = self.cu_seqlens_k
+        for b, L in enumerate(sp.kvlens):
             j = np.arange(L, dtype=np.int64)
             sl[cu[b]:cu[b + 1]] = bt2[b, j // sp.page_size].astype(np.int64) * sp.page_size + j % sp.page_size
         pool[sl] = tok
@@ -225,6 +251,8 @@ class Workload:
             q=q, k_cache=kc, v_cache=vc,
             block_table=torch.from_numpy(self.block_table).to(device),
             cu_seqlens=torch.from_numpy(self.cu_seqlens).to(device),
+            cu_seqlens_k=(None if self.spec.prefix is None
+                          else torch.from_numpy(self.cu_seqlens_k).to(device)),
             q_scale=torch.from_numpy(self.q_scale).to(device),
             k_scale=torch.from_numpy(self.k_scale).to(device),
             v_scale=torch.from_numpy(self.v_scale).to(device),
@@ -238,8 +266,13 @@ def generate(spec: Spec) -> Workload:
     assert Hq % Hkv == 0
     g = Hq // Hkv
     seed = sp.seed
+    pre = sp.prefixes
+    assert all(x >= 0 and x % B == 0 for x in pre), "prefix lengths must be multiples of the block"
+    kvl = sp.kvlens
+    # Q, K and V are drawn for all KV positions of a sequence; Q then keeps
+    # its last seqlens[b] rows, so a chunk reproduces the rows of the whole
     cu = np.zeros(sp.batch + 1, dtype=np.int32)
-    cu[1:] = np.cumsum(sp.seqlens)
+    cu[1:] = np.cumsum(kvl)
     total = int(cu[-1])
 
     ug = np.random.default_rng([seed, 4])
@@ -255,7 +288,7 @@ def generate(spec: Spec) -> Workload:
     # query bias pattern: head hq of group h gets query_bias * u_h
     qbias = torch.from_numpy(np.repeat(sp.query_bias * u, g, axis=0))          # [Hq, d]
     salient: List[List[np.ndarray]] = []
-    for b, L in enumerate(sp.seqlens):
+    for b, L in enumerate(kvl):
         s0 = int(cu[b])
         if L == 0:
             salient.append([np.zeros(0, dtype=np.int64) for _ in range(Hkv)])
@@ -282,6 +315,15 @@ def generate(spec: Spec) -> Workload:
             qt[s0 + full:s0 + min(L, full + B)] += qbias
         salient.append(per_head)
 
+    # query rows: the last seqlens[b] positions of every sequence
+    cu_q = np.zeros(sp.batch + 1, dtype=np.int32)
+    cu_q[1:] = np.cumsum(sp.seqlens)
+    if sp.prefix is not None:
+        rows = np.concatenate([np.arange(cu[b] + pre[b], cu[b + 1]) for b in range(sp.batch)]
+                              + [np.zeros(0, np.int64)]).astype(np.int64)
+    else:
+        rows = None
+
     if sp.dtype == "bf16":
         q, k, v = _to_bf16_bits(qf), _to_bf16_bits(kf), _to_bf16_bits(vf)
         qs = np.ones(Hq, dtype=np.float32)
@@ -303,10 +345,12 @@ def generate(spec: Spec) -> Workload:
     else:
         raise ValueError(sp.dtype)
     del qf, kf, vf, qt, kt
+    if rows is not None:
+        q = np.ascontiguousarray(q[rows])
 
     if sp.page_size > 0:
         p = sp.page_size
-        npg = [(L + p - 1) // p for L in sp.seqlens]
+        npg = [(L + p - 1) // p for L in kvl]
         max_pages = max(1, max(npg) if npg else 1)
         bt = np.zeros((sp.batch, max_pages), dtype=np.int32)
         if sp.page_order == "identity":
@@ -332,7 +376,8 @@ def generate(spec: Spec) -> Workload:
     else:
         bt = np.zeros((sp.batch, 1), dtype=np.int32)
         num_pages = 0
-    return Workload(sp, q, k, v, qs, ks, vs, cu, bt, num_pages, salient)
+    return Workload(sp, q, k, v, qs, ks, vs, cu_q, bt, num_pages, salient,
+                    cu_seqlens_k=cu if sp.prefix is not None else None)
 
 
 # ---------------------------------------------------------------------------
