@@ -32,26 +32,47 @@
  *   fp2_last_error() gives a one-line reason for the last failure of the
  *   calling thread.
  *
+ * Prefix KV (chunked prefill)
+ * ---------------------------
+ * A sequence may hold more keys than queries: its L_q queries (cu_seqlens)
+ * are the last L_q of its L_kv keys (cu_seqlens_k), i.e. query i sits at
+ * absolute position P + i with P = L_kv - L_q, the tokens already in the KV
+ * cache from earlier chunks. P must be a multiple of block_size, so query
+ * block I is key block Ia = I + P / block_size, and every rule below that
+ * compares a query block or position with a key block or position uses Ia
+ * and the absolute position. With cu_seqlens_k == NULL, L_kv = L_q (P = 0).
+ * The selection of a query block depends only on its own rows and the keys
+ * before it, so a chunked prefill gives, row for row, the output of one call
+ * over the whole sequence.
+ *
  * Layouts (row-major, innermost last)
  * -----------------------------------
  *   q, out       [total_tokens, num_q_heads, head_dim]; sequence b occupies
  *                token rows cu_seqlens[b] .. cu_seqlens[b+1]-1.
  *   k_cache,     page_size > 0: a token pool [num_slots, num_kv_heads,
- *   v_cache      head_dim]; token j of sequence b is slot
+ *   v_cache      head_dim]; key j (0 <= j < L_kv) of sequence b is slot
  *                block_table[b][j / page_size] * page_size + j % page_size
  *                (Sec. 3.3, Eq. page). page_size == 0: contiguous
- *                [total_tokens, num_kv_heads, head_dim], laid out like q.
+ *                [total_kv_tokens, num_kv_heads, head_dim], sequence b at
+ *                rows cu_seqlens_k[b] .. cu_seqlens_k[b+1]-1 (cu_seqlens
+ *                without a prefix).
  *   block_table  int32 [batch, max_pages_per_seq] (ignored when page_size == 0).
- *   cu_seqlens   int32 [batch + 1], cu_seqlens[0] == 0, non-decreasing.
+ *   cu_seqlens   int32 [batch + 1], cu_seqlens[0] == 0, non-decreasing:
+ *                the query rows.
+ *   cu_seqlens_k int32 [batch + 1] or NULL: the KV lengths, same rules;
+ *                cu_seqlens_k[b+1] - cu_seqlens_k[b] >= the query length,
+ *                the difference a multiple of block_size.
  *   q/k/v_scale  fp32 per head ([num_q_heads] / [num_kv_heads] / [num_kv_heads]);
  *                only read when dtype == FP2_FP8_E4M3 (the dequantised value
  *                is scale * code, Sec. 3.3 Eq. fp8; a per-tensor scale is the
  *                all-equal case).
- *   block_mask   uint8 [batch, num_kv_heads, nb, nb], nb = ceil(max_seq_len /
- *                block_size). Entry (b, h, I, J): bit 0 = key block J is
- *                attended exactly by query block I of KV head h (kept);
- *                bit 1 = J is a forced block (sink, window, diagonal or
- *                recent). Zero for J > I and for blocks past the sequence.
+ *   block_mask   uint8 [batch, num_kv_heads, nbq, nbk], nbq = ceil(max_seq_len
+ *                / block_size) query blocks, nbk = ceil(max_kv_len / block_size)
+ *                key blocks (nbk == nbq without a prefix). Entry (b, h, I, J):
+ *                bit 0 = key block J is attended exactly by query block I of
+ *                KV head h (kept); bit 1 = J is a forced block (sink, window,
+ *                diagonal or recent). Zero for J > Ia and for blocks past the
+ *                sequence.
  *   lse          fp32 [total_tokens, num_q_heads], natural-log log-sum-exp of
  *                the scaled logits (including the correction masses).
  *
@@ -63,8 +84,9 @@
  * khat_J = the bf16 rounding (nearest, ties to even) of the mean of the
  * dequantised keys of block J. Block J is kept iff alpha == 0, or
  * E[I][J] >= alpha * max_J' E[I][J'], or J is forced: J < sink_blocks,
- * I - J < window_blocks, J == I, or J >= n_b - recent_blocks (n_b = blocks of
- * sequence b). With mean_correction, every block J < I that is not kept adds
+ * I - J < window_blocks, J == I, or J >= n_b - recent_blocks (n_b = key
+ * blocks of sequence b; with a prefix I reads Ia here and below). With
+ * mean_correction, every block J < I that is not kept adds
  * |B_J| * exp(scale * q . kbar_J) * vbar_J to the softmax numerator and
  * |B_J| * exp(scale * q . kbar_J) to its denominator (Sec. 3.2 Eq.
  * correction); kbar/vbar are the block means (stored in bf16 on the GPU).
@@ -105,8 +127,8 @@ typedef struct {
   int32_t head_dim;           /* d: must be 128 */
   int32_t block_size;         /* selection block B in tokens: must be 128 */
   int32_t page_size;          /* p >= 1 tokens per page, or 0 for contiguous KV */
-  int32_t max_seq_len;        /* upper bound of every sequence length, <= 1048576 */
-  int32_t max_pages_per_seq;  /* block_table row stride, >= ceil(max_seq_len / p) */
+  int32_t max_seq_len;        /* upper bound of every query length, <= 1048576 */
+  int32_t max_pages_per_seq;  /* block_table row stride, >= ceil(max_kv_len / p) */
   float alpha;                /* threshold ratio >= 0 (0 keeps every causal block) */
   int32_t sink_blocks;        /* forced leading key blocks, >= 0 */
   int32_t window_blocks;      /* forced local band incl. the diagonal, >= 0 */
@@ -114,6 +136,9 @@ typedef struct {
   int32_t mean_correction;    /* 0 or 1 */
   float softmax_scale;        /* <= 0 selects 1/sqrt(head_dim) */
   int32_t dtype;              /* fp2_dtype_t */
+  int32_t max_kv_len;         /* upper bound of every KV length (prefix + chunk);
+                                 0 selects max_seq_len; else >= max_seq_len,
+                                 <= 1048576 */
 } fp2_params_t;
 
 /* Bytes of workspace the entry points need for `params` (0 for a null or
@@ -126,13 +151,16 @@ size_t fp2_workspace_bytes(const fp2_params_t* params);
  * selection, then attention over the kept blocks of every (sequence, KV head,
  * query block) with the mean correction for the pruned ones (Sec. 3.2-3.3).
  * Inputs: params, q, cu_seqlens (device), cu_seqlens_host (nullable host
- * copy, validated when given), k_cache, v_cache, block_table (device;
+ * copy, validated when given), cu_seqlens_k (device KV lengths, NULL = no
+ * prefix), cu_seqlens_k_host (nullable host copy, validated with
+ * cu_seqlens_host when given), k_cache, v_cache, block_table (device;
  * ignored if page_size == 0), q_scale/k_scale/v_scale (device; fp8 only,
  * else may be null). Outputs: out (bf16, always), lse (nullable), block_mask
  * (every entry written). Rows of out/lse outside [0, cu_seqlens[batch]) are
  * not touched. */
 fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
-                         const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                         const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                         const int32_t* cu_seqlens_k_host, const void* k_cache, const void* v_cache,
                          const int32_t* block_table, const float* q_scale, const float* k_scale,
                          const float* v_scale, void* out, float* lse, uint8_t* block_mask,
                          void* workspace, size_t workspace_bytes, void* stream);
@@ -141,30 +169,34 @@ fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_
  * 1 steps 1-5): writes every entry of block_mask and leaves the pooled means
  * and kept-block lists in the workspace. Arguments as for fp2_prefill. */
 fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
-                          const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
-                          const int32_t* block_table, const float* q_scale, const float* k_scale,
-                          const float* v_scale, uint8_t* block_mask, void* workspace,
+                          const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                          const int32_t* cu_seqlens_k_host, const void* k_cache,
+                          const void* v_cache, const int32_t* block_table, const float* q_scale,
+                          const float* k_scale, const float* v_scale, uint8_t* block_mask,
+                          void* workspace,
                           size_t workspace_bytes, void* stream);
 
 /* The attention stage alone (Sec. 3.2 Eq. correction, Sec. 3.3; Algorithm 1
  * steps 6-11) under a caller-given mask: bit 0 of block_mask_in[b][h][I][J]
- * selects key block J for query block I (entries with J > I are ignored).
- * The caller should select the diagonal J == I of every valid block I: the
+ * selects key block J for query block I (entries with J > Ia are ignored).
+ * The caller should select the diagonal J == Ia of every valid block I: the
  * mask is not checked, and a row whose keys are all excluded (no selected
  * key at or before its position and no corrected block) gets an undefined
  * output. Recomputes the block means and the kept lists from the mask in
  * the workspace. Arguments as for fp2_prefill. */
 fp2_status_t fp2_attend(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
-                        const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                        const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                        const int32_t* cu_seqlens_k_host, const void* k_cache, const void* v_cache,
                         const int32_t* block_table, const float* q_scale, const float* k_scale,
                         const float* v_scale, const uint8_t* block_mask_in, void* out, float* lse,
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* Block means of K and V (Sec. 3.2, the pooled statistics of Eq. correction;
- * Algorithm 1 step 2), dequantised for fp8. khat [batch, num_kv_heads, nb,
- * head_dim] receives the bf16 (nearest-even) rounding of the key means, vbar
- * the same layout for the value means; entries of blocks past a sequence are
- * zero. Needs no workspace. */
+ * Algorithm 1 step 2), dequantised for fp8. Here cu_seqlens are the KV
+ * lengths (a prefix included) and blocks are counted over max_kv_len. khat
+ * [batch, num_kv_heads, nbk, head_dim] receives the bf16 (nearest-even)
+ * rounding of the key means, vbar the same layout for the value means;
+ * entries of blocks past a sequence are zero. Needs no workspace. */
 fp2_status_t fp2_pool(const fp2_params_t* params, const int32_t* cu_seqlens,
                       const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
                       const int32_t* block_table, const float* k_scale, const float* v_scale,

@@ -41,6 +41,7 @@ class Params(ctypes.Structure):
         ("sink_blocks", ctypes.c_int32), ("window_blocks", ctypes.c_int32),
         ("recent_blocks", ctypes.c_int32), ("mean_correction", ctypes.c_int32),
         ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
+        ("max_kv_len", ctypes.c_int32),
     ]
 
 
@@ -60,11 +61,11 @@ def lib():
         L.fp2_workspace_bytes.restype = ctypes.c_size_t
         L.fp2_workspace_bytes.argtypes = [P]
         L.fp2_prefill.restype = ctypes.c_int
-        L.fp2_prefill.argtypes = [P] + [vp] * 13 + [ctypes.c_size_t, vp]
+        L.fp2_prefill.argtypes = [P] + [vp] * 15 + [ctypes.c_size_t, vp]
         L.fp2_estimate.restype = ctypes.c_int
-        L.fp2_estimate.argtypes = [P] + [vp] * 11 + [ctypes.c_size_t, vp]
+        L.fp2_estimate.argtypes = [P] + [vp] * 13 + [ctypes.c_size_t, vp]
         L.fp2_attend.restype = ctypes.c_int
-        L.fp2_attend.argtypes = [P] + [vp] * 13 + [ctypes.c_size_t, vp]
+        L.fp2_attend.argtypes = [P] + [vp] * 15 + [ctypes.c_size_t, vp]
         L.fp2_pool.restype = ctypes.c_int
         L.fp2_pool.argtypes = [P] + [vp] * 10
         L.fp2_status_str.restype = ctypes.c_char_p
@@ -91,18 +92,31 @@ def _check(fn: str, st: int) -> None:
 def make_params(*, batch, num_q_heads, num_kv_heads, max_seq_len, page_size=0,
                 max_pages_per_seq=0, alpha=0.0, sink_blocks=1, window_blocks=2,
                 recent_blocks=0, mean_correction=1, softmax_scale=0.0, dtype="bf16",
-                head_dim=HEAD_DIM, block_size=BLOCK) -> Params:
+                head_dim=HEAD_DIM, block_size=BLOCK, max_kv_len=0) -> Params:
+    """fp2_params_t; max_kv_len bounds the KV lengths with a prefix (0: max_seq_len)."""
     dt = {"bf16": BF16, "fp8": FP8_E4M3}.get(dtype, dtype)
     return Params(batch=batch, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
                   head_dim=head_dim, block_size=block_size, page_size=page_size,
                   max_seq_len=max_seq_len, max_pages_per_seq=max_pages_per_seq,
                   alpha=alpha, sink_blocks=sink_blocks, window_blocks=window_blocks,
                   recent_blocks=recent_blocks, mean_correction=int(mean_correction),
-                  softmax_scale=softmax_scale, dtype=dt)
+                  softmax_scale=softmax_scale, dtype=dt, max_kv_len=max_kv_len)
 
 
 def num_blocks(p: Params) -> int:
+    """Query blocks per sequence bound (block_mask rows)."""
     return (p.max_seq_len + p.block_size - 1) // p.block_size
+
+
+def num_key_blocks(p: Params) -> int:
+    """Key blocks per sequence bound (block_mask columns, pooled rows)."""
+    kv = p.max_kv_len if p.max_kv_len > 0 else p.max_seq_len
+    return (kv + p.block_size - 1) // p.block_size
+
+
+def alloc_mask(p: Params, device="cuda") -> torch.Tensor:
+    return torch.empty((p.batch, p.num_kv_heads, max(1, num_blocks(p)), max(1, num_key_blocks(p))),
+                       dtype=torch.uint8, device=device)
 
 
 def workspace_bytes(p: Params) -> int:
@@ -131,18 +145,21 @@ def alloc_workspace(p: Params, device="cuda") -> torch.Tensor:
 
 
 def alloc_outputs(p: Params, total_tokens: int, device="cuda", want_lse=False):
-    nb = max(1, num_blocks(p))
-    out = torch.empty((total_tokens, p.num_q_heads, p.head_dim), dtype=torch.bfloat16, device=device)
-    mask = torch.empty((p.batch, p.num_kv_heads, nb, nb), dtype=torch.uint8, device=device)
+    out = torch.empty((total_tokens, p.num_q_heads, p.head_dim), dtype=torch.bfloat16,
+                      device=device)
+    mask = alloc_mask(p, device)
     lse = (torch.empty((total_tokens, p.num_q_heads), dtype=torch.float32, device=device)
            if want_lse else None)
     return out, mask, lse
 
 
 def prefill(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_seqlens_host=None,
-            q_scale=None, k_scale=None, v_scale=None, out=None, lse=None, block_mask=None,
-            workspace=None, want_lse=False, stream=None):
-    """fp2_prefill: returns (out [total, Hq, 128] bf16, block_mask uint8, lse or None)."""
+            cu_seqlens_k=None, cu_seqlens_k_host=None, q_scale=None, k_scale=None, v_scale=None,
+            out=None, lse=None, block_mask=None, workspace=None, want_lse=False, stream=None):
+    """fp2_prefill: returns (out [total, Hq, 128] bf16, block_mask uint8, lse or None).
+
+    cu_seqlens_k (device) gives the KV lengths when the queries are the last
+    tokens of longer sequences (a prefix KV); None means no prefix."""
     if out is None or block_mask is None:
         o2, m2, l2 = alloc_outputs(p, q.shape[0], q.device, want_lse and lse is None)
         out = o2 if out is None else out
@@ -151,34 +168,35 @@ def prefill(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_
     if workspace is None:
         workspace = alloc_workspace(p, q.device)
     st = lib().fp2_prefill(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
-                           _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(q_scale),
-                           _ptr(k_scale), _ptr(v_scale), _ptr(out), _ptr(lse), _ptr(block_mask),
+                           _ptr(cu_seqlens_k), _host_ptr(cu_seqlens_k_host), _ptr(k_cache),
+                           _ptr(v_cache), _ptr(block_table), _ptr(q_scale), _ptr(k_scale),
+                           _ptr(v_scale), _ptr(out), _ptr(lse), _ptr(block_mask),
                            _ptr(workspace), workspace.numel(), _stream(stream))
     _check("fp2_prefill", st)
     return out, block_mask, lse
 
 
 def estimate(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *,
-             cu_seqlens_host=None, q_scale=None, k_scale=None, v_scale=None, block_mask=None,
-             workspace=None, stream=None):
+             cu_seqlens_host=None, cu_seqlens_k=None, cu_seqlens_k_host=None, q_scale=None,
+             k_scale=None, v_scale=None, block_mask=None, workspace=None, stream=None):
     """fp2_estimate: returns (block_mask, workspace)."""
     if block_mask is None:
-        nb = max(1, num_blocks(p))
-        block_mask = torch.empty((p.batch, p.num_kv_heads, nb, nb), dtype=torch.uint8,
-                                 device=q.device)
+        block_mask = alloc_mask(p, q.device)
     if workspace is None:
         workspace = alloc_workspace(p, q.device)
     st = lib().fp2_estimate(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
-                            _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(q_scale),
-                            _ptr(k_scale), _ptr(v_scale), _ptr(block_mask), _ptr(workspace),
+                            _ptr(cu_seqlens_k), _host_ptr(cu_seqlens_k_host), _ptr(k_cache),
+                            _ptr(v_cache), _ptr(block_table), _ptr(q_scale), _ptr(k_scale),
+                            _ptr(v_scale), _ptr(block_mask), _ptr(workspace),
                             workspace.numel(), _stream(stream))
     _check("fp2_estimate", st)
     return block_mask, workspace
 
 
 def attend(p: Params, q, k_cache, v_cache, cu_seqlens, block_mask, block_table=None, *,
-           cu_seqlens_host=None, q_scale=None, k_scale=None, v_scale=None, out=None, lse=None,
-           workspace=None, want_lse=False, stream=None):
+           cu_seqlens_host=None, cu_seqlens_k=None, cu_seqlens_k_host=None, q_scale=None,
+           k_scale=None, v_scale=None, out=None, lse=None, workspace=None, want_lse=False,
+           stream=None):
     """fp2_attend under ``block_mask`` (bit 0 = kept): returns (out, lse or None)."""
     if out is None:
         out = torch.empty((q.shape[0], p.num_q_heads, p.head_dim), dtype=torch.bfloat16,
@@ -188,8 +206,9 @@ def attend(p: Params, q, k_cache, v_cache, cu_seqlens, block_mask, block_table=N
     if workspace is None:
         workspace = alloc_workspace(p, q.device)
     st = lib().fp2_attend(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
-                          _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(q_scale),
-                          _ptr(k_scale), _ptr(v_scale), _ptr(block_mask), _ptr(out), _ptr(lse),
+                          _ptr(cu_seqlens_k), _host_ptr(cu_seqlens_k_host), _ptr(k_cache),
+                          _ptr(v_cache), _ptr(block_table), _ptr(q_scale), _ptr(k_scale),
+                          _ptr(v_scale), _ptr(block_mask), _ptr(out), _ptr(lse),
                           _ptr(workspace), workspace.numel(), _stream(stream))
     _check("fp2_attend", st)
     return out, lse
@@ -197,8 +216,9 @@ def attend(p: Params, q, k_cache, v_cache, cu_seqlens, block_mask, block_table=N
 
 def pool(p: Params, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_seqlens_host=None,
          k_scale=None, v_scale=None, stream=None):
-    """fp2_pool: returns (khat, vbar) as bf16 [batch, Hkv, nb, 128]."""
-    nb = max(1, num_blocks(p))
+    """fp2_pool over the KV lengths cu_seqlens: returns (khat, vbar) as bf16
+    [batch, Hkv, nbk, 128]."""
+    nb = max(1, num_key_blocks(p))
     shape = (p.batch, p.num_kv_heads, nb, p.head_dim)
     khat = torch.empty(shape, dtype=torch.bfloat16, device=k_cache.device)
     vbar = torch.empty(shape, dtype=torch.bfloat16, device=k_cache.device)

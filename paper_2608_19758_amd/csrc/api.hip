@@ -30,7 +30,10 @@ fp2_status_t ok() {
 
 constexpr int kMaxSeqLen = fp2::kMaxBlocks * fp2::kBlock;   // 1M tokens
 
-int nb_of(const fp2_params_t* p) { return (p->max_seq_len + fp2::kBlock - 1) / fp2::kBlock; }
+int max_kv_of(const fp2_params_t* p) { return p->max_kv_len > 0 ? p->max_kv_len : p->max_seq_len; }
+// query blocks (mask rows) and key blocks (mask columns, pooled rows)
+int nbq_of(const fp2_params_t* p) { return (p->max_seq_len + fp2::kBlock - 1) / fp2::kBlock; }
+int nbk_of(const fp2_params_t* p) { return (max_kv_of(p) + fp2::kBlock - 1) / fp2::kBlock; }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -40,14 +43,16 @@ struct Layout {
 
 Layout layout_of(const fp2_params_t* p) {
   Layout l{};
-  const size_t rows = (size_t)p->batch * p->num_kv_heads * nb_of(p);
+  const size_t heads = (size_t)p->batch * p->num_kv_heads;
+  const size_t rows = heads * nbq_of(p);    // (sequence, KV head, query block)
+  const size_t krows = heads * nbk_of(p);   // (sequence, KV head, key block)
   size_t off = 0;
   l.khat = off;
-  off = align256(off + rows * fp2::kHeadDim * sizeof(uint16_t));
+  off = align256(off + krows * fp2::kHeadDim * sizeof(uint16_t));
   l.vbar = off;
-  off = align256(off + rows * fp2::kHeadDim * sizeof(uint16_t));
+  off = align256(off + krows * fp2::kHeadDim * sizeof(uint16_t));
   l.kidx = off;
-  off = align256(off + rows * nb_of(p) * sizeof(int32_t));
+  off = align256(off + rows * nbk_of(p) * sizeof(int32_t));
   l.kcnt = off;
   off = align256(off + rows * sizeof(int32_t));
   l.queue = off;
@@ -74,10 +79,15 @@ fp2_status_t validate_params(const fp2_params_t* p) {
   if (p->max_seq_len < 0) return fail(FP2_EINVAL, "max_seq_len %d < 0", p->max_seq_len);
   if (p->max_seq_len > kMaxSeqLen)
     return fail(FP2_EUNSUPPORTED, "max_seq_len %d > %d", p->max_seq_len, kMaxSeqLen);
+  if (p->max_kv_len < 0) return fail(FP2_EINVAL, "max_kv_len %d < 0", p->max_kv_len);
+  if (p->max_kv_len > 0 && p->max_kv_len < p->max_seq_len)
+    return fail(FP2_EINVAL, "max_kv_len %d < max_seq_len %d", p->max_kv_len, p->max_seq_len);
+  if (p->max_kv_len > kMaxSeqLen)
+    return fail(FP2_EUNSUPPORTED, "max_kv_len %d > %d", p->max_kv_len, kMaxSeqLen);
   if (p->page_size > 0) {
-    const int need = (p->max_seq_len + p->page_size - 1) / p->page_size;
+    const int need = (max_kv_of(p) + p->page_size - 1) / p->page_size;
     if (p->max_pages_per_seq < need)
-      return fail(FP2_EINVAL, "max_pages_per_seq %d < ceil(max_seq_len / page_size) = %d",
+      return fail(FP2_EINVAL, "max_pages_per_seq %d < ceil(max_kv_len / page_size) = %d",
                   p->max_pages_per_seq, need);
   }
   if (!(p->alpha >= 0.f) || !isfinite(p->alpha))
@@ -96,10 +106,23 @@ bool aligned16(const void* x) { return ((uintptr_t)x & 15u) == 0; }
 
 // Validation of everything but the workspace; `work` is false when there is
 // nothing to compute (no sequence or zero-length bound).
+// Host copy of cumulative lengths: starts at 0, non-decreasing, each length
+// at most `bound`.
+fp2_status_t check_cu(const int32_t* cu, int batch, int bound, const char* name, const char* bname) {
+  if (cu[0] != 0) return fail(FP2_EINVAL, "%s[0] = %d != 0", name, cu[0]);
+  for (int b = 0; b < batch; ++b) {
+    const int len = cu[b + 1] - cu[b];
+    if (len < 0) return fail(FP2_EINVAL, "%s decreases at %d", name, b);
+    if (len > bound)
+      return fail(FP2_EINVAL, "%s: sequence %d has length %d > %s %d", name, b, len, bname, bound);
+  }
+  return FP2_OK;
+}
+
 fp2_status_t validate_common(const fp2_params_t* p, const void* q, const int32_t* cu,
-                             const int32_t* cu_host, const void* k, const void* v,
-                             const int32_t* bt, const float* qs, const float* ks,
-                             const float* vs, bool need_q, bool* work) {
+                             const int32_t* cu_host, const int32_t* cuk, const int32_t* cuk_host,
+                             const void* k, const void* v, const int32_t* bt, const float* qs,
+                             const float* ks, const float* vs, bool need_q, bool* work) {
   fp2_status_t st = validate_params(p);
   if (st != FP2_OK) return st;
   *work = p->batch > 0 && p->max_seq_len > 0;
@@ -112,13 +135,17 @@ fp2_status_t validate_common(const fp2_params_t* p, const void* q, const int32_t
   if (p->page_size > 0 && !bt) return fail(FP2_EINVAL, "block_table is null with page_size > 0");
   if (p->dtype == FP2_FP8_E4M3 && ((need_q && !qs) || !ks || !vs))
     return fail(FP2_EINVAL, "fp8 needs q_scale, k_scale and v_scale");
-  if (cu_host) {
-    if (cu_host[0] != 0) return fail(FP2_EINVAL, "cu_seqlens[0] = %d != 0", cu_host[0]);
+  if (cuk_host && !cuk) return fail(FP2_EINVAL, "cu_seqlens_k_host given without cu_seqlens_k");
+  if (cu_host && (st = check_cu(cu_host, p->batch, p->max_seq_len, "cu_seqlens", "max_seq_len")))
+    return st;
+  if (cuk_host && (st = check_cu(cuk_host, p->batch, max_kv_of(p), "cu_seqlens_k", "max_kv_len")))
+    return st;
+  if (cu_host && cuk_host) {
     for (int b = 0; b < p->batch; ++b) {
-      const int len = cu_host[b + 1] - cu_host[b];
-      if (len < 0) return fail(FP2_EINVAL, "cu_seqlens decreases at %d", b);
-      if (len > p->max_seq_len)
-        return fail(FP2_EINVAL, "sequence %d has length %d > max_seq_len %d", b, len, p->max_seq_len);
+      const int pre = (cuk_host[b + 1] - cuk_host[b]) - (cu_host[b + 1] - cu_host[b]);
+      if (pre < 0 || pre % fp2::kBlock)
+        return fail(FP2_EINVAL, "sequence %d: KV length - query length = %d is not a "
+                    "non-negative multiple of block_size", b, pre);
     }
   }
   return FP2_OK;
@@ -140,12 +167,13 @@ int log2_exact(int x) {
   return s;
 }
 
-fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* cu, const void* k,
-                          const void* v, const int32_t* bt, const float* qs, const float* ks,
-                          const float* vs) {
+fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* cu,
+                          const int32_t* cuk, const void* k, const void* v, const int32_t* bt,
+                          const float* qs, const float* ks, const float* vs) {
   fp2::Problem pr{};
   pr.q = q;
   pr.cu = cu;
+  pr.cuk = cuk ? cuk : cu;
   pr.k = k;
   pr.v = v;
   pr.pm.table = bt;
@@ -159,7 +187,8 @@ fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* c
   pr.hq = p->num_q_heads;
   pr.hkv = p->num_kv_heads;
   pr.g = p->num_q_heads / p->num_kv_heads;
-  pr.nbmax = nb_of(p);
+  pr.nbmax = nbq_of(p);
+  pr.nbk = nbk_of(p);
   pr.sink = p->sink_blocks;
   pr.window = p->window_blocks;
   pr.recent = p->recent_blocks;
@@ -203,20 +232,22 @@ size_t fp2_workspace_bytes(const fp2_params_t* params) {
 }
 
 fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
-                         const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                         const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                         const int32_t* cu_seqlens_k_host, const void* k_cache, const void* v_cache,
                          const int32_t* block_table, const float* q_scale, const float* k_scale,
                          const float* v_scale, void* out, float* lse, uint8_t* block_mask,
                          void* workspace, size_t workspace_bytes, void* stream) {
   bool work = false;
-  fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, k_cache, v_cache,
-                                    block_table, q_scale, k_scale, v_scale, true, &work);
+  fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, cu_seqlens_k,
+                                    cu_seqlens_k_host, k_cache, v_cache, block_table, q_scale,
+                                    k_scale, v_scale, true, &work);
   if (st != FP2_OK) return st;
   if (!work) return ok();
   if (!out || !block_mask) return fail(FP2_EINVAL, "out or block_mask is null");
   if (!aligned16(out)) return fail(FP2_EINVAL, "out must be 16-byte aligned");
   if ((st = validate_ws(params, workspace, workspace_bytes)) != FP2_OK) return st;
-  const fp2::Problem pr = make_problem(params, q, cu_seqlens, k_cache, v_cache, block_table,
-                                       q_scale, k_scale, v_scale);
+  const fp2::Problem pr = make_problem(params, q, cu_seqlens, cu_seqlens_k, k_cache, v_cache,
+                                       block_table, q_scale, k_scale, v_scale);
   const Views vw = views_of(params, workspace);
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = fp2::launch_pool(pr, vw.pooled, s);
@@ -226,19 +257,21 @@ fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_
 }
 
 fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
-                          const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
-                          const int32_t* block_table, const float* q_scale, const float* k_scale,
-                          const float* v_scale, uint8_t* block_mask, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+                          const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                          const int32_t* cu_seqlens_k_host, const void* k_cache,
+                          const void* v_cache, const int32_t* block_table, const float* q_scale,
+                          const float* k_scale, const float* v_scale, uint8_t* block_mask,
+                          void* workspace, size_t workspace_bytes, void* stream) {
   bool work = false;
-  fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, k_cache, v_cache,
-                                    block_table, q_scale, k_scale, v_scale, true, &work);
+  fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, cu_seqlens_k,
+                                    cu_seqlens_k_host, k_cache, v_cache, block_table, q_scale,
+                                    k_scale, v_scale, true, &work);
   if (st != FP2_OK) return st;
   if (!work) return ok();
   if (!block_mask) return fail(FP2_EINVAL, "block_mask is null");
   if ((st = validate_ws(params, workspace, workspace_bytes)) != FP2_OK) return st;
-  const fp2::Problem pr = make_problem(params, q, cu_seqlens, k_cache, v_cache, block_table,
-                                       q_scale, k_scale, v_scale);
+  const fp2::Problem pr = make_problem(params, q, cu_seqlens, cu_seqlens_k, k_cache, v_cache,
+                                       block_table, q_scale, k_scale, v_scale);
   const Views vw = views_of(params, workspace);
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = fp2::launch_pool(pr, vw.pooled, s);
@@ -247,20 +280,22 @@ fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32
 }
 
 fp2_status_t fp2_attend(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
-                        const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
+                        const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                        const int32_t* cu_seqlens_k_host, const void* k_cache, const void* v_cache,
                         const int32_t* block_table, const float* q_scale, const float* k_scale,
                         const float* v_scale, const uint8_t* block_mask_in, void* out, float* lse,
                         void* workspace, size_t workspace_bytes, void* stream) {
   bool work = false;
-  fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, k_cache, v_cache,
-                                    block_table, q_scale, k_scale, v_scale, true, &work);
+  fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, cu_seqlens_k,
+                                    cu_seqlens_k_host, k_cache, v_cache, block_table, q_scale,
+                                    k_scale, v_scale, true, &work);
   if (st != FP2_OK) return st;
   if (!work) return ok();
   if (!out || !block_mask_in) return fail(FP2_EINVAL, "out or block_mask_in is null");
   if (!aligned16(out)) return fail(FP2_EINVAL, "out must be 16-byte aligned");
   if ((st = validate_ws(params, workspace, workspace_bytes)) != FP2_OK) return st;
-  const fp2::Problem pr = make_problem(params, q, cu_seqlens, k_cache, v_cache, block_table,
-                                       q_scale, k_scale, v_scale);
+  const fp2::Problem pr = make_problem(params, q, cu_seqlens, cu_seqlens_k, k_cache, v_cache,
+                                       block_table, q_scale, k_scale, v_scale);
   const Views vw = views_of(params, workspace);
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = hipSuccess;
@@ -275,13 +310,17 @@ fp2_status_t fp2_pool(const fp2_params_t* params, const int32_t* cu_seqlens,
                       const int32_t* block_table, const float* k_scale, const float* v_scale,
                       void* khat, void* vbar, void* stream) {
   bool work = false;
-  fp2_status_t st = validate_common(params, nullptr, cu_seqlens, cu_seqlens_host, k_cache, v_cache,
-                                    block_table, nullptr, k_scale, v_scale, false, &work);
+  // the lengths here are KV lengths, bounded by max_kv_len
+  fp2_params_t pp = params ? *params : fp2_params_t{};
+  if (params) pp.max_seq_len = max_kv_of(params);
+  fp2_status_t st = validate_common(params ? &pp : nullptr, nullptr, cu_seqlens, cu_seqlens_host,
+                                    nullptr, nullptr, k_cache, v_cache, block_table, nullptr,
+                                    k_scale, v_scale, false, &work);
   if (st != FP2_OK) return st;
   if (!work) return ok();
   if (!khat || !vbar) return fail(FP2_EINVAL, "khat or vbar is null");
-  const fp2::Problem pr = make_problem(params, nullptr, cu_seqlens, k_cache, v_cache, block_table,
-                                       nullptr, k_scale, v_scale);
+  const fp2::Problem pr = make_problem(&pp, nullptr, cu_seqlens, nullptr, k_cache, v_cache,
+                                       block_table, nullptr, k_scale, v_scale);
   fp2::Pooled pooled{(uint16_t*)khat, (uint16_t*)vbar};
   return hip_status(fp2::launch_pool(pr, pooled, (hipStream_t)stream), "fp2_pool launch");
 }

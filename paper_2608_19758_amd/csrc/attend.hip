@@ -32,13 +32,21 @@
 // per-head scales c_q c_k are applied to the fp32 scores, the probabilities
 // are stored as e4m3(2^8 * exp(S - m)) (range [0, 256]) and the denominator
 // sums those stored values (Sec. 3.3 Eq. fp8); c_v is applied in the
-// epilogue and the 2^8 is removed from the LSE. The fp8 loop is software
-// pipelined: the scores of step s+1 are issued to the matrix cores before
-// the softmax of step s runs on the vector ALUs.
+// epilogue and the 2^8 is removed from the LSE. Within a step the two waves
+// of a SIMD overlap each other's matrix and vector work; the vector issue
+// count per step is what bounds the fp8 loop, so the softmax is kept lean
+// (masking only on the diagonal and last correction steps, constants held
+// in registers across steps).
 // bf16 uses v_mfma_f32_32x32x16_bf16. Correction steps use the pooled means
 // as keys khat_J and values vbar_J (bf16, real units, bf16 MFMA for both
 // dtypes), logits shifted by log2|B_J| = 7 (Sec. 3.2 implementation
 // paragraph).
+//
+// Prefix KV (chunked prefill): the queries of a sequence may be the last
+// L_q of its L_kv keys. Keys, key blocks and the pooled means are then those
+// of the L_kv tokens, query block I is key block Ia = I + (L_kv - L_q)/B, and
+// the causal mask, the diagonal and the correction range J < Ia use absolute
+// positions; query rows and the LSE are indexed by the local position.
 #include <algorithm>
 #include <utility>
 
@@ -628,10 +636,15 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     const int I = p.nbmax - 1 - u / nbh;
     const int bh = u % nbh;
     const int b = bh / p.hkv, h = bh % p.hkv;
-    const int64_t tok0 = p.cu[b];
-    const int L = p.cu[b + 1] - (int)tok0;
-    const int n = (L + kBlock - 1) / kBlock;
-    if (I >= n) continue;
+    const int Lq = p.cu[b + 1] - p.cu[b];
+    if (I * kBlock >= Lq) continue;
+    // KV tokens of the sequence (a prefix included) and the absolute key
+    // block Ia of query block I; positions below are absolute, and query
+    // position x is packed row qbase + x
+    const int64_t tok0 = p.cuk[b];
+    const int L = p.cuk[b + 1] - (int)tok0;
+    const int Ia = I + (L - Lq) / kBlock;
+    const int64_t qbase = (int64_t)p.cu[b] - (L - Lq);
 
     const int lane = tid & 63, w = tid >> 6;
     const int half = lane >> 5, l32 = lane & 31;
@@ -647,9 +660,9 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     int64_t qoff[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      pos[rt] = I * kBlock + (pr0 + 32 * rt) / G;
+      pos[rt] = Ia * kBlock + (pr0 + 32 * rt) / G;
       qvalid[rt] = pos[rt] < L;
-      qoff[rt] = ((tok0 + pos[rt]) * p.hq + hq) * kHeadDim;   // element index
+      qoff[rt] = ((qbase + pos[rt]) * p.hq + hq) * kHeadDim;   // element index
     }
 
     RowState<RT> rs;
@@ -667,16 +680,14 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     const float off = FP8 ? 8.f : 0.f;        // log2 of the probability offset
     asm volatile("" : "+v"(qsc), "+v"(vsc), "+v"(ksc));  // loads complete before the rings
 
-    using PK = Plan<W, FP8>;
-
     // ---- kept blocks: step s of a chunk -> its block list entry s/2, half s%2
     {
       const uint8_t* K = (const uint8_t*)p.k;
       const uint8_t* V = (const uint8_t*)p.v;
       constexpr int esz = FP8 ? 1 : 2;
       const int cnt = kl.cnt[row];
-      const int32_t* kidx = kl.idx + row * p.nbmax;
-      const bool has_diag = cnt > 0 && kidx[cnt - 1] == I;
+      const int32_t* kidx = kl.idx + row * p.nbk;
+      const bool has_diag = cnt > 0 && kidx[cnt - 1] == Ia;
       const int64_t rowbytes = (int64_t)p.hkv * kHeadDim * esz;     // one token slot of the pool
       const int64_t hbytes = (int64_t)h * kHeadDim * esz;
       const int page = p.pm.page, shift = p.pm.shift;
@@ -765,7 +776,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
-                fin_fp8<RT>(st, S, rs, cs, I * kBlock + kStep * (s & 1), pos, s < ndiag, lane,
+                fin_fp8<RT>(st, S, rs, cs, Ia * kBlock + kStep * (s & 1), pos, s < ndiag, lane,
                             ones);
               },
               tid);
@@ -774,7 +785,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
-                fin_bf16<0, RT, NPRE>(st, S, rs, cs, off, 1.f, I * kBlock + kStep * (s & 1), pos,
+                fin_bf16<0, RT, NPRE>(st, S, rs, cs, off, 1.f, Ia * kBlock + kStep * (s & 1), pos,
                                       s < ndiag, 0, lane);
               },
               tid);
@@ -787,9 +798,9 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       for (int rt = 0; rt < RT; ++rt) rs.l[rt] += half == 0 ? rs.ls[rt][0] : 0.f;
     }
 
-    // ---- mean correction over the pruned blocks J < I, compacted into a list
-    if (p.corr && I > 0) {
-      const uint8_t* mrow = mask + row * p.nbmax;
+    // ---- mean correction over the pruned blocks J < Ia, compacted into a list
+    if (p.corr && Ia > 0) {
+      const uint8_t* mrow = mask + row * p.nbk;
       uint16_t* plist = (uint16_t*)aux;
       // Q as bf16 (fp8 codes widen exactly); the fp8 scale goes into cs.
       bf16x8_t qb[RT][8];
@@ -820,12 +831,12 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       // real-valued vbar enters with weight 1/c_v.
       const float pv_scale = FP8 ? 1.f / vsc : 1.f;
       const float cs = p.scale_log2 * qsc;
-      const int64_t pbase = ((int64_t)b * p.hkv + h) * p.nbmax * kHeadDim;
+      const int64_t pbase = ((int64_t)b * p.hkv + h) * p.nbk * kHeadDim;
       const uint8_t* Kh = (const uint8_t*)(pooled.khat + pbase);
       const uint8_t* Vh = (const uint8_t*)(pooled.vbar + pbase);
 #pragma unroll 1
-      for (int j0 = 0; j0 < I; j0 += kPlist) {
-        const int j1 = min(I, j0 + kPlist);
+      for (int j0 = 0; j0 < Ia; j0 += kPlist) {
+        const int j1 = min(Ia, j0 + kPlist);
         // compaction of the pruned J in [j0, j1), in ascending order
         int np = 0;
 #pragma unroll 1
@@ -884,7 +895,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
           *(uint2*)(orow + d) = v;
         }
       if (lse && half == 0)
-        lse[(tok0 + pos[rt]) * p.hq + hq] = (rs.m[rt] + fast_log2(l_tot) - off) * kLn2;
+        lse[(qbase + pos[rt]) * p.hq + hq] = (rs.m[rt] + fast_log2(l_tot) - off) * kLn2;
     }
   }
 }

@@ -18,6 +18,9 @@
 // log2(alpha), or J is forced (sink, window incl. diagonal, recent). The mask
 // row is written in full (zeros past I) and the kept blocks are compacted in
 // ascending order with wave ballots into the per-row list of the workspace.
+// With a prefix KV (the queries are the last keys of the sequence) the key
+// blocks are those of the KV tokens and query block I is key block
+// Ia = I + prefix/B; every comparison of I with a key block uses Ia.
 //
 // Precision: fp8 queries are widened to bf16 exactly, the per-head fp8 scale
 // is applied in fp32 after the MFMA, and exponentials use the hardware
@@ -39,7 +42,7 @@ template <int FP8, int G>
 __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled pooled,
                                                             uint8_t* __restrict__ mask,
                                                             KeptLists kl) {
-  extern __shared__ float ell[];            // [nbmax] block log2-energies of this row
+  extern __shared__ float ell[];            // [nbk] block log2-energies of this row
   __shared__ uint4 qt[2][32 * 16];          // Q tiles (double buffer): 32 rows x 16 chunks of 8 bf16
   __shared__ float redf[kWaves];
   __shared__ int redi[kWaves];
@@ -71,11 +74,15 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
   const int64_t tok0 = p.cu[b];
   const int L = p.cu[b + 1] - (int)tok0;
   const int n = (L + kBlock - 1) / kBlock;
+  // KV tokens and key blocks; with a prefix query block I is key block Ia
+  const int Lk = p.cuk[b + 1] - p.cuk[b];
+  const int nk = (Lk + kBlock - 1) / kBlock;
+  const int Ia = I + (Lk - L) / kBlock;
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
-  uint8_t* mrow = mask + row * p.nbmax;
+  uint8_t* mrow = mask + row * p.nbk;
 
   if (I >= n) {
-    for (int J = tid; J < p.nbmax; J += kThreads) mrow[J] = 0;
+    for (int J = tid; J < p.nbk; J += kThreads) mrow[J] = 0;
     if (tid == 0) kl.cnt[row] = 0;
     continue;
   }
@@ -92,7 +99,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     cs[j] = FP8 ? p.scale_log2 * p.q_scale[h * G + hd] : p.scale_log2;
   }
 
-  const uint16_t* khat = pooled.khat + ((int64_t)b * p.hkv + h) * p.nbmax * kHeadDim;
+  const uint16_t* khat = pooled.khat + ((int64_t)b * p.hkv + h) * p.nbk * kHeadDim;
 
   // This thread's 16 bytes of Q tile t (bf16: row tid/16, chunk tid%16;
   // fp8: threads < 256, row tid/8, 16 codes tid%8), zero past the block.
@@ -128,21 +135,21 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     }
   };
 
-  for (int grp = 0; grp <= I; grp += kGroup) {
+  for (int grp = 0; grp <= Ia; grp += kGroup) {
     bf16x8_t kf[kChunksPerWave][8];
     float m[kChunksPerWave], E[kChunksPerWave];
     bool act[kChunksPerWave];
 #pragma unroll
     for (int c = 0; c < kChunksPerWave; ++c) {
       const int J0 = grp + 32 * (w + kWaves * c);
-      act[c] = J0 <= I;
+      act[c] = J0 <= Ia;
       m[c] = -INFINITY;
       E[c] = 0.f;
       const int J = J0 + l32;
 #pragma unroll
       for (int ds = 0; ds < 8; ++ds) {
         uint4 v = make_uint4(0, 0, 0, 0);
-        if (act[c] && J <= I) v = *(const uint4*)(khat + (int64_t)J * kHeadDim + 16 * ds + 8 * half);
+        if (act[c] && J <= Ia) v = *(const uint4*)(khat + (int64_t)J * kHeadDim + 16 * ds + 8 * half);
         kf[c][ds] = __builtin_bit_cast(bf16x8_t, v);
       }
     }
@@ -224,14 +231,14 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       float e1 = m[c] == -INFINITY ? 0.f : E[c] * fast_exp2(m[c] - M);
       float e2 = m2 == -INFINITY ? 0.f : E2 * fast_exp2(m2 - M);
       const int J = grp + 32 * (w + kWaves * c) + l32;
-      if (half == 0 && J <= I) ell[J] = M + fast_log2(e1 + e2);
+      if (half == 0 && J <= Ia) ell[J] = M + fast_log2(e1 + e2);
     }
     __syncthreads();   // every wave is done with the Q tile buffers and ell of this group
   }
 
   // ---- selection: max-based threshold plus forced blocks (Eq. select)
   float mu = -INFINITY;
-  for (int J = tid; J <= I; J += kThreads) mu = fmaxf(mu, ell[J]);
+  for (int J = tid; J <= Ia; J += kThreads) mu = fmaxf(mu, ell[J]);
   mu = wave_max(mu);
   if (lane == 0) redf[w] = mu;
   __syncthreads();
@@ -241,15 +248,15 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
   const bool keep_all = p.alpha == 0.f;
   const float thr = keep_all ? -INFINITY : mu + fast_log2(p.alpha);
 
-  int32_t* kidx = kl.idx + row * p.nbmax;
+  int32_t* kidx = kl.idx + row * p.nbk;
   int base = 0;
-  for (int J0 = 0; J0 < p.nbmax; J0 += kThreads) {
+  for (int J0 = 0; J0 < p.nbk; J0 += kThreads) {
     const int J = J0 + tid;
-    const bool valid = J <= I;
-    const bool forced = valid && (J < p.sink || I - J < p.window || J == I || J >= n - p.recent);
+    const bool valid = J <= Ia;
+    const bool forced = valid && (J < p.sink || Ia - J < p.window || J == Ia || J >= nk - p.recent);
     const bool keep = valid && (keep_all || forced || ell[J] >= thr);
-    if (J < p.nbmax) mrow[J] = (uint8_t)((keep ? 1 : 0) | (forced ? 2 : 0));
-    if (J0 <= I) {
+    if (J < p.nbk) mrow[J] = (uint8_t)((keep ? 1 : 0) | (forced ? 2 : 0));
+    if (J0 <= Ia) {
       const uint64_t bal = __ballot(keep);
       const int pre = __popcll(bal & ((1ull << lane) - 1ull));
       __syncthreads();
@@ -280,18 +287,19 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int L = p.cu[b + 1] - p.cu[b];
   const int n = (L + kBlock - 1) / kBlock;
+  const int Ia = I + (p.cuk[b + 1] - p.cuk[b] - L) / kBlock;   // key block of query block I
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
   if (blockIdx.x == 0 && tid == 0) *kl.queue = 0;
   if (I >= n) {
     if (tid == 0) kl.cnt[row] = 0;
     return;
   }
-  const uint8_t* mrow = mask + row * p.nbmax;
-  int32_t* kidx = kl.idx + row * p.nbmax;
+  const uint8_t* mrow = mask + row * p.nbk;
+  int32_t* kidx = kl.idx + row * p.nbk;
   int base = 0;
-  for (int J0 = 0; J0 <= I; J0 += 256) {
+  for (int J0 = 0; J0 <= Ia; J0 += 256) {
     const int J = J0 + tid;
-    const bool keep = J <= I && (mrow[J] & 1);
+    const bool keep = J <= Ia && (mrow[J] & 1);
     const uint64_t bal = __ballot(keep);
     const int pre = __popcll(bal & ((1ull << lane) - 1ull));
     __syncthreads();
@@ -328,7 +336,7 @@ hipError_t launch_est_dt(const Problem& p, const Pooled& pooled, uint8_t* mask, 
   const int cus = est_device_cus();
   if (cus <= 0) return hipErrorInvalidDevice;
   const unsigned grid = (unsigned)std::min<int64_t>((int64_t)p.nbmax * p.batch * p.hkv, cus);
-  const size_t smem = (size_t)p.nbmax * sizeof(float);
+  const size_t smem = (size_t)p.nbk * sizeof(float);
   switch (p.g) {
     case 1: estimate_kernel<FP8, 1><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
     case 2: estimate_kernel<FP8, 2><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;

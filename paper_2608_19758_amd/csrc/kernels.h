@@ -10,14 +10,18 @@ namespace fp2 {
 // Everything a kernel needs to find its rows, shared by all stages.
 struct Problem {
   const void* q;            // [total, Hq, d] bf16 or e4m3 codes
-  const int32_t* cu;        // [batch + 1]
+  const int32_t* cu;        // [batch + 1] query rows
+  const int32_t* cuk;       // [batch + 1] KV tokens (== cu without a prefix); the
+                            // queries of sequence b are its last cu-lengths keys
   const void* k;            // pool or contiguous, bf16 or e4m3 codes
   const void* v;
   PageMap pm;
   const float* q_scale;     // fp8 only
   const float* k_scale;
   const float* v_scale;
-  int32_t batch, hq, hkv, g, nbmax;
+  int32_t batch, hq, hkv, g;
+  int32_t nbmax;            // query blocks per sequence bound (mask rows)
+  int32_t nbk;              // key blocks per sequence bound (mask columns, pooled rows)
   int32_t sink, window, recent, corr;
   float alpha;
   float scale_log2;         // softmax_scale * log2(e)
@@ -26,12 +30,12 @@ struct Problem {
 
 // Workspace views.
 struct Pooled {
-  uint16_t* khat;           // [batch, Hkv, nbmax, d] bf16 key means (scoring and correction)
-  uint16_t* vbar;           // [batch, Hkv, nbmax, d] bf16 value means (correction)
+  uint16_t* khat;           // [batch, Hkv, nbk, d] bf16 key means (scoring and correction)
+  uint16_t* vbar;           // [batch, Hkv, nbk, d] bf16 value means (correction)
 };
 
 struct KeptLists {
-  int32_t* idx;             // [batch, Hkv, nbmax, nbmax] ascending kept blocks per row
+  int32_t* idx;             // [batch, Hkv, nbmax, nbk] ascending kept blocks per row
   int32_t* cnt;             // [batch, Hkv, nbmax]
   int32_t* queue;           // work counter of the attention kernel; the kernel that
                             // builds the lists sets it to 0

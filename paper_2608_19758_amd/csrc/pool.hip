@@ -2,7 +2,8 @@
 // Eq. correction; Algorithm 1 step 2). HBM-bound: every K/V byte of the
 // sequence is read once with 16-byte loads through the page table.
 //
-// One workgroup per (key block J, KV head h, sequence b), 256 threads.
+// One workgroup per (key block J, KV head h, sequence b), 256 threads, over
+// the sequence's KV tokens (a prefix included).
 //  - bf16: thread (row group rg = tid/16, column chunk c = tid%16) sums tokens
 //    rg, rg+16, ... of the block for columns 8c..8c+7 in fp64. Every bf16
 //    value is exact in fp64 and so are the partial sums of realistic data, so
@@ -25,9 +26,9 @@ template <int FP8>
 __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
   const int J = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
-  const int64_t tok0 = p.cu[b];
-  const int L = p.cu[b + 1] - (int)tok0;
-  const int64_t obase = (((int64_t)b * p.hkv + h) * p.nbmax + J) * kHeadDim;
+  const int64_t tok0 = p.cuk[b];
+  const int L = p.cuk[b + 1] - (int)tok0;     // KV tokens, a prefix included
+  const int64_t obase = (((int64_t)b * p.hkv + h) * p.nbk + J) * kHeadDim;
   const int n = (L + kBlock - 1) / kBlock;
   if (J >= n) {
     if (tid < kHeadDim) {
@@ -124,8 +125,8 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
 }  // namespace
 
 hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s) {
-  if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
-  dim3 grid(p.nbmax, p.hkv, p.batch);
+  if (p.batch == 0 || p.nbk == 0) return hipSuccess;
+  dim3 grid(p.nbk, p.hkv, p.batch);
   if (p.fp8)
     pool_kernel<1><<<grid, kThreads, 0, s>>>(p, out);
   else

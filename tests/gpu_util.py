@@ -28,7 +28,8 @@ def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=
         window_blocks=sp.window_blocks if window is None else window,
         recent_blocks=sp.recent_blocks if recent is None else recent,
         mean_correction=sp.mean_correction if corr is None else corr,
-        softmax_scale=scale, dtype=sp.dtype)
+        softmax_scale=scale, dtype=sp.dtype,
+        max_kv_len=sp.max_kv_len if sp.prefix is not None else 0)
 
 
 def device_tensors(wl):
@@ -40,13 +41,20 @@ def device_tensors(wl):
     return d
 
 
+def kv_args(wl, d):
+    """Keyword arguments of the prefix KV lengths (none without a prefix)."""
+    if wl.spec.prefix is None:
+        return {}
+    return dict(cu_seqlens_k=d["cu_seqlens_k"], cu_seqlens_k_host=wl.cu_seqlens_k)
+
+
 def gpu_prefill(wl, p, d=None, want_lse=True):
     d = device_tensors(wl) if d is None else d
     out, mask, lse = fp2.prefill(p, d["q"], d["k_cache"], d["v_cache"], d["cu_seqlens"],
                                  d["block_table"] if wl.spec.page_size else None,
                                  cu_seqlens_host=wl.cu_seqlens,
                                  q_scale=d["q_scale"], k_scale=d["k_scale"], v_scale=d["v_scale"],
-                                 want_lse=want_lse)
+                                 want_lse=want_lse, **kv_args(wl, d))
     torch.cuda.synchronize()
     return (out.float().cpu().numpy().astype(np.float64), mask.cpu().numpy(),
             None if lse is None else lse.cpu().numpy().astype(np.float64))

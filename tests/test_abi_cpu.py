@@ -42,19 +42,24 @@ def test_workspace_bytes():
     assert want <= got <= want + 4 * 256
     assert fp2.workspace_bytes(base(head_dim=64)) == 0
     assert fp2.workspace_bytes(base(batch=0)) == 0
+    # prefix KV: pooled rows and list columns per key block, list rows per query block
+    pk = base(max_kv_len=3 * 4096, max_pages_per_seq=192)
+    nq, nk = 32, 96
+    want = 2 * 8 * (nk * 128 * 2 * 2 + nq * nk * 4 + nq * 4) + 256
+    assert want <= fp2.workspace_bytes(pk) <= want + 4 * 256
 
 
 FAKE = ctypes.c_void_p(0x100000)   # never dereferenced: validation fails first
 
 
 def call_prefill(p, **over):
-    args = dict(q=FAKE, cu=FAKE, cuh=None, k=FAKE, v=FAKE, bt=FAKE, qs=None, ks=None, vs=None,
-                out=FAKE, lse=None, mask=FAKE, ws=None, wsb=0)
+    args = dict(q=FAKE, cu=FAKE, cuh=None, cuk=None, cukh=None, k=FAKE, v=FAKE, bt=FAKE, qs=None,
+                ks=None, vs=None, out=FAKE, lse=None, mask=FAKE, ws=None, wsb=0)
     args.update(over)
-    return fp2.lib().fp2_prefill(ctypes.byref(p), args["q"], args["cu"], args["cuh"], args["k"],
-                                 args["v"], args["bt"], args["qs"], args["ks"], args["vs"],
-                                 args["out"], args["lse"], args["mask"], args["ws"], args["wsb"],
-                                 None)
+    return fp2.lib().fp2_prefill(ctypes.byref(p), args["q"], args["cu"], args["cuh"], args["cuk"],
+                                 args["cukh"], args["k"], args["v"], args["bt"], args["qs"],
+                                 args["ks"], args["vs"], args["out"], args["lse"], args["mask"],
+                                 args["ws"], args["wsb"], None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -75,6 +80,10 @@ def call_prefill(p, **over):
     (dict(mean_correction=2), fp2.EINVAL),
     (dict(dtype=7), fp2.EINVAL),
     (dict(batch=-1), fp2.EINVAL),
+    (dict(max_kv_len=-1), fp2.EINVAL),
+    (dict(max_kv_len=2048), fp2.EINVAL),                           # < max_seq_len
+    (dict(max_kv_len=8192), fp2.EINVAL),                           # needs 128 pages
+    (dict(max_kv_len=(1 << 20) + 1, max_pages_per_seq=1 << 15), fp2.EUNSUPPORTED),
 ])
 def test_invalid_params(kw, status):
     assert call_prefill(base(**kw)) == status
@@ -105,6 +114,27 @@ def test_host_lengths_checked():
     assert call_prefill(p, cuh=ctypes.c_void_p(bad2.ctypes.data)) == fp2.EINVAL
     bad3 = np.array([0, 10, 5], dtype=np.int32)
     assert call_prefill(p, cuh=ctypes.c_void_p(bad3.ctypes.data)) == fp2.EINVAL
+
+
+def test_host_kv_lengths_checked():
+    p = base(max_kv_len=8192, max_pages_per_seq=128)
+    cu = np.array([0, 300, 1000], dtype=np.int32)
+    host = lambda a: ctypes.c_void_p(a.ctypes.data)
+    good = np.array([0, 300 + 256, 556 + 700 + 384], dtype=np.int32)  # prefixes 256 and 384
+    assert call_prefill(p, cuh=host(cu), cuk=FAKE, cukh=host(good)) == fp2.EWORKSPACE
+    # host KV lengths without the device array
+    assert call_prefill(p, cuh=host(cu), cukh=host(good)) == fp2.EINVAL
+    # a prefix that is not a multiple of the block size
+    bad = np.array([0, 300 + 100, 400 + 700], dtype=np.int32)        # prefix 100
+    assert call_prefill(p, cuh=host(cu), cuk=FAKE, cukh=host(bad)) == fp2.EINVAL
+    assert "block_size" in fp2.last_error()
+    # fewer keys than queries
+    bad = np.array([0, 200, 900], dtype=np.int32)                    # 200 keys < 300 queries
+    assert call_prefill(p, cuh=host(cu), cuk=FAKE, cukh=host(bad)) == fp2.EINVAL
+    # a KV length over max_kv_len
+    bad = np.array([0, 300 + 8192, 8492 + 700], dtype=np.int32)
+    assert call_prefill(p, cuh=host(cu), cuk=FAKE, cukh=host(bad)) == fp2.EINVAL
+    assert "max_kv_len" in fp2.last_error()
 
 
 def test_noop_problems_return_ok():

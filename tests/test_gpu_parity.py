@@ -159,7 +159,7 @@ def test_empty_and_degenerate():
     p = fp2.make_params(batch=0, num_q_heads=4, num_kv_heads=1, max_seq_len=128)
     e = torch.empty(0, device="cuda")
     ws = torch.empty(256, dtype=torch.uint8, device="cuda")
-    st = fp2.lib().fp2_prefill(__import__("ctypes").byref(p), *([None] * 13), 0, None)
+    st = fp2.lib().fp2_prefill(__import__("ctypes").byref(p), *([None] * 15), 0, None)
     assert st == fp2.OK
     # a sequence of length 0 next to a length-1 sequence
     wl = synth.generate(spec([0, 1, 5], hq=4, hkv=2, page=4, seed=9))
