@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--variants", action="store_true",
                     help="also measure the other 128K variants (not part of the headline line)")
     ap.add_argument("--no-variants", action="store_true", help="(default; kept for old scripts)")
+    ap.add_argument("--chunked", action="store_true",
+                    help="also measure chunked prefill of the default workload (prefix KV) and "
+                         "its short tail chunks with and without KV splits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=64,
                     help="(sequence, KV head, query block) units the oracle runs for the CPU baseline")
@@ -190,6 +193,64 @@ def measure(cfg, steps, warmup):
     )
 
 
+def chunked(cfg, steps, warmup):
+    """Chunked prefill of the headline sequence: the same 128K tokens as
+    sequential calls over chunks of C tokens, chunk c attending to the c*C
+    tokens before it as a prefix KV (the serving mode of the paper's
+    chunked-prefill experiments), each chunk's total latency against the one
+    call; and short tail chunks (the last T tokens after a 128K - T prefix)
+    with the automatic KV splits against kv_splits = 1."""
+    import torch
+    import paper_2608_19758_amd as fp2
+    sp, wl, d = cfg["spec"], cfg["wl"], cfg["d"]
+    L = sp.seqlens[0]
+    bt = d["block_table"] if sp.page_size else None
+    dev = d["q"].device
+
+    def make(q0, q1, splits=0):
+        # queries q0..q1-1 after the q0 tokens before them
+        p = fp2.make_params(batch=1, num_q_heads=sp.num_q_heads, num_kv_heads=sp.num_kv_heads,
+                            max_seq_len=q1 - q0, page_size=sp.page_size,
+                            max_pages_per_seq=wl.max_pages, alpha=cfg["alpha"],
+                            sink_blocks=sp.sink_blocks, window_blocks=sp.window_blocks,
+                            recent_blocks=sp.recent_blocks, mean_correction=sp.mean_correction,
+                            dtype=sp.dtype, max_kv_len=q1, kv_splits=splits)
+        cu = torch.tensor([0, q1 - q0], dtype=torch.int32, device=dev)
+        cuk = torch.tensor([0, q1], dtype=torch.int32, device=dev)
+        q = d["q"][q0:q1]
+        out, mask, _ = fp2.alloc_outputs(p, q1 - q0)
+        ws = fp2.alloc_workspace(p)
+
+        def run():
+            fp2.prefill(p, q, d["k_cache"], d["v_cache"], cu, bt, cu_seqlens_k=cuk, out=out,
+                        block_mask=mask, workspace=ws, q_scale=d["q_scale"],
+                        k_scale=d["k_scale"], v_scale=d["v_scale"])
+        return run, p
+
+    res = {"chunks": [], "tails": []}
+    for C in (16384, 8192):
+        runs = [make(c, c + C)[0] for c in range(0, L, C)]
+
+        def all_chunks():
+            for r in runs:
+                r()
+        t, _ = time_loop(all_chunks, max(3, steps // 4), max(1, warmup // 2))
+        res["chunks"].append({"chunk": C, "calls": len(runs), "total_ms": round(t, 4)})
+        print("[bench] chunked %d x %d: %.3f ms" % (len(runs), C, t), file=sys.stderr, flush=True)
+        del runs
+    for T in (128, 1024, 4096):
+        run_auto, p = make(L - T, L)
+        run_one, _ = make(L - T, L, splits=1)
+        ta, _ = time_loop(run_auto, steps, warmup)
+        t1, _ = time_loop(run_one, steps, warmup)
+        res["tails"].append({"tail_tokens": T, "prefix": L - T, "kv_splits_auto": fp2.kv_splits(p),
+                             "ms_auto_splits": round(ta, 4), "ms_no_splits": round(t1, 4)})
+        print("[bench] tail %d: auto splits %.3f ms, none %.3f ms" % (T, ta, t1), file=sys.stderr,
+              flush=True)
+    torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(cfg, nunits):
     """The oracle on a bounded sample of the same workload: every KV head,
     query blocks at an even stride (heaviest included); estimation plus
@@ -250,6 +311,8 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, args.cpu_units)
         print("[bench] cpu baseline: %s" % cpu["sample"], file=sys.stderr, flush=True)
+
+    chunk_res = chunked(cfg, args.steps, args.warmup) if args.chunked else None
 
     variants = []
     if args.variants:
@@ -319,6 +382,8 @@ def main():
     }
     if variants:
         line["variants"] = variants
+    if chunk_res:
+        line["chunked_prefill"] = chunk_res
     print(json.dumps(line), flush=True)
 
 

@@ -4,6 +4,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <string>
 
 #include "fp2.h"
@@ -37,8 +38,22 @@ int nbk_of(const fp2_params_t* p) { return (max_kv_of(p) + fp2::kBlock - 1) / fp
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+constexpr int kMaxSplits = 64;
+constexpr int kAutoSplitItems = 1024;   // work items below which splits are added
+constexpr int kAutoMaxSplits = 16;
+
+// KV splits of every unit (Eq. split): the caller's count, or enough for
+// about kAutoSplitItems attention work items (at most kAutoMaxSplits).
+int splits_of(const fp2_params_t* p) {
+  if (p->kv_splits > 0) return p->kv_splits;
+  const int64_t items = (int64_t)p->batch * p->num_kv_heads * nbq_of(p) *
+                        fp2::attend_items_per_unit(p->num_q_heads / p->num_kv_heads);
+  if (items <= 0 || items >= kAutoSplitItems) return 1;
+  return (int)std::min<int64_t>(kAutoMaxSplits, kAutoSplitItems / items);
+}
+
 struct Layout {
-  size_t khat, vbar, kidx, kcnt, queue, total;
+  size_t khat, vbar, kidx, kcnt, queue, part_o, part_ml, total;
 };
 
 Layout layout_of(const fp2_params_t* p) {
@@ -57,6 +72,14 @@ Layout layout_of(const fp2_params_t* p) {
   off = align256(off + rows * sizeof(int32_t));
   l.queue = off;
   off += 256;
+  const int U = splits_of(p);
+  if (U > 1) {   // partials: per (unit, split) g*B packed rows of d fp32 and {m, l}
+    const size_t prow = rows * U * (size_t)(p->num_q_heads / p->num_kv_heads) * fp2::kBlock;
+    l.part_o = off;
+    off = align256(off + prow * fp2::kHeadDim * sizeof(float));
+    l.part_ml = off;
+    off = align256(off + prow * 2 * sizeof(float));
+  }
   l.total = rows ? off : 0;
   return l;
 }
@@ -99,6 +122,8 @@ fp2_status_t validate_params(const fp2_params_t* p) {
   if (!isfinite(p->softmax_scale)) return fail(FP2_EINVAL, "softmax_scale is not finite");
   if (p->dtype != FP2_BF16 && p->dtype != FP2_FP8_E4M3)
     return fail(FP2_EINVAL, "dtype %d unknown", p->dtype);
+  if (p->kv_splits < 0 || p->kv_splits > kMaxSplits)
+    return fail(FP2_EINVAL, "kv_splits %d not in [0, %d]", p->kv_splits, kMaxSplits);
   return FP2_OK;
 }
 
@@ -193,6 +218,7 @@ fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* c
   pr.window = p->window_blocks;
   pr.recent = p->recent_blocks;
   pr.corr = p->mean_correction;
+  pr.splits = splits_of(p);
   pr.alpha = p->alpha;
   const double scale = p->softmax_scale > 0.f ? (double)p->softmax_scale : 1.0 / sqrt((double)p->head_dim);
   pr.scale_log2 = (float)(scale * 1.4426950408889634074);
@@ -203,6 +229,7 @@ fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* c
 struct Views {
   fp2::Pooled pooled;
   fp2::KeptLists kl;
+  fp2::Partials part;
 };
 
 Views views_of(const fp2_params_t* p, void* ws) {
@@ -214,6 +241,8 @@ Views views_of(const fp2_params_t* p, void* ws) {
   v.kl.idx = (int32_t*)(base + l.kidx);
   v.kl.cnt = (int32_t*)(base + l.kcnt);
   v.kl.queue = (int32_t*)(base + l.queue);
+  v.part.o = l.part_o ? (float*)(base + l.part_o) : nullptr;
+  v.part.ml = l.part_ml ? (float*)(base + l.part_ml) : nullptr;
   return v;
 }
 
@@ -229,6 +258,11 @@ extern "C" {
 size_t fp2_workspace_bytes(const fp2_params_t* params) {
   if (validate_params(params) != FP2_OK) return 0;
   return layout_of(params).total;
+}
+
+int32_t fp2_kv_splits(const fp2_params_t* params) {
+  if (validate_params(params) != FP2_OK) return 0;
+  return splits_of(params);
 }
 
 fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
@@ -252,7 +286,8 @@ fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = fp2::launch_pool(pr, vw.pooled, s);
   if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s);
-  if (e == hipSuccess) e = fp2::launch_attend(pr, vw.pooled, block_mask, vw.kl, out, lse, s);
+  if (e == hipSuccess)
+    e = fp2::launch_attend(pr, vw.pooled, block_mask, vw.kl, vw.part, out, lse, s);
   return hip_status(e, "fp2_prefill launch");
 }
 
@@ -301,7 +336,8 @@ fp2_status_t fp2_attend(const fp2_params_t* params, const void* q, const int32_t
   hipError_t e = hipSuccess;
   if (params->mean_correction) e = fp2::launch_pool(pr, vw.pooled, s);
   if (e == hipSuccess) e = fp2::launch_compact(pr, block_mask_in, vw.kl, s);
-  if (e == hipSuccess) e = fp2::launch_attend(pr, vw.pooled, block_mask_in, vw.kl, out, lse, s);
+  if (e == hipSuccess)
+    e = fp2::launch_attend(pr, vw.pooled, block_mask_in, vw.kl, vw.part, out, lse, s);
   return hip_status(e, "fp2_attend launch");
 }
 

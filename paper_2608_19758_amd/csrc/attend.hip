@@ -594,7 +594,7 @@ __device__ __forceinline__ void run_steps(uint4* ring, int n, const uint8_t* Kb,
 template <int FP8, int W, int RT, int PIPE>
 __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled pooled,
                                                            const uint8_t* __restrict__ mask,
-                                                           KeptLists kl,
+                                                           KeptLists kl, Partials part,
                                                            uint16_t* __restrict__ out,
                                                            float* __restrict__ lse) {
   __shared__ uint4 ring[kRingU4];
@@ -604,14 +604,15 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
 
   constexpr int M = 32 * RT * W;            // packed rows per work item
   constexpr int NPRE = W > 4 ? 2 : 4;       // V^T key groups read ahead of the softmax
-  const int wpu = p0.g * kBlock / M;        // work items per unit
+  const int wpu = p0.g * kBlock / M;        // row slices per unit
+  const int ipu = wpu * p0.splits;          // work items per unit
   const int nbh = p0.batch * p0.hkv;
-  const int nitems = p0.nbmax * nbh * wpu;
+  const int nitems = p0.nbmax * nbh * ipu;
   const int tid0 = threadIdx.x;
 
-  // Persistent workgroups: items (unit, row slice) are taken from a counter
-  // in order of decreasing query block, i.e. heaviest first; the loop ends
-  // for every wave once the counter passes the last item.
+  // Persistent workgroups: items (unit, KV split, row slice) are taken from
+  // a counter in order of decreasing query block, i.e. heaviest first; the
+  // loop ends for every wave once the counter passes the last item.
 #pragma unroll 1
   for (;;) {
     if (tid0 == 0) s_item = atomicAdd(kl.queue, 1);
@@ -631,8 +632,9 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     asm volatile("" : "+s"(pk));
     KProblem& p = *pk;
 
-    const int u = item / wpu;
-    const int msub = item - u * wpu;
+    const int u = item / ipu;
+    const int sp = (item - u * ipu) / wpu;   // KV split of the unit
+    const int msub = item - u * ipu - sp * wpu;
     const int I = p.nbmax - 1 - u / nbh;
     const int bh = u % nbh;
     const int b = bh / p.hkv, h = bh % p.hkv;
@@ -688,6 +690,10 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       const int cnt = kl.cnt[row];
       const int32_t* kidx = kl.idx + row * p.nbk;
       const bool has_diag = cnt > 0 && kidx[cnt - 1] == Ia;
+      // Eq. split: split sp walks list positions [lo, hi) of the descending
+      // walk, ceil(cnt / splits) each
+      const int per = (cnt + p.splits - 1) / p.splits;
+      const int lo = min(cnt, sp * per), hi = min(cnt, lo + per);
       const int64_t rowbytes = (int64_t)p.hkv * kHeadDim * esz;     // one token slot of the pool
       const int64_t hbytes = (int64_t)h * kHeadDim * esz;
       const int page = p.pm.page, shift = p.pm.shift;
@@ -735,8 +741,8 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       const float cs = FP8 ? p.scale_log2 * qsc * ksc : p.scale_log2;
 
 #pragma unroll 1
-      for (int c0 = 0; c0 < cnt; c0 += chunk) {
-        const int nbc = min(chunk, cnt - c0);
+      for (int c0 = lo; c0 < hi; c0 += chunk) {
+        const int nbc = min(chunk, hi - c0);
         // Record (block i, half hf, group e) = {slot of its first row, that
         // row's index in the half, last valid row index}: row r of the half
         // then lives at slot + min(r, last) - first. Rows past the sequence
@@ -798,8 +804,11 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       for (int rt = 0; rt < RT; ++rt) rs.l[rt] += half == 0 ? rs.ls[rt][0] : 0.f;
     }
 
-    // ---- mean correction over the pruned blocks J < Ia, compacted into a list
-    if (p.corr && Ia > 0) {
+    // ---- mean correction over the pruned blocks J < Ia, compacted into a
+    // list; split sp takes the blocks J in [jlo, jhi)
+    const int perj = (Ia + p.splits - 1) / p.splits;
+    const int jlo = min(Ia, sp * perj), jhi = min(Ia, jlo + perj);
+    if (p.corr && jhi > jlo) {
       const uint8_t* mrow = mask + row * p.nbk;
       uint16_t* plist = (uint16_t*)aux;
       // Q as bf16 (fp8 codes widen exactly); the fp8 scale goes into cs.
@@ -835,8 +844,8 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       const uint8_t* Kh = (const uint8_t*)(pooled.khat + pbase);
       const uint8_t* Vh = (const uint8_t*)(pooled.vbar + pbase);
 #pragma unroll 1
-      for (int j0 = 0; j0 < Ia; j0 += kPlist) {
-        const int j1 = min(Ia, j0 + kPlist);
+      for (int j0 = jlo; j0 < jhi; j0 += kPlist) {
+        const int j1 = min(jhi, j0 + kPlist);
         // compaction of the pruned J in [j0, j1), in ascending order
         int np = 0;
 #pragma unroll 1
@@ -877,7 +886,28 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       }
     }
 
-    // epilogue: O = c_v O^T / l, LSE = (m + log2 l - off) ln 2
+    // epilogue: O = c_v O^T / l, LSE = (m + log2 l - off) ln 2; with KV
+    // splits the unnormalised partials go to the workspace instead
+    if (p.splits > 1) {
+      const int64_t slot = row * p.splits + sp;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const float l_tot = rs.l[rt] + __shfl_xor(rs.l[rt], 32, 64);
+        if (!qvalid[rt]) continue;
+        const int64_t prow = slot * (G * kBlock) + pr0 + 32 * rt;
+        float* po = part.o + prow * kHeadDim;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int d = 32 * dt + 8 * i + 4 * half;
+            *(float4*)(po + d) = make_float4(rs.o[rt][dt][4 * i + 0], rs.o[rt][dt][4 * i + 1],
+                                             rs.o[rt][dt][4 * i + 2], rs.o[rt][dt][4 * i + 3]);
+          }
+        if (half == 0) *(float2*)(part.ml + 2 * prow) = make_float2(rs.m[rt], l_tot);
+      }
+      continue;
+    }
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const float l_tot = rs.l[rt] + __shfl_xor(rs.l[rt], 32, 64);
@@ -900,6 +930,61 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
   }
 }
 
+// LSE-weighted merge of the KV splits of every unit (the combine implied by
+// Eq. split): M = max_u m_u, w_u = 2^(m_u - M), O = c_v sum_u w_u o_u /
+// sum_u w_u l_u, LSE = (M + log2 sum_u w_u l_u - off) ln 2. Splits that saw
+// no key have m_u = -inf and weight 0. Workgroup: 64 packed rows of one unit,
+// 32 lanes per row (4 values each). HBM-bound: splits x 520 B read and 256 B
+// written per row.
+template <int FP8>
+__global__ __launch_bounds__(256) void combine_kernel(Problem p, Partials part,
+                                                      uint16_t* __restrict__ out,
+                                                      float* __restrict__ lse) {
+  const int nbh = p.batch * p.hkv;
+  const int row = blockIdx.x;                     // (b * Hkv + h) * nbmax + I
+  const int I = row % p.nbmax, bh = row / p.nbmax;
+  const int b = bh / p.hkv, h = bh % p.hkv;
+  (void)nbh;
+  const int Lq = p.cu[b + 1] - p.cu[b];
+  const int G = p.g;
+  const int r = blockIdx.y * 64 + (threadIdx.x >> 5) * 8;   // first packed row of this half-wave
+  const int c = (threadIdx.x & 31) * 4;
+  const float vsc = FP8 ? p.v_scale[h] : 1.f;
+  const float off = FP8 ? 8.f : 0.f;
+  const int U = p.splits;
+#pragma unroll 1
+  for (int k = 0; k < 8; ++k) {
+    const int pr = r + k;
+    const int pos = I * kBlock + pr / G;
+    if (pr >= G * kBlock || pos >= Lq) continue;
+    const int hq = h * G + pr % G;
+    const int64_t base = ((int64_t)row * U) * (G * kBlock) + pr;   // slot row*U, packed row pr
+    const int64_t sstride = (int64_t)G * kBlock;
+    float M = -INFINITY;
+    for (int u = 0; u < U; ++u) M = fmaxf(M, part.ml[2 * (base + u * sstride)]);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float l = 0.f;
+    for (int u = 0; u < U; ++u) {
+      const float2 ml = *(const float2*)(part.ml + 2 * (base + u * sstride));
+      if (ml.x == -INFINITY) continue;
+      const float w = fast_exp2(ml.x - M);
+      const float4 o = *(const float4*)(part.o + (base + u * sstride) * kHeadDim + c);
+      acc.x = fmaf(w, o.x, acc.x);
+      acc.y = fmaf(w, o.y, acc.y);
+      acc.z = fmaf(w, o.z, acc.z);
+      acc.w = fmaf(w, o.w, acc.w);
+      l = fmaf(w, ml.y, l);
+    }
+    const float inv = vsc / l;
+    const int64_t t = (int64_t)p.cu[b] + pos;
+    uint2 v;
+    v.x = pack_bf16x2(acc.x * inv, acc.y * inv);
+    v.y = pack_bf16x2(acc.z * inv, acc.w * inv);
+    *(uint2*)(out + (t * p.hq + hq) * kHeadDim + c) = v;
+    if (lse && c == 0) lse[t * p.hq + hq] = (M + fast_log2(l) - off) * kLn2;
+  }
+}
+
 // Compute units of the current device (one resident workgroup each: the
 // kernel's LDS use admits one per CU).
 int device_cus() {
@@ -916,31 +1001,45 @@ int device_cus() {
 
 template <int FP8, int W, int RT, int PIPE>
 hipError_t launch_cfg(const Problem& p, const Pooled& pooled, const uint8_t* mask,
-                      const KeptLists& kl, void* out, float* lse, hipStream_t s) {
-  const int64_t nitems = (int64_t)p.nbmax * p.batch * p.hkv * (p.g * kBlock / (32 * RT * W));
+                      const KeptLists& kl, const Partials& part, void* out, float* lse,
+                      hipStream_t s) {
+  const int64_t nitems =
+      (int64_t)p.nbmax * p.batch * p.hkv * (p.g * kBlock / (32 * RT * W)) * p.splits;
   const int cus = device_cus();
   if (cus <= 0) return hipErrorInvalidDevice;
   const unsigned grid = (unsigned)std::min<int64_t>(nitems, cus);
-  attend_kernel<FP8, W, RT, PIPE><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, (uint16_t*)out, lse);
+  attend_kernel<FP8, W, RT, PIPE><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, part,
+                                                          (uint16_t*)out, lse);
+  if (p.splits > 1) {
+    const dim3 cgrid((unsigned)(p.nbmax * p.batch * p.hkv), (unsigned)(p.g * kBlock / 64));
+    combine_kernel<FP8><<<cgrid, 256, 0, s>>>(p, part, (uint16_t*)out, lse);
+  }
   return hipSuccess;
 }
 
+// 32 query rows per wave; 8 waves (two per SIMD) when the unit has at least
+// 256 packed rows, else 4.
+constexpr int waves_for(int g) { return g == 1 ? 4 : ATT_W; }
+
 template <int FP8>
 hipError_t launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask,
-                     const KeptLists& kl, void* out, float* lse, hipStream_t s) {
-  // 32 query rows per wave; 8 waves (two per SIMD) when the unit has at
-  // least 256 packed rows, else 4
-  if (p.g == 1) return launch_cfg<FP8, 4, 1, 0>(p, pooled, mask, kl, out, lse, s);
-  return launch_cfg<FP8, ATT_W, 1, ATT_PIPE>(p, pooled, mask, kl, out, lse, s);
+                     const KeptLists& kl, const Partials& part, void* out, float* lse,
+                     hipStream_t s) {
+  if (p.g == 1) return launch_cfg<FP8, waves_for(1), 1, 0>(p, pooled, mask, kl, part, out, lse, s);
+  return launch_cfg<FP8, ATT_W, 1, ATT_PIPE>(p, pooled, mask, kl, part, out, lse, s);
 }
 
 }  // namespace
 
+int attend_items_per_unit(int g) { return g * kBlock / (32 * waves_for(g)); }
+
 hipError_t launch_attend(const Problem& p, const Pooled& pooled, const uint8_t* mask,
-                         const KeptLists& kl, void* out, float* lse, hipStream_t s) {
+                         const KeptLists& kl, const Partials& part, void* out, float* lse,
+                         hipStream_t s) {
   if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
-  const hipError_t e = p.fp8 ? launch_dt<1>(p, pooled, mask, kl, out, lse, s)
-                             : launch_dt<0>(p, pooled, mask, kl, out, lse, s);
+  if (p.splits < 1 || (p.splits > 1 && (!part.o || !part.ml))) return hipErrorInvalidValue;
+  const hipError_t e = p.fp8 ? launch_dt<1>(p, pooled, mask, kl, part, out, lse, s)
+                             : launch_dt<0>(p, pooled, mask, kl, part, out, lse, s);
   return e != hipSuccess ? e : hipGetLastError();
 }
 

@@ -23,6 +23,7 @@ struct Problem {
   int32_t nbmax;            // query blocks per sequence bound (mask rows)
   int32_t nbk;              // key blocks per sequence bound (mask columns, pooled rows)
   int32_t sink, window, recent, corr;
+  int32_t splits;           // KV splits per unit (Eq. split), >= 1
   float alpha;
   float scale_log2;         // softmax_scale * log2(e)
   int32_t fp8;
@@ -41,11 +42,26 @@ struct KeptLists {
                             // builds the lists sets it to 0
 };
 
+// Partial results of the KV splits of each unit (used when splits > 1): for
+// unit row `row` = (b * Hkv + h) * nbmax + I and split u, slot row * splits + u
+// holds, per packed row r of the unit, the unnormalised accumulator o (fp32,
+// 128 values; value codes for fp8) and {m, l} (running maximum of the base-2
+// logits and the denominator).
+struct Partials {
+  float* o;                 // [rows * splits, g * B, d]
+  float* ml;                // [rows * splits, g * B, 2]
+};
+
+// Work items of the attention kernel per (sequence, KV head, query block),
+// before splitting: row slices of 32 * waves packed rows.
+int attend_items_per_unit(int g);
+
 hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s);
 hipError_t launch_estimate(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
                            hipStream_t s);
 hipError_t launch_compact(const Problem& p, const uint8_t* mask, KeptLists kl, hipStream_t s);
 hipError_t launch_attend(const Problem& p, const Pooled& pooled, const uint8_t* mask,
-                         const KeptLists& kl, void* out, float* lse, hipStream_t s);
+                         const KeptLists& kl, const Partials& part, void* out, float* lse,
+                         hipStream_t s);
 
 }  // namespace fp2

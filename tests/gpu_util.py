@@ -19,7 +19,7 @@ BAND = 1e-4                         # relative distance of a block energy from t
 LSE_TOL = {"bf16": 1e-2, "fp8": 0.0625}
 
 
-def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=0.0):
+def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=0.0, kv_splits=0):
     sp = wl.spec
     return fp2.make_params(
         batch=sp.batch, num_q_heads=sp.num_q_heads, num_kv_heads=sp.num_kv_heads,
@@ -29,7 +29,7 @@ def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=
         recent_blocks=sp.recent_blocks if recent is None else recent,
         mean_correction=sp.mean_correction if corr is None else corr,
         softmax_scale=scale, dtype=sp.dtype,
-        max_kv_len=sp.max_kv_len if sp.prefix is not None else 0)
+        max_kv_len=sp.max_kv_len if sp.prefix is not None else 0, kv_splits=kv_splits)
 
 
 def device_tensors(wl):

@@ -84,6 +84,8 @@ def call_prefill(p, **over):
     (dict(max_kv_len=2048), fp2.EINVAL),                           # < max_seq_len
     (dict(max_kv_len=8192), fp2.EINVAL),                           # needs 128 pages
     (dict(max_kv_len=(1 << 20) + 1, max_pages_per_seq=1 << 15), fp2.EUNSUPPORTED),
+    (dict(kv_splits=-1), fp2.EINVAL),
+    (dict(kv_splits=65), fp2.EINVAL),
 ])
 def test_invalid_params(kw, status):
     assert call_prefill(base(**kw)) == status
@@ -114,6 +116,29 @@ def test_host_lengths_checked():
     assert call_prefill(p, cuh=ctypes.c_void_p(bad2.ctypes.data)) == fp2.EINVAL
     bad3 = np.array([0, 10, 5], dtype=np.int32)
     assert call_prefill(p, cuh=ctypes.c_void_p(bad3.ctypes.data)) == fp2.EINVAL
+
+
+def test_workspace_with_kv_splits():
+    # forced splits: U partial slots of g*B packed rows (d fp32 + {m, l}) per unit
+    p = base(kv_splits=4)
+    rows, gB = 2 * 8 * 32, 4 * 128
+    plain = fp2.workspace_bytes(base())
+    want = plain + rows * 4 * gB * (128 * 4 + 8)
+    assert want <= fp2.workspace_bytes(p) <= want + 4 * 256
+    assert fp2.workspace_bytes(base(kv_splits=1)) == plain
+    # automatic: 1 * 8 heads * 8 query blocks * 2 row slices = 128 items -> 8 splits
+    small = dict(batch=1, max_seq_len=1024, max_kv_len=65536, max_pages_per_seq=1024)
+    rows, U = 8 * 8, 8
+    a = fp2.workspace_bytes(base(**small))
+    one = fp2.workspace_bytes(base(kv_splits=1, **small))
+    assert one + rows * U * gB * 520 <= a <= one + rows * U * gB * 520 + 2 * 256
+    # enough items: no splits
+    assert fp2.workspace_bytes(base(batch=4)) == fp2.workspace_bytes(base(batch=4, kv_splits=1))
+    assert fp2.kv_splits(base(**small)) == 8
+    assert fp2.kv_splits(base(batch=4)) == 1
+    assert fp2.kv_splits(base(kv_splits=5)) == 5
+    assert fp2.kv_splits(base(batch=1, num_q_heads=8, max_seq_len=128, max_pages_per_seq=2)) == 16
+    assert fp2.kv_splits(base(kv_splits=-3)) == 0
 
 
 def test_host_kv_lengths_checked():
