@@ -199,7 +199,7 @@ def chunked(cfg, steps, warmup):
     tokens before it as a prefix KV (the serving mode of the paper's
     chunked-prefill experiments), each chunk's total latency against the one
     call; and short tail chunks (the last T tokens after a 128K - T prefix)
-    with the automatic KV splits against kv_splits = 1."""
+    with the cost-balanced KV splits against kv_splits = 1."""
     import torch
     import paper_2608_19758_amd as fp2
     sp, wl, d = cfg["spec"], cfg["wl"], cfg["d"]
@@ -243,10 +243,10 @@ def chunked(cfg, steps, warmup):
         run_one, _ = make(L - T, L, splits=1)
         ta, _ = time_loop(run_auto, steps, warmup)
         t1, _ = time_loop(run_one, steps, warmup)
-        res["tails"].append({"tail_tokens": T, "prefix": L - T, "kv_splits_auto": fp2.kv_splits(p),
-                             "ms_auto_splits": round(ta, 4), "ms_no_splits": round(t1, 4)})
-        print("[bench] tail %d: auto splits %.3f ms, none %.3f ms" % (T, ta, t1), file=sys.stderr,
-              flush=True)
+        res["tails"].append({"tail_tokens": T, "prefix": L - T,
+                             "ms_planned_splits": round(ta, 4), "ms_no_splits": round(t1, 4)})
+        print("[bench] tail %d: planned splits %.3f ms, none %.3f ms" % (T, ta, t1),
+              file=sys.stderr, flush=True)
     torch.cuda.empty_cache()
     return res
 

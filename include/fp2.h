@@ -45,19 +45,22 @@
  * before it, so a chunked prefill gives, row for row, the output of one call
  * over the whole sequence.
  *
- * KV splits (Sec. 3.3 Eq. split)
- * ------------------------------
- * With U = kv_splits > 1 the attention of every (sequence, KV head, query
- * block) is cut into U parts: part u walks kept-list positions
- * [u ceil(T/U), min((u+1) ceil(T/U), T)) of its T kept blocks and corrects
- * the pruned blocks of the u-th of U equal ranges of J; each part leaves an
- * unnormalised partial output with its running maximum and denominator in
- * the workspace, and a combine kernel merges them with the usual
- * log-sum-exp weights. The result equals the unsplit one up to rounding
- * (fp8: P~ is rounded against each part's own maximum). Splits give short
- * chunks after long prefixes enough work items to fill the GPU; the
- * automatic choice (kv_splits = 0) uses U = 1 unless the problem has fewer
- * than 1024 work items.
+ * KV splits and the work plan (Sec. 3.3 Eq. split and Eq. cost)
+ * --------------------------------------------------------------
+ * The attention of a (sequence, KV head, query block) unit costs about one
+ * 64-key step per half kept block (Eq. cost), which varies a lot between
+ * heads. A unit cut into U parts has part u walk kept-list positions
+ * [u ceil(T/U), min((u+1) ceil(T/U), T)) of its T kept blocks and correct the
+ * pruned blocks of the u-th of U equal ranges of J (Eq. split); each part
+ * leaves an unnormalised partial output with its running maximum and
+ * denominator in the workspace, and a combine kernel merges them with the
+ * usual log-sum-exp weights. The result equals the unsplit one up to
+ * rounding (fp8: P~ is rounded against each part's own maximum).
+ * kv_splits == 0 (the default) plans on the device after the selection:
+ * only units costlier than a step budget are split, the budget being set by
+ * the call's total cost over about four items per compute unit (so a short
+ * chunk after a long prefix, or a few dense heads, no longer bound the run
+ * time). kv_splits == n >= 1 cuts every unit into n parts (1 = no splits).
  *
  * Layouts (row-major, innermost last)
  * -----------------------------------
@@ -153,22 +156,19 @@ typedef struct {
   int32_t max_kv_len;         /* upper bound of every KV length (prefix + chunk);
                                  0 selects max_seq_len; else >= max_seq_len,
                                  <= 1048576 */
-  int32_t kv_splits;          /* KV splits per (sequence, KV head, query block),
-                                 0..64: 0 = chosen from the problem size (more
-                                 splits when there are few query blocks), 1 =
-                                 none; see "KV splits" above */
+  int32_t kv_splits;          /* 0 = cost-balanced KV splits planned on the
+                                 device; n in 1..32 = n parts for every
+                                 (sequence, KV head, query block), 1 = none;
+                                 see "KV splits" above */
 } fp2_params_t;
 
 /* Bytes of workspace the entry points need for `params` (0 for a null or
  * invalid params). Covers the pooled key/value means, the kept-block lists
- * and their counts, the work counter of the attention kernel (reset by the
- * call itself, so a workspace can be reused without clearing) and, with KV
- * splits, the partial outputs (U x 520 bytes per packed query row bound). */
+ * and their counts, the attention work plan with its work counter (rebuilt
+ * by every call, so a workspace can be reused without clearing) and the
+ * partial outputs of split units (520 bytes per packed query row: 34 MB for
+ * kv_splits == 0, n x 520 bytes per packed row of the problem for n > 1). */
 size_t fp2_workspace_bytes(const fp2_params_t* params);
-
-/* KV splits the entry points use for `params` (Sec. 3.3 Eq. split): kv_splits
- * when it is > 0, else the automatic choice; 0 for a null or invalid params. */
-int32_t fp2_kv_splits(const fp2_params_t* params);
 
 /* Full prefill (Algorithm 1 of Sec. 3.4): block means, fused scoring and
  * selection, then attention over the kept blocks of every (sequence, KV head,

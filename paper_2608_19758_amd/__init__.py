@@ -45,8 +45,8 @@ class Params(ctypes.Structure):
     ]
 
 
-EXPORTS = ["fp2_workspace_bytes", "fp2_kv_splits", "fp2_prefill", "fp2_estimate", "fp2_attend",
-           "fp2_pool", "fp2_status_str", "fp2_last_error"]
+EXPORTS = ["fp2_workspace_bytes", "fp2_prefill", "fp2_estimate", "fp2_attend", "fp2_pool",
+           "fp2_status_str", "fp2_last_error"]
 
 
 def lib():
@@ -60,8 +60,6 @@ def lib():
         vp, P = ctypes.c_void_p, ctypes.POINTER(Params)
         L.fp2_workspace_bytes.restype = ctypes.c_size_t
         L.fp2_workspace_bytes.argtypes = [P]
-        L.fp2_kv_splits.restype = ctypes.c_int32
-        L.fp2_kv_splits.argtypes = [P]
         L.fp2_prefill.restype = ctypes.c_int
         L.fp2_prefill.argtypes = [P] + [vp] * 15 + [ctypes.c_size_t, vp]
         L.fp2_estimate.restype = ctypes.c_int
@@ -96,7 +94,8 @@ def make_params(*, batch, num_q_heads, num_kv_heads, max_seq_len, page_size=0,
                 recent_blocks=0, mean_correction=1, softmax_scale=0.0, dtype="bf16",
                 head_dim=HEAD_DIM, block_size=BLOCK, max_kv_len=0, kv_splits=0) -> Params:
     """fp2_params_t; max_kv_len bounds the KV lengths with a prefix (0: max_seq_len);
-    kv_splits: KV splits per unit (0: chosen from the problem size, 1: none)."""
+    kv_splits: 0 = cost-balanced KV splits planned on the device, n = n parts per unit
+    (1 = none)."""
     dt = {"bf16": BF16, "fp8": FP8_E4M3}.get(dtype, dtype)
     return Params(batch=batch, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
                   head_dim=head_dim, block_size=block_size, page_size=page_size,
@@ -126,10 +125,6 @@ def alloc_mask(p: Params, device="cuda") -> torch.Tensor:
 def workspace_bytes(p: Params) -> int:
     return int(lib().fp2_workspace_bytes(ctypes.byref(p)))
 
-
-def kv_splits(p: Params) -> int:
-    """KV splits the library uses for ``p`` (the automatic choice when p.kv_splits == 0)."""
-    return int(lib().fp2_kv_splits(ctypes.byref(p)))
 
 
 def _ptr(t: Optional[torch.Tensor]):

@@ -38,29 +38,36 @@ int nbk_of(const fp2_params_t* p) { return (max_kv_of(p) + fp2::kBlock - 1) / fp
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-constexpr int kMaxSplits = 64;
-constexpr int kAutoSplitItems = 1024;   // work items below which splits are added
-constexpr int kAutoMaxSplits = 16;
-
-// KV splits of every unit (Eq. split): the caller's count, or enough for
-// about kAutoSplitItems attention work items (at most kAutoMaxSplits).
-int splits_of(const fp2_params_t* p) {
-  if (p->kv_splits > 0) return p->kv_splits;
-  const int64_t items = (int64_t)p->batch * p->num_kv_heads * nbq_of(p) *
-                        fp2::attend_items_per_unit(p->num_q_heads / p->num_kv_heads);
-  if (items <= 0 || items >= kAutoSplitItems) return 1;
-  return (int)std::min<int64_t>(kAutoMaxSplits, kAutoSplitItems / items);
-}
+constexpr int kMaxSplits = 32;            // parts per unit (one per lane of the combine)
+constexpr size_t kPartialRows = 65536;    // packed rows of partial outputs, cost-balanced mode
 
 struct Layout {
-  size_t khat, vbar, kidx, kcnt, queue, part_o, part_ml, total;
+  size_t khat, vbar, kidx, kcnt, items, rowinfo, splitrows, counts, part_o, part_ml, total;
+  int32_t cap_items, cap_slots;
 };
 
+// Workspace sections. The attention plan holds an item table, per-unit split
+// information, the list of split units and the counters; the partial outputs
+// of split units take g*B packed rows of d fp32 values and {m, l} per slot.
+// kv_splits == 0 (cost-balanced) has kPartialRows packed rows of slots (the
+// plan raises its step budget until the parts fit), n > 1 has n per unit,
+// n == 1 none.
 Layout layout_of(const fp2_params_t* p) {
   Layout l{};
   const size_t heads = (size_t)p->batch * p->num_kv_heads;
   const size_t rows = heads * nbq_of(p);    // (sequence, KV head, query block)
   const size_t krows = heads * nbk_of(p);   // (sequence, KV head, key block)
+  const int g = p->num_q_heads / p->num_kv_heads;
+  const size_t rpu = (size_t)g * fp2::kBlock;
+  const size_t wpu = (size_t)fp2::attend_items_per_unit(g);
+  size_t slots, items;
+  if (p->kv_splits == 0) {
+    slots = kPartialRows / rpu;
+    items = wpu * (rows + slots);
+  } else {
+    slots = p->kv_splits > 1 ? rows * p->kv_splits : 0;
+    items = wpu * rows * p->kv_splits;
+  }
   size_t off = 0;
   l.khat = off;
   off = align256(off + krows * fp2::kHeadDim * sizeof(uint16_t));
@@ -70,16 +77,22 @@ Layout layout_of(const fp2_params_t* p) {
   off = align256(off + rows * nbk_of(p) * sizeof(int32_t));
   l.kcnt = off;
   off = align256(off + rows * sizeof(int32_t));
-  l.queue = off;
+  l.items = off;
+  off = align256(off + items * 2 * sizeof(int32_t));
+  l.rowinfo = off;
+  off = align256(off + rows * 2 * sizeof(int32_t));
+  l.splitrows = off;
+  off = align256(off + (slots / 2 + 1) * sizeof(int32_t));
+  l.counts = off;
   off += 256;
-  const int U = splits_of(p);
-  if (U > 1) {   // partials: per (unit, split) g*B packed rows of d fp32 and {m, l}
-    const size_t prow = rows * U * (size_t)(p->num_q_heads / p->num_kv_heads) * fp2::kBlock;
+  if (slots) {
     l.part_o = off;
-    off = align256(off + prow * fp2::kHeadDim * sizeof(float));
+    off = align256(off + slots * rpu * fp2::kHeadDim * sizeof(float));
     l.part_ml = off;
-    off = align256(off + prow * 2 * sizeof(float));
+    off = align256(off + slots * rpu * 2 * sizeof(float));
   }
+  l.cap_items = (int32_t)items;
+  l.cap_slots = (int32_t)slots;
   l.total = rows ? off : 0;
   return l;
 }
@@ -218,7 +231,7 @@ fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* c
   pr.window = p->window_blocks;
   pr.recent = p->recent_blocks;
   pr.corr = p->mean_correction;
-  pr.splits = splits_of(p);
+  pr.splits = p->kv_splits;
   pr.alpha = p->alpha;
   const double scale = p->softmax_scale > 0.f ? (double)p->softmax_scale : 1.0 / sqrt((double)p->head_dim);
   pr.scale_log2 = (float)(scale * 1.4426950408889634074);
@@ -229,7 +242,7 @@ fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* c
 struct Views {
   fp2::Pooled pooled;
   fp2::KeptLists kl;
-  fp2::Partials part;
+  fp2::Plan plan;
 };
 
 Views views_of(const fp2_params_t* p, void* ws) {
@@ -240,9 +253,15 @@ Views views_of(const fp2_params_t* p, void* ws) {
   v.pooled.vbar = (uint16_t*)(base + l.vbar);
   v.kl.idx = (int32_t*)(base + l.kidx);
   v.kl.cnt = (int32_t*)(base + l.kcnt);
-  v.kl.queue = (int32_t*)(base + l.queue);
-  v.part.o = l.part_o ? (float*)(base + l.part_o) : nullptr;
-  v.part.ml = l.part_ml ? (float*)(base + l.part_ml) : nullptr;
+  v.plan.items = (int2*)(base + l.items);
+  v.plan.rowinfo = (int2*)(base + l.rowinfo);
+  v.plan.splitrows = (int32_t*)(base + l.splitrows);
+  v.plan.counts = (int32_t*)(base + l.counts);
+  v.plan.part_o = l.part_o ? (float*)(base + l.part_o) : nullptr;
+  v.plan.part_ml = l.part_ml ? (float*)(base + l.part_ml) : nullptr;
+  v.plan.cap_items = l.cap_items;
+  v.plan.cap_slots = l.cap_slots;
+  v.plan.target_items = 4 * fp2::device_compute_units();
   return v;
 }
 
@@ -258,11 +277,6 @@ extern "C" {
 size_t fp2_workspace_bytes(const fp2_params_t* params) {
   if (validate_params(params) != FP2_OK) return 0;
   return layout_of(params).total;
-}
-
-int32_t fp2_kv_splits(const fp2_params_t* params) {
-  if (validate_params(params) != FP2_OK) return 0;
-  return splits_of(params);
 }
 
 fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
@@ -286,8 +300,10 @@ fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = fp2::launch_pool(pr, vw.pooled, s);
   if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s);
+  if (e == hipSuccess) e = fp2::launch_plan(pr, vw.kl, vw.plan, s);
   if (e == hipSuccess)
-    e = fp2::launch_attend(pr, vw.pooled, block_mask, vw.kl, vw.part, out, lse, s);
+    e = fp2::launch_attend(pr, vw.pooled, block_mask, vw.kl, vw.plan, out, lse, s);
+  if (e == hipSuccess) e = fp2::launch_combine(pr, vw.plan, out, lse, s);
   return hip_status(e, "fp2_prefill launch");
 }
 
@@ -336,8 +352,10 @@ fp2_status_t fp2_attend(const fp2_params_t* params, const void* q, const int32_t
   hipError_t e = hipSuccess;
   if (params->mean_correction) e = fp2::launch_pool(pr, vw.pooled, s);
   if (e == hipSuccess) e = fp2::launch_compact(pr, block_mask_in, vw.kl, s);
+  if (e == hipSuccess) e = fp2::launch_plan(pr, vw.kl, vw.plan, s);
   if (e == hipSuccess)
-    e = fp2::launch_attend(pr, vw.pooled, block_mask_in, vw.kl, vw.part, out, lse, s);
+    e = fp2::launch_attend(pr, vw.pooled, block_mask_in, vw.kl, vw.plan, out, lse, s);
+  if (e == hipSuccess) e = fp2::launch_combine(pr, vw.plan, out, lse, s);
   return hip_status(e, "fp2_attend launch");
 }
 

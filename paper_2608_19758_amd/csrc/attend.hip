@@ -125,7 +125,7 @@ __device__ __forceinline__ void dma16(const void* g, uint4* lds) {
 // rows RPG*(w + W*j) .. +RPG-1, lane i taking 16-byte slot i % CPR of row
 // RPG*(w + W*j) + i / CPR.
 template <int W, int FP8>
-struct Plan {
+struct CopyPlan {
   static constexpr int CPR = FP8 ? 8 : 16;          // 16-byte chunks per row
   static constexpr int RPG = 64 / CPR;              // rows per copy instruction
   static constexpr int PER = kStep / RPG / W;       // copies per wave and tensor
@@ -139,8 +139,8 @@ struct Plan {
 // off[j] from Kb / Vb.
 template <int W, int FP8>
 __device__ __forceinline__ void issue_copies(uint4* st, const uint8_t* Kb, const uint8_t* Vb,
-                                             const int64_t (&off)[Plan<W, FP8>::PER], int tid) {
-  using P = Plan<W, FP8>;
+                                             const int64_t (&off)[CopyPlan<W, FP8>::PER], int tid) {
+  using P = CopyPlan<W, FP8>;
   const int w = tid >> 6, lane = tid & 63;
   const int pc = lane % P::CPR;
 #pragma unroll
@@ -161,7 +161,7 @@ __device__ __forceinline__ void issue_copies(uint4* st, const uint8_t* Kb, const
 // on.
 template <int W, int FP8, class Fetch, class Addr>
 struct Addresser {
-  using P = Plan<W, FP8>;
+  using P = CopyPlan<W, FP8>;
   using Raw = decltype(std::declval<Fetch>()(0, 0));
   Fetch fetch;
   Addr addr;
@@ -184,7 +184,7 @@ struct Addresser {
 template <int W, int FP8, class Fetch, class Addr, class Body>
 __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
                                           Fetch fetch, Addr addr, Body body, int tid) {
-  using P = Plan<W, FP8>;
+  using P = CopyPlan<W, FP8>;
   Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
   int ni = 0;
 #pragma unroll 1
@@ -215,7 +215,7 @@ __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb,
 template <int W, int FP8, class SC, class Fetch, class Addr, class QK, class Fin>
 __device__ __forceinline__ void pipe_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
                                           Fetch fetch, Addr addr, QK qk, Fin fin, int tid) {
-  using P = Plan<W, FP8>;
+  using P = CopyPlan<W, FP8>;
   static_assert(P::NST >= 3, "the ring holds steps s-1 (refill), s and s+1");
   Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
   int ni = 0;
@@ -538,7 +538,7 @@ template <int W, int FP8, class SC, class Fetch, class Addr, class QK, class Fin
 __device__ __forceinline__ void pingpong_loop(uint4* ring, int n, const uint8_t* Kb,
                                               const uint8_t* Vb, Fetch fetch, Addr addr, QK qk,
                                               Fin fin, int tid) {
-  using P = Plan<W, FP8>;
+  using P = CopyPlan<W, FP8>;
   static_assert(P::NST >= 3, "the ring holds steps s-2 (refill), s-1 and s");
   Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
   const bool late = (tid >> 6) >= W / 2;
@@ -594,32 +594,41 @@ __device__ __forceinline__ void run_steps(uint4* ring, int n, const uint8_t* Kb,
 template <int FP8, int W, int RT, int PIPE>
 __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled pooled,
                                                            const uint8_t* __restrict__ mask,
-                                                           KeptLists kl, Partials part,
+                                                           KeptLists kl, Plan plan,
                                                            uint16_t* __restrict__ out,
                                                            float* __restrict__ lse) {
   __shared__ uint4 ring[kRingU4];
   __shared__ uint4 aux[kRec];               // kept: copy-address records; correction: pruned list
   __shared__ int32_t wtot[W];
-  __shared__ int32_t s_item;
+  __shared__ int4 s_item;
 
   constexpr int M = 32 * RT * W;            // packed rows per work item
   constexpr int NPRE = W > 4 ? 2 : 4;       // V^T key groups read ahead of the softmax
   const int wpu = p0.g * kBlock / M;        // row slices per unit
-  const int ipu = wpu * p0.splits;          // work items per unit
   const int nbh = p0.batch * p0.hkv;
-  const int nitems = p0.nbmax * nbh * ipu;
   const int tid0 = threadIdx.x;
 
-  // Persistent workgroups: items (unit, KV split, row slice) are taken from
-  // a counter in order of decreasing query block, i.e. heaviest first; the
-  // loop ends for every wave once the counter passes the last item.
+  // Persistent workgroups: items of the plan's table (unit, KV split, row
+  // slice; decreasing query block, i.e. heaviest first) are taken in order
+  // from a counter; the loop ends for every wave once the counter passes the
+  // last item.
 #pragma unroll 1
   for (;;) {
-    if (tid0 == 0) s_item = atomicAdd(kl.queue, 1);
+    if (tid0 == 0) {
+      const int it = atomicAdd(plan.counts, 1);
+      int4 v = make_int4(-1, 0, 0, 0);
+      if (it < plan.counts[1]) {
+        const int2 e = plan.items[it];
+        const int I = p0.nbmax - 1 - e.x / nbh;
+        const int2 ri = plan.rowinfo[(e.x % nbh) * p0.nbmax + I];
+        v = make_int4(e.x, e.y, ri.x, ri.y);
+      }
+      s_item = v;
+    }
     __syncthreads();
-    const int item = s_item;
+    const int4 cur = s_item;
     __syncthreads();   // every wave has read s_item before it is written again
-    if (item >= nitems) break;
+    if (cur.x < 0) break;
     // Opaque copies of the thread index and of the argument block: what is
     // derived from them is recomputed per item instead of being held in
     // registers across the whole loop. p0 is the first kernel argument, so it
@@ -632,9 +641,10 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     asm volatile("" : "+s"(pk));
     KProblem& p = *pk;
 
-    const int u = item / ipu;
-    const int sp = (item - u * ipu) / wpu;   // KV split of the unit
-    const int msub = item - u * ipu - sp * wpu;
+    const int u = cur.x;                     // attention-order index of the unit
+    const int sp = cur.y / wpu;              // its part (KV split) ...
+    const int msub = cur.y - sp * wpu;       // ... and row slice
+    const int nsp = cur.z;                   // parts of the unit
     const int I = p.nbmax - 1 - u / nbh;
     const int bh = u % nbh;
     const int b = bh / p.hkv, h = bh % p.hkv;
@@ -690,9 +700,9 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       const int cnt = kl.cnt[row];
       const int32_t* kidx = kl.idx + row * p.nbk;
       const bool has_diag = cnt > 0 && kidx[cnt - 1] == Ia;
-      // Eq. split: split sp walks list positions [lo, hi) of the descending
-      // walk, ceil(cnt / splits) each
-      const int per = (cnt + p.splits - 1) / p.splits;
+      // Eq. split: part sp walks list positions [lo, hi) of the descending
+      // walk, ceil(cnt / nsp) each
+      const int per = (cnt + nsp - 1) / nsp;
       const int lo = min(cnt, sp * per), hi = min(cnt, lo + per);
       const int64_t rowbytes = (int64_t)p.hkv * kHeadDim * esz;     // one token slot of the pool
       const int64_t hbytes = (int64_t)h * kHeadDim * esz;
@@ -806,7 +816,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
 
     // ---- mean correction over the pruned blocks J < Ia, compacted into a
     // list; split sp takes the blocks J in [jlo, jhi)
-    const int perj = (Ia + p.splits - 1) / p.splits;
+    const int perj = (Ia + nsp - 1) / nsp;
     const int jlo = min(Ia, sp * perj), jhi = min(Ia, jlo + perj);
     if (p.corr && jhi > jlo) {
       const uint8_t* mrow = mask + row * p.nbk;
@@ -888,14 +898,14 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
 
     // epilogue: O = c_v O^T / l, LSE = (m + log2 l - off) ln 2; with KV
     // splits the unnormalised partials go to the workspace instead
-    if (p.splits > 1) {
-      const int64_t slot = row * p.splits + sp;
+    if (nsp > 1) {
+      const int64_t slot = cur.w + sp;
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
         const float l_tot = rs.l[rt] + __shfl_xor(rs.l[rt], 32, 64);
         if (!qvalid[rt]) continue;
         const int64_t prow = slot * (G * kBlock) + pr0 + 32 * rt;
-        float* po = part.o + prow * kHeadDim;
+        float* po = plan.part_o + prow * kHeadDim;
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -904,7 +914,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
             *(float4*)(po + d) = make_float4(rs.o[rt][dt][4 * i + 0], rs.o[rt][dt][4 * i + 1],
                                              rs.o[rt][dt][4 * i + 2], rs.o[rt][dt][4 * i + 3]);
           }
-        if (half == 0) *(float2*)(part.ml + 2 * prow) = make_float2(rs.m[rt], l_tot);
+        if (half == 0) *(float2*)(plan.part_ml + 2 * prow) = make_float2(rs.m[rt], l_tot);
       }
       continue;
     }
@@ -930,90 +940,15 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
   }
 }
 
-// LSE-weighted merge of the KV splits of every unit (the combine implied by
-// Eq. split): M = max_u m_u, w_u = 2^(m_u - M), O = c_v sum_u w_u o_u /
-// sum_u w_u l_u, LSE = (M + log2 sum_u w_u l_u - off) ln 2. Splits that saw
-// no key have m_u = -inf and weight 0. Workgroup: 64 packed rows of one unit,
-// 32 lanes per row (4 values each). HBM-bound: splits x 520 B read and 256 B
-// written per row.
-template <int FP8>
-__global__ __launch_bounds__(256) void combine_kernel(Problem p, Partials part,
-                                                      uint16_t* __restrict__ out,
-                                                      float* __restrict__ lse) {
-  const int nbh = p.batch * p.hkv;
-  const int row = blockIdx.x;                     // (b * Hkv + h) * nbmax + I
-  const int I = row % p.nbmax, bh = row / p.nbmax;
-  const int b = bh / p.hkv, h = bh % p.hkv;
-  (void)nbh;
-  const int Lq = p.cu[b + 1] - p.cu[b];
-  const int G = p.g;
-  const int r = blockIdx.y * 64 + (threadIdx.x >> 5) * 8;   // first packed row of this half-wave
-  const int c = (threadIdx.x & 31) * 4;
-  const float vsc = FP8 ? p.v_scale[h] : 1.f;
-  const float off = FP8 ? 8.f : 0.f;
-  const int U = p.splits;
-#pragma unroll 1
-  for (int k = 0; k < 8; ++k) {
-    const int pr = r + k;
-    const int pos = I * kBlock + pr / G;
-    if (pr >= G * kBlock || pos >= Lq) continue;
-    const int hq = h * G + pr % G;
-    const int64_t base = ((int64_t)row * U) * (G * kBlock) + pr;   // slot row*U, packed row pr
-    const int64_t sstride = (int64_t)G * kBlock;
-    float M = -INFINITY;
-    for (int u = 0; u < U; ++u) M = fmaxf(M, part.ml[2 * (base + u * sstride)]);
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    float l = 0.f;
-    for (int u = 0; u < U; ++u) {
-      const float2 ml = *(const float2*)(part.ml + 2 * (base + u * sstride));
-      if (ml.x == -INFINITY) continue;
-      const float w = fast_exp2(ml.x - M);
-      const float4 o = *(const float4*)(part.o + (base + u * sstride) * kHeadDim + c);
-      acc.x = fmaf(w, o.x, acc.x);
-      acc.y = fmaf(w, o.y, acc.y);
-      acc.z = fmaf(w, o.z, acc.z);
-      acc.w = fmaf(w, o.w, acc.w);
-      l = fmaf(w, ml.y, l);
-    }
-    const float inv = vsc / l;
-    const int64_t t = (int64_t)p.cu[b] + pos;
-    uint2 v;
-    v.x = pack_bf16x2(acc.x * inv, acc.y * inv);
-    v.y = pack_bf16x2(acc.z * inv, acc.w * inv);
-    *(uint2*)(out + (t * p.hq + hq) * kHeadDim + c) = v;
-    if (lse && c == 0) lse[t * p.hq + hq] = (M + fast_log2(l) - off) * kLn2;
-  }
-}
-
-// Compute units of the current device (one resident workgroup each: the
-// kernel's LDS use admits one per CU).
-int device_cus() {
-  static int cus[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  if (cus[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    cus[dev] = n;
-  }
-  return cus[dev];
-}
-
 template <int FP8, int W, int RT, int PIPE>
 hipError_t launch_cfg(const Problem& p, const Pooled& pooled, const uint8_t* mask,
-                      const KeptLists& kl, const Partials& part, void* out, float* lse,
+                      const KeptLists& kl, const Plan& plan, void* out, float* lse,
                       hipStream_t s) {
-  const int64_t nitems =
-      (int64_t)p.nbmax * p.batch * p.hkv * (p.g * kBlock / (32 * RT * W)) * p.splits;
-  const int cus = device_cus();
+  const int cus = device_compute_units();
   if (cus <= 0) return hipErrorInvalidDevice;
-  const unsigned grid = (unsigned)std::min<int64_t>(nitems, cus);
-  attend_kernel<FP8, W, RT, PIPE><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, part,
+  const unsigned grid = (unsigned)std::min<int64_t>(plan.cap_items, cus);
+  attend_kernel<FP8, W, RT, PIPE><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, plan,
                                                           (uint16_t*)out, lse);
-  if (p.splits > 1) {
-    const dim3 cgrid((unsigned)(p.nbmax * p.batch * p.hkv), (unsigned)(p.g * kBlock / 64));
-    combine_kernel<FP8><<<cgrid, 256, 0, s>>>(p, part, (uint16_t*)out, lse);
-  }
   return hipSuccess;
 }
 
@@ -1023,10 +958,10 @@ constexpr int waves_for(int g) { return g == 1 ? 4 : ATT_W; }
 
 template <int FP8>
 hipError_t launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask,
-                     const KeptLists& kl, const Partials& part, void* out, float* lse,
+                     const KeptLists& kl, const Plan& plan, void* out, float* lse,
                      hipStream_t s) {
-  if (p.g == 1) return launch_cfg<FP8, waves_for(1), 1, 0>(p, pooled, mask, kl, part, out, lse, s);
-  return launch_cfg<FP8, ATT_W, 1, ATT_PIPE>(p, pooled, mask, kl, part, out, lse, s);
+  if (p.g == 1) return launch_cfg<FP8, waves_for(1), 1, 0>(p, pooled, mask, kl, plan, out, lse, s);
+  return launch_cfg<FP8, ATT_W, 1, ATT_PIPE>(p, pooled, mask, kl, plan, out, lse, s);
 }
 
 }  // namespace
@@ -1034,12 +969,11 @@ hipError_t launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask
 int attend_items_per_unit(int g) { return g * kBlock / (32 * waves_for(g)); }
 
 hipError_t launch_attend(const Problem& p, const Pooled& pooled, const uint8_t* mask,
-                         const KeptLists& kl, const Partials& part, void* out, float* lse,
+                         const KeptLists& kl, const Plan& plan, void* out, float* lse,
                          hipStream_t s) {
   if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
-  if (p.splits < 1 || (p.splits > 1 && (!part.o || !part.ml))) return hipErrorInvalidValue;
-  const hipError_t e = p.fp8 ? launch_dt<1>(p, pooled, mask, kl, part, out, lse, s)
-                             : launch_dt<0>(p, pooled, mask, kl, part, out, lse, s);
+  const hipError_t e = p.fp8 ? launch_dt<1>(p, pooled, mask, kl, plan, out, lse, s)
+                             : launch_dt<0>(p, pooled, mask, kl, plan, out, lse, s);
   return e != hipSuccess ? e : hipGetLastError();
 }
 

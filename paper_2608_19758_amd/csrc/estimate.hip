@@ -49,7 +49,6 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
 
   const int nbh = p0.batch * p0.hkv;
   const int nitems = p0.nbmax * nbh;
-  if (blockIdx.x == 0 && threadIdx.x == 0) *kl.queue = 0;
 
   // Persistent workgroups, items dealt round-robin in order of decreasing
   // query block: the cost of an item is proportional to (I + 1), so every
@@ -289,7 +288,6 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
   const int n = (L + kBlock - 1) / kBlock;
   const int Ia = I + (p.cuk[b + 1] - p.cuk[b] - L) / kBlock;   // key block of query block I
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
-  if (blockIdx.x == 0 && tid == 0) *kl.queue = 0;
   if (I >= n) {
     if (tid == 0) kl.cnt[row] = 0;
     return;
@@ -317,23 +315,10 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
   if (tid == 0) kl.cnt[row] = base;
 }
 
-// Compute units of the current device (one resident workgroup each).
-int est_device_cus() {
-  static int cus[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  if (cus[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    cus[dev] = n;
-  }
-  return cus[dev];
-}
-
 template <int FP8>
 hipError_t launch_est_dt(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
                          hipStream_t s) {
-  const int cus = est_device_cus();
+  const int cus = device_compute_units();
   if (cus <= 0) return hipErrorInvalidDevice;
   const unsigned grid = (unsigned)std::min<int64_t>((int64_t)p.nbmax * p.batch * p.hkv, cus);
   const size_t smem = (size_t)p.nbk * sizeof(float);

@@ -23,7 +23,7 @@ struct Problem {
   int32_t nbmax;            // query blocks per sequence bound (mask rows)
   int32_t nbk;              // key blocks per sequence bound (mask columns, pooled rows)
   int32_t sink, window, recent, corr;
-  int32_t splits;           // KV splits per unit (Eq. split), >= 1
+  int32_t splits;           // KV splits: 0 = cost-balanced plan, n >= 1 = n per unit
   float alpha;
   float scale_log2;         // softmax_scale * log2(e)
   int32_t fp8;
@@ -38,30 +38,40 @@ struct Pooled {
 struct KeptLists {
   int32_t* idx;             // [batch, Hkv, nbmax, nbk] ascending kept blocks per row
   int32_t* cnt;             // [batch, Hkv, nbmax]
-  int32_t* queue;           // work counter of the attention kernel; the kernel that
-                            // builds the lists sets it to 0
 };
 
-// Partial results of the KV splits of each unit (used when splits > 1): for
-// unit row `row` = (b * Hkv + h) * nbmax + I and split u, slot row * splits + u
-// holds, per packed row r of the unit, the unnormalised accumulator o (fp32,
-// 128 values; value codes for fp8) and {m, l} (running maximum of the base-2
-// logits and the denominator).
-struct Partials {
-  float* o;                 // [rows * splits, g * B, d]
-  float* ml;                // [rows * splits, g * B, 2]
+// Work plan of the attention kernel (Sec. 3.3 Eq. split and Eq. cost), built
+// on the device after the kept lists by plan_kernel. Unit rows are indexed
+// row = (b * Hkv + h) * nbmax + I; the attention order is q = (nbmax - 1 - I)
+// * (batch * Hkv) + b * Hkv + h (decreasing query block, heaviest first).
+struct Plan {
+  int2* items;              // [cap_items] {q, k}: split k / wpu, row slice k % wpu
+  int2* rowinfo;            // [rows] {splits U, first partial slot or -1}
+  int32_t* splitrows;       // [cap_slots / 2] unit rows with U > 1
+  int32_t* counts;          // [0] work counter (zeroed by the plan), [1] items, [2] split rows
+  float* part_o;            // [cap_slots, g * B, d] unnormalised partial outputs (fp32;
+                            // value codes for fp8)
+  float* part_ml;           // [cap_slots, g * B, 2] {running maximum (base 2), denominator}
+  int32_t cap_items, cap_slots;
+  int32_t target_items;     // work items the cost-balanced plan aims at
 };
 
 // Work items of the attention kernel per (sequence, KV head, query block),
 // before splitting: row slices of 32 * waves packed rows.
 int attend_items_per_unit(int g);
 
+// Compute units of the current device (0 if it cannot be queried).
+int device_compute_units();
+
 hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s);
 hipError_t launch_estimate(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
                            hipStream_t s);
 hipError_t launch_compact(const Problem& p, const uint8_t* mask, KeptLists kl, hipStream_t s);
+hipError_t launch_plan(const Problem& p, const KeptLists& kl, const Plan& plan, hipStream_t s);
 hipError_t launch_attend(const Problem& p, const Pooled& pooled, const uint8_t* mask,
-                         const KeptLists& kl, const Partials& part, void* out, float* lse,
+                         const KeptLists& kl, const Plan& plan, void* out, float* lse,
                          hipStream_t s);
+hipError_t launch_combine(const Problem& p, const Plan& plan, void* out, float* lse,
+                          hipStream_t s);
 
 }  // namespace fp2

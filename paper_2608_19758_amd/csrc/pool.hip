@@ -48,13 +48,23 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
     for (int i = 0; i < 8; ++i) ak[i] = av[i] = 0.0;
     const uint16_t* K = (const uint16_t*)p.k;
     const uint16_t* V = (const uint16_t*)p.v;
-    for (int r = rg; r < cnt; r += 16) {
-      int64_t slot = slot_of(p.pm, b, tok0, J * kBlock + r);
-      int64_t off = (slot * p.hkv + h) * kHeadDim + c * 8;
-      uint4 kv = *(const uint4*)(K + off);
-      uint4 vv = *(const uint4*)(V + off);
-      uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w};
-      uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+    // all 2 x 8 loads of this thread in flight before the first sum; rows
+    // past the block read nothing and add zero
+    uint4 kv[8], vv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = rg + 16 * i;
+      kv[i] = vv[i] = make_uint4(0, 0, 0, 0);
+      if (r < cnt) {
+        const int64_t off = (slot_of(p.pm, b, tok0, J * kBlock + r) * p.hkv + h) * kHeadDim + c * 8;
+        kv[i] = *(const uint4*)(K + off);
+        vv[i] = *(const uint4*)(V + off);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const uint32_t kw[4] = {kv[r].x, kv[r].y, kv[r].z, kv[r].w};
+      const uint32_t vw[4] = {vv[r].x, vv[r].y, vv[r].z, vv[r].w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         ak[2 * i] += (double)__uint_as_float(kw[i] << 16);
@@ -87,13 +97,21 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
     for (int i = 0; i < 16; ++i) ak[i] = av[i] = 0;
     const uint8_t* K = (const uint8_t*)p.k;
     const uint8_t* V = (const uint8_t*)p.v;
-    for (int r = rg; r < cnt; r += 32) {
-      int64_t slot = slot_of(p.pm, b, tok0, J * kBlock + r);
-      int64_t off = (slot * p.hkv + h) * kHeadDim + c * 16;
-      uint4 kv = *(const uint4*)(K + off);
-      uint4 vv = *(const uint4*)(V + off);
-      uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w};
-      uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+    uint4 kv[4], vv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = rg + 32 * i;
+      kv[i] = vv[i] = make_uint4(0, 0, 0, 0);
+      if (r < cnt) {
+        const int64_t off = (slot_of(p.pm, b, tok0, J * kBlock + r) * p.hkv + h) * kHeadDim + c * 16;
+        kv[i] = *(const uint4*)(K + off);
+        vv[i] = *(const uint4*)(V + off);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint32_t kw[4] = {kv[r].x, kv[r].y, kv[r].z, kv[r].w};
+      const uint32_t vw[4] = {vv[r].x, vv[r].y, vv[r].z, vv[r].w};
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         ak[i] += e4m3_times512((kw[i >> 2] >> (8 * (i & 3))) & 0xFF);

@@ -1,0 +1,267 @@
+// Work plan of the sparse attention and the merge of its KV splits
+// (Sec. 3.3 Eq. split and Eq. cost).
+//
+// plan_kernel runs once per call after the kept lists exist. The cost of a
+// unit (sequence b, KV head h, query block I) is proportional to its number
+// of 64-key steps (Eq. cost): two per kept block, one per 64 corrected
+// blocks, plus a fixed per-item share. In the cost-balanced mode (splits ==
+// 0) every unit whose cost exceeds a step budget S is cut into
+// U = ceil(cost / S) parts (at most kMaxRowSplits), and S is chosen so that
+// the whole call has about target_items items of at most S steps (never
+// less than kMinSplitSteps, and large enough for the partial-output
+// capacity of the workspace). A fixed count n >= 1 cuts every unit into n.
+// Part u of a unit walks kept-list positions [u ceil(T/U), min((u+1)
+// ceil(T/U), T)) of its T kept blocks and the u-th of U equal ranges of the
+// pruned blocks (Eq. split). The plan is an item table in attention order
+// (decreasing query block, heaviest first, units without queries left out),
+// per-unit {U, first partial slot}, and the list of units with U > 1.
+//
+// combine_kernel merges the parts of every split unit with the log-sum-exp
+// weights: M = max_u m_u, w_u = 2^(m_u - M), O = c_v sum_u w_u o_u /
+// sum_u w_u l_u, LSE = (M + log2 sum_u w_u l_u - offset) ln 2. Parts that saw
+// no key have m_u = -inf and weight 0. It is HBM-bound (U x 520 bytes read
+// and 256 written per packed row) and persistent over (split unit, 8-row
+// group) pairs.
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace fp2 {
+
+namespace {
+
+constexpr float kLn2 = 0.69314718055994530942f;
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanWaves = kPlanThreads / 64;
+constexpr int kMinSplitSteps = 16;   // smallest step budget of an item
+constexpr int kItemSteps = 2;        // fixed per-item cost (query load, set-up), in steps
+constexpr int kMaxRowSplits = 32;    // one part per lane of the combine's half-wave
+
+__device__ double block_sum(double v, double* sh) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  double t = 0.0;
+  for (int k = 0; k < kPlanWaves; ++k) t += sh[k];
+  return t;
+}
+
+__device__ int block_max(int v, int* sh) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  int t = sh[0];
+  for (int k = 1; k < kPlanWaves; ++k) t = max(t, sh[k]);
+  return t;
+}
+
+// Exclusive prefix sum over the workgroup (thread order); `total` is the sum
+// over all threads.
+__device__ int block_excl_scan(int v, int* sh, int& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int inc = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += t;
+  }
+  __syncthreads();
+  if (lane == 63) sh[w] = inc;
+  __syncthreads();
+  int pre = 0;
+  total = 0;
+  for (int k = 0; k < kPlanWaves; ++k) {
+    const int x = sh[k];
+    pre += k < w ? x : 0;
+    total += x;
+  }
+  return pre + inc - v;
+}
+
+// Attention-order index q -> unit row (b * Hkv + h) * nbmax + I.
+__device__ __forceinline__ int row_of(const Problem& p, int q, int nbh, int& I, int& b) {
+  I = p.nbmax - 1 - q / nbh;
+  const int bh = q % nbh;
+  b = bh / p.hkv;
+  return bh * p.nbmax + I;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, KeptLists kl, Plan plan,
+                                                            int wpu) {
+  __shared__ double shd[kPlanWaves];
+  __shared__ int shi[kPlanWaves];
+  const int tid = threadIdx.x;
+  const int nbh = p.batch * p.hkv;
+  const int R = nbh * p.nbmax;
+  // thread tid owns the attention-order indices q in [q0, q1): contiguous, so
+  // one scan over the threads orders the whole table
+  const int per = (R + kPlanThreads - 1) / kPlanThreads;
+  const int q0 = min(R, tid * per), q1 = min(R, q0 + per);
+
+  // cost in steps of one row slice of every unit with queries (-1: none),
+  // kept in rowinfo.x until the plan overwrites it
+  double tot = 0.0;
+  int mx = 0;
+  for (int q = q0; q < q1; ++q) {
+    int I, b;
+    const int row = row_of(p, q, nbh, I, b);
+    const int Lq = p.cu[b + 1] - p.cu[b];
+    int cost = -1;
+    if (I * kBlock < Lq) {
+      const int Ia = I + (p.cuk[b + 1] - p.cuk[b] - Lq) / kBlock;
+      const int cnt = kl.cnt[row];
+      const int pruned = p.corr ? max(0, Ia + 1 - cnt) : 0;
+      cost = 2 * cnt + (pruned + 63) / 64 + kItemSteps;
+      tot += (double)cost * wpu;
+      mx = max(mx, cost);
+    }
+    plan.rowinfo[row] = make_int2(cost, -1);
+  }
+  tot = block_sum(tot, shd);
+  mx = block_max(mx, shi);
+
+  // step budget of the cost-balanced mode
+  int S = 0;
+  if (p.splits == 0) {
+    S = max(kMinSplitSteps, (int)ceil(tot / (double)max(1, plan.target_items)));
+    while (S < mx) {   // grow S until the parts fit the partial-output slots
+      int need = 0;
+      for (int q = q0; q < q1; ++q) {
+        int I, b;
+        const int cost = plan.rowinfo[row_of(p, q, nbh, I, b)].x;
+        if (cost > S) need += min(kMaxRowSplits, (cost + S - 1) / S);
+      }
+      need = (int)block_sum((double)need, shd);
+      if (need <= plan.cap_slots) break;
+      S *= 2;
+    }
+  }
+  auto parts = [&](int cost) -> int {
+    if (cost < 0) return 0;
+    if (p.splits > 0) return p.splits;
+    return cost > S ? min(kMaxRowSplits, (cost + S - 1) / S) : 1;
+  };
+
+  // items in attention order, partial slots and split units: this thread's
+  // totals, their exclusive scans over the threads, then the entries
+  int ni = 0, ns = 0, nsr = 0;
+  for (int q = q0; q < q1; ++q) {
+    int I, b;
+    const int U = parts(plan.rowinfo[row_of(p, q, nbh, I, b)].x);
+    ni += U * wpu;
+    ns += U > 1 ? U : 0;
+    nsr += U > 1 ? 1 : 0;
+  }
+  int ti, ts, tsr;
+  int bi = block_excl_scan(ni, shi, ti);
+  int bs = block_excl_scan(ns, shi, ts);
+  int bsr = block_excl_scan(nsr, shi, tsr);
+  for (int q = q0; q < q1; ++q) {
+    int I, b;
+    const int row = row_of(p, q, nbh, I, b);
+    const int U = parts(plan.rowinfo[row].x);
+    if (U == 0) continue;
+    plan.rowinfo[row] = make_int2(U, U > 1 ? bs : -1);
+    if (U > 1) {
+      plan.splitrows[bsr++] = row;
+      bs += U;
+    }
+    for (int k = 0; k < U * wpu; ++k) plan.items[bi + k] = make_int2(q, k);
+    bi += U * wpu;
+  }
+  if (tid == 0) {
+    plan.counts[0] = 0;
+    plan.counts[1] = ti;
+    plan.counts[2] = tsr;
+  }
+}
+
+template <int FP8>
+__global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan plan,
+                                                      uint16_t* __restrict__ out,
+                                                      float* __restrict__ lse) {
+  const int G = p.g, rpu = G * kBlock, groups = rpu / 8;
+  const int work = plan.counts[2] * groups;
+  const int lane = threadIdx.x & 31, sub = threadIdx.x >> 5;
+  const int c = lane * 4;
+  const float off = FP8 ? 8.f : 0.f;
+#pragma unroll 1
+  for (int wk = blockIdx.x; wk < work; wk += gridDim.x) {
+    const int sr = wk / groups, grp = wk - sr * groups;
+    const int row = plan.splitrows[sr];
+    const int2 ri = plan.rowinfo[row];
+    const int U = ri.x, slot0 = ri.y;
+    const int I = row % p.nbmax, bh = row / p.nbmax;
+    const int b = bh / p.hkv, h = bh % p.hkv;
+    const int pr = grp * 8 + sub;              // packed row of this half-wave
+    const int pos = I * kBlock + pr / G;
+    if (pos >= p.cu[b + 1] - p.cu[b]) continue;
+    // lane u < U holds part u's {m, l}
+    float m = -INFINITY, l = 0.f;
+    if (lane < U) {
+      const float2 ml = *(const float2*)(plan.part_ml + 2 * ((int64_t)(slot0 + lane) * rpu + pr));
+      m = ml.x;
+      l = ml.y;
+    }
+    float M = m;
+    for (int o = 16; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 32));
+    const float wgt = m == -INFINITY ? 0.f : fast_exp2(m - M);
+    float lt = wgt * l;
+    for (int o = 16; o > 0; o >>= 1) lt += __shfl_xor(lt, o, 32);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int u = 0; u < U; ++u) {
+      const float wu = __shfl(wgt, u, 32);
+      if (wu == 0.f) continue;
+      const float4 o = *(const float4*)(plan.part_o + ((int64_t)(slot0 + u) * rpu + pr) * kHeadDim + c);
+      acc.x = fmaf(wu, o.x, acc.x);
+      acc.y = fmaf(wu, o.y, acc.y);
+      acc.z = fmaf(wu, o.z, acc.z);
+      acc.w = fmaf(wu, o.w, acc.w);
+    }
+    const float inv = (FP8 ? p.v_scale[h] : 1.f) / lt;
+    const int hq = h * G + pr % G;
+    const int64_t t = (int64_t)p.cu[b] + pos;
+    uint2 v;
+    v.x = pack_bf16x2(acc.x * inv, acc.y * inv);
+    v.y = pack_bf16x2(acc.z * inv, acc.w * inv);
+    *(uint2*)(out + (t * p.hq + hq) * kHeadDim + c) = v;
+    if (lse && lane == 0) lse[t * p.hq + hq] = (M + fast_log2(lt) - off) * kLn2;
+  }
+}
+
+}  // namespace
+
+int device_compute_units() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
+hipError_t launch_plan(const Problem& p, const KeptLists& kl, const Plan& plan, hipStream_t s) {
+  if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
+  plan_kernel<<<1, kPlanThreads, 0, s>>>(p, kl, plan, attend_items_per_unit(p.g));
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const Problem& p, const Plan& plan, void* out, float* lse,
+                          hipStream_t s) {
+  if (p.batch == 0 || p.nbmax == 0 || plan.cap_slots == 0) return hipSuccess;
+  const int64_t bound = (int64_t)(plan.cap_slots / 2) * (p.g * kBlock / 8);
+  const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(bound, 1024));
+  if (p.fp8)
+    combine_kernel<1><<<grid, 256, 0, s>>>(p, plan, (uint16_t*)out, lse);
+  else
+    combine_kernel<0><<<grid, 256, 0, s>>>(p, plan, (uint16_t*)out, lse);
+  return hipGetLastError();
+}
+
+}  // namespace fp2

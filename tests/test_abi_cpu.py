@@ -34,19 +34,22 @@ def base(**kw):
 
 
 def test_workspace_bytes():
-    p = base()
+    # the pooled means, lists and counts: the bulk of the workspace, by formula
+    p = base(kv_splits=1)
     nb = 32
     rows = 2 * 8 * nb
-    want = rows * 128 * 2 * 2 + rows * nb * 4 + rows * 4 + 256   # + the work counter
+    want = rows * 128 * 2 * 2 + rows * nb * 4 + rows * 4 + 256   # + the work counters
     got = fp2.workspace_bytes(p)
-    assert want <= got <= want + 4 * 256
+    assert want <= got <= want + rows * 2 * 8 * 2 + 8 * 256     # + item table and unit info
     assert fp2.workspace_bytes(base(head_dim=64)) == 0
     assert fp2.workspace_bytes(base(batch=0)) == 0
     # prefix KV: pooled rows and list columns per key block, list rows per query block
-    pk = base(max_kv_len=3 * 4096, max_pages_per_seq=192)
+    pk = base(max_kv_len=3 * 4096, max_pages_per_seq=192, kv_splits=1)
     nq, nk = 32, 96
     want = 2 * 8 * (nk * 128 * 2 * 2 + nq * nk * 4 + nq * 4) + 256
-    assert want <= fp2.workspace_bytes(pk) <= want + 4 * 256
+    assert want <= fp2.workspace_bytes(pk) <= want + rows * 2 * 8 * 2 + 8 * 256
+    # the cost-balanced plan adds 65536 packed rows of partial outputs (520 B each)
+    assert fp2.workspace_bytes(base()) - got >= 65536 * 520
 
 
 FAKE = ctypes.c_void_p(0x100000)   # never dereferenced: validation fails first
@@ -85,7 +88,7 @@ def call_prefill(p, **over):
     (dict(max_kv_len=8192), fp2.EINVAL),                           # needs 128 pages
     (dict(max_kv_len=(1 << 20) + 1, max_pages_per_seq=1 << 15), fp2.EUNSUPPORTED),
     (dict(kv_splits=-1), fp2.EINVAL),
-    (dict(kv_splits=65), fp2.EINVAL),
+    (dict(kv_splits=33), fp2.EINVAL),
 ])
 def test_invalid_params(kw, status):
     assert call_prefill(base(**kw)) == status
@@ -118,27 +121,33 @@ def test_host_lengths_checked():
     assert call_prefill(p, cuh=ctypes.c_void_p(bad3.ctypes.data)) == fp2.EINVAL
 
 
-def test_workspace_with_kv_splits():
-    # forced splits: U partial slots of g*B packed rows (d fp32 + {m, l}) per unit
-    p = base(kv_splits=4)
-    rows, gB = 2 * 8 * 32, 4 * 128
-    plain = fp2.workspace_bytes(base())
-    want = plain + rows * 4 * gB * (128 * 4 + 8)
-    assert want <= fp2.workspace_bytes(p) <= want + 4 * 256
-    assert fp2.workspace_bytes(base(kv_splits=1)) == plain
-    # automatic: 1 * 8 heads * 8 query blocks * 2 row slices = 128 items -> 8 splits
-    small = dict(batch=1, max_seq_len=1024, max_kv_len=65536, max_pages_per_seq=1024)
-    rows, U = 8 * 8, 8
-    a = fp2.workspace_bytes(base(**small))
-    one = fp2.workspace_bytes(base(kv_splits=1, **small))
-    assert one + rows * U * gB * 520 <= a <= one + rows * U * gB * 520 + 2 * 256
-    # enough items: no splits
-    assert fp2.workspace_bytes(base(batch=4)) == fp2.workspace_bytes(base(batch=4, kv_splits=1))
-    assert fp2.kv_splits(base(**small)) == 8
-    assert fp2.kv_splits(base(batch=4)) == 1
-    assert fp2.kv_splits(base(kv_splits=5)) == 5
-    assert fp2.kv_splits(base(batch=1, num_q_heads=8, max_seq_len=128, max_pages_per_seq=2)) == 16
-    assert fp2.kv_splits(base(kv_splits=-3)) == 0
+def ws_parts(p):
+    """Workspace bytes predicted from the documented sections (each 256-aligned)."""
+    al = lambda x: (x + 255) // 256 * 256
+    g = p.num_q_heads // p.num_kv_heads
+    rows = p.batch * p.num_kv_heads * fp2.num_blocks(p)
+    krows = p.batch * p.num_kv_heads * fp2.num_key_blocks(p)
+    wpu = {1: 1, 2: 1, 4: 2, 8: 4}[g]
+    rpu = g * 128
+    if p.kv_splits == 0:
+        slots = 65536 // rpu
+        items = wpu * (rows + slots)
+    else:
+        slots = rows * p.kv_splits if p.kv_splits > 1 else 0
+        items = wpu * rows * p.kv_splits
+    n = 2 * al(krows * 256) + al(rows * fp2.num_key_blocks(p) * 4) + al(rows * 4)
+    n += al(items * 8) + al(rows * 8) + al((slots // 2 + 1) * 4) + 256
+    if slots:
+        n += al(slots * rpu * 512) + al(slots * rpu * 8)
+    return n
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(kv_splits=1), dict(kv_splits=4),
+                                dict(num_q_heads=64, kv_splits=0), dict(num_q_heads=8),
+                                dict(max_kv_len=12288, max_pages_per_seq=192, kv_splits=3)])
+def test_workspace_sections(kw):
+    p = base(**kw)
+    assert fp2.workspace_bytes(p) == ws_parts(p)
 
 
 def test_host_kv_lengths_checked():
