@@ -48,7 +48,7 @@ def parse():
                     help="also measure chunked prefill of the default workload (prefix KV) and "
                          "its short tail chunks with and without KV splits")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=64,
+    ap.add_argument("--cpu-units", type=int, default=160,
                     help="(sequence, KV head, query block) units the oracle runs for the CPU baseline")
     ap.add_argument("--profile-only", action="store_true",
                     help="only run the timed loop of the default workload (for rocprofv3)")
