@@ -272,12 +272,23 @@ struct Scores {
   f32x16_t v[RT][2];
 };
 
-// Online-softmax rescale of row tile rt to the new running maximum of the
-// raw scores s (-inf where masked); the logits are x = cs * s + shift (log2
-// units, cs > 0). Returns the bias b with x - m + off = cs * s + b.
+// Lazy rescale thresholds (log2 units): the running maximum m of a row is
+// only moved when a new logit exceeds it by more than tau, so probabilities
+// reach 2^(off + tau). fp8 keeps P~ = e4m3(2^8 exp(x - m)) within the e4m3
+// range: 2^(8 + 0.8) = 445.7 < 448. bf16 probabilities stay far from any
+// limit at 2^(8 + 8).
+constexpr float kTauFp8 = 0.8f;
+constexpr float kTauBf16 = 8.0f;
+
+// Online-softmax rescale of row tile rt for the raw scores s (-inf where
+// masked); the logits are x = cs * s + shift (log2 units, cs > 0). The
+// running maximum moves to the new row maximum only if that exceeds it by
+// more than tau (any finite value moves it from -inf); the accumulators are
+// rescaled only when some row of the wave moved. Returns the bias b with
+// x - m + off = cs * s + b.
 template <int NU, bool LS, int RT>
 __device__ __forceinline__ float softmax_rescale(const f32x16_t (&s)[NU], RowState<RT>& rs, int rt,
-                                                 float cs, float shift, float off) {
+                                                 float cs, float shift, float off, float tau) {
   float mr = -INFINITY;
 #pragma unroll
   for (int u = 0; u < NU; ++u)
@@ -285,12 +296,13 @@ __device__ __forceinline__ float softmax_rescale(const f32x16_t (&s)[NU], RowSta
     for (int e = 0; e < 16; ++e) mr = fmaxf(mr, s[u][e]);
   mr = xhalf_max(mr);
   const float mx = mr == -INFINITY ? -INFINITY : fmaf(mr, cs, shift);
-  // m_new stays -inf only while no key of this row has been visible; the
-  // update is then the identity (scale 1, p = 0), without branching the
-  // wave away from the MFMAs that follow.
-  const float m_new = fmaxf(rs.m[rt], mx);
+  // m stays -inf only while no key of this row has been visible; the update
+  // is then the identity (scale 1, p = 0), without branching the wave away
+  // from the MFMAs that follow.
+  const bool up = mx > rs.m[rt] + tau;
+  const float m_new = up ? mx : rs.m[rt];
   const float m_use = m_new == -INFINITY ? 0.f : m_new;
-  if (__any(m_new != rs.m[rt])) {
+  if (__any(up)) {
     const float a = fast_exp2(rs.m[rt] - m_use);
     rs.l[rt] *= a;
     if (LS) rs.ls[rt][0] *= a;   // the only element of the row-sum tile that is read
@@ -395,7 +407,8 @@ __device__ __forceinline__ void fin_bf16(const uint4* st, Scores<RT>& S, RowStat
     }
     // KIND 1: the PV weight pv_scale (> 0) enters the exponent as log2
     // pv_scale, and the row sum divides it out once.
-    const float bias = softmax_rescale<2, false>(S.v[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off) +
+    const float bias = softmax_rescale<2, false>(S.v[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off,
+                                                 kTauBf16) +
                        (KIND == 1 ? lg_pv : 0.f);
     float pv[2][16];
 #pragma unroll
@@ -509,7 +522,7 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
             s[rt][u][4 * i + j] = (key0 + key > pos[rt]) ? -INFINITY : s[rt][u][4 * i + j];
           }
     }
-    const float bias = softmax_rescale<2, true>(s[rt], rs, rt, cs, 0.0f, 8.0f);
+    const float bias = softmax_rescale<2, true>(s[rt], rs, rt, cs, 0.0f, 8.0f, kTauFp8);
     int pk[8];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
