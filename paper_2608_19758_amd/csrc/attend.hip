@@ -846,14 +846,8 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
               v = *(const uint4*)((const uint16_t*)p.q + qoff[rt] + 16 * ds + 8 * half);
             } else {
               const uint2 cc = *(const uint2*)((const uint8_t*)p.q + qoff[rt] + 16 * ds + 8 * half);
-              const uint32_t wv[2] = {cc.x, cc.y};
-              uint32_t ow[4];
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const uint32_t src = wv[i >> 1] >> (16 * (i & 1));
-                ow[i] = e4m3_to_bf16(src & 0xFF) | (e4m3_to_bf16((src >> 8) & 0xFF) << 16);
-              }
-              v = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+              const uint2 lo = e4m3x4_to_bf16(cc.x), hi = e4m3x4_to_bf16(cc.y);
+              v = make_uint4(lo.x, lo.y, hi.x, hi.y);
             }
           }
           qb[rt][ds] = __builtin_bit_cast(bf16x8_t, v);

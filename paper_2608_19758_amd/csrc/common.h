@@ -63,15 +63,16 @@ __device__ __forceinline__ int e4m3_times512(uint32_t code) {
   return (code & 0x80) ? -mag : mag;
 }
 
-// OCP e4m3fn code -> bf16 bits (exact: every e4m3 value is a bf16 value).
-// Normal codes rebias the exponent (7 -> 127); subnormal codes m * 2^-9 are
-// formed as an exact float product. Branch-free.
-__device__ __forceinline__ uint32_t e4m3_to_bf16(uint32_t code) {
-  const uint32_t s = (code & 0x80u) << 8;
-  const uint32_t e = (code >> 3) & 15u, m = code & 7u;
-  const uint32_t normal = ((e + 120u) << 7) | (m << 4);
-  const uint32_t sub = __float_as_uint((float)m * 0x1p-9f) >> 16;
-  return s | (e != 0u ? normal : sub);
+typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+
+// Four OCP e4m3fn codes (the bytes of w, lowest first) -> two packed bf16
+// pairs. Exact: v_cvt_pk_f32_fp8 decodes two codes to fp32 (subnormals
+// included) and every e4m3 value is a bf16 value, so the bf16 packing does
+// not round.
+__device__ __forceinline__ uint2 e4m3x4_to_bf16(uint32_t w) {
+  const f32x2_t lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
+  const f32x2_t hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);
+  return make_uint2(pack_bf16x2(lo.x, lo.y), pack_bf16x2(hi.x, hi.y));
 }
 
 // ---------------------------------------------------------------------------

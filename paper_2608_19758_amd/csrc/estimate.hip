@@ -26,6 +26,7 @@
 // is applied in fp32 after the MFMA, and exponentials use the hardware
 // v_exp_f32; block energies match the fp64 definition to ~1e-6 relative.
 #include <algorithm>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -37,13 +38,14 @@ constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kChunksPerWave = 4;                          // 4 x 32 key blocks per wave
 constexpr int kGroup = kWaves * kChunksPerWave * 32;       // key blocks per pass (1024)
+constexpr int kQRow = 17;                                  // LDS row stride of a Q tile, 16-byte slots
 
 template <int FP8, int G>
 __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled pooled,
                                                             uint8_t* __restrict__ mask,
                                                             KeptLists kl) {
   extern __shared__ float ell[];            // [nbk] block log2-energies of this row
-  __shared__ uint4 qt[2][32 * 16];          // Q tiles (double buffer): 32 rows x 16 chunks of 8 bf16
+  __shared__ uint4 qt[2][32 * kQRow];       // Q tiles (double buffer): 32 rows x 16 chunks of 8 bf16
   __shared__ float redf[kWaves];
   __shared__ int redi[kWaves];
 
@@ -115,22 +117,19 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     }
     return v;
   };
-  // Store it into LDS buffer qb (fp8 codes widened to bf16, exact).
+  // Store it into LDS buffer qb (fp8 codes widened to bf16, exact). Rows are
+  // kQRow 16-byte slots apart: a lane's eight reads of its row then share
+  // one base address, and 16 lanes reading 16 bytes each cover all banks.
   auto qstore = [&](uint4* qb, uint4 v) {
     if (!FP8) {
       const int r = tid >> 4, c = tid & 15;
-      qb[r * 16 + (c ^ (r & 15))] = v;
+      qb[r * kQRow + c] = v;
     } else if (tid < 256) {
       const int r = tid >> 3, c8 = tid & 7;
-      uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-      uint32_t o[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        uint32_t src = wv[i >> 1] >> (16 * (i & 1));
-        o[i] = e4m3_to_bf16(src & 0xFF) | (e4m3_to_bf16((src >> 8) & 0xFF) << 16);
-      }
-      qb[r * 16 + ((2 * c8) ^ (r & 15))] = make_uint4(o[0], o[1], o[2], o[3]);
-      qb[r * 16 + ((2 * c8 + 1) ^ (r & 15))] = make_uint4(o[4], o[5], o[6], o[7]);
+      const uint2 a = e4m3x4_to_bf16(v.x), b2 = e4m3x4_to_bf16(v.y);
+      const uint2 c2 = e4m3x4_to_bf16(v.z), d = e4m3x4_to_bf16(v.w);
+      qb[r * kQRow + 2 * c8] = make_uint4(a.x, a.y, b2.x, b2.y);
+      qb[r * kQRow + 2 * c8 + 1] = make_uint4(c2.x, c2.y, d.x, d.y);
     }
   };
 
@@ -138,6 +137,8 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     bf16x8_t kf[kChunksPerWave][8];
     float m[kChunksPerWave], E[kChunksPerWave];
     bool act[kChunksPerWave];
+    // 32-block chunks per wave in this group (the most any wave has)
+    const int ncw = min(kChunksPerWave, ((Ia - grp) / 32 + kWaves) / kWaves);
 #pragma unroll
     for (int c = 0; c < kChunksPerWave; ++c) {
       const int J0 = grp + 32 * (w + kWaves * c);
@@ -154,9 +155,12 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     }
 
     // Q tiles stream through two LDS buffers; the global loads of tile t+2
-    // are in flight while tile t is scored.
+    // are in flight while tile t is scored. Only the last tile can be
+    // partial: it runs as a separate instance of the tile body, so the row
+    // validity tests stay out of the full tiles.
     uint4 qa_next = qload(0), qa_next2 = qload(1);
-    for (int t = 0; t < ntiles; ++t) {
+    auto tile = [&](int t, auto partial) {
+      constexpr bool kPartial = decltype(partial)::value;
       qstore(qt[t & 1], qa_next);
       __syncthreads();   // tile t visible; every wave is done with tile t-1
       qa_next = qa_next2;
@@ -166,10 +170,8 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       bf16x8_t qa[8];
 #pragma unroll
       for (int ds = 0; ds < 8; ++ds)
-        qa[ds] = __builtin_bit_cast(bf16x8_t, qb[l32 * 16 + ((2 * ds + half) ^ (l32 & 15))]);
-      // validity of this lane's 16 rows (only the last tile can be partial)
-      const int rbase = t * 32 + 4 * half;
-      const bool full = t * 32 + 32 <= nrows;
+        qa[ds] = __builtin_bit_cast(bf16x8_t, qb[l32 * kQRow + 2 * ds + half]);
+      const int rbase = t * 32 + 4 * half;   // first of this lane's 16 rows
 
       // Scores of chunk c (the other wave of the SIMD runs its vector work
       // while these MFMAs execute).
@@ -182,10 +184,10 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       };
       // Fold one chunk's scores into its running (m, E): rows of head
       // offset j carry the scale cs[j] (> 0), so the maximum of cs * s is
-      // taken per j on the raw scores. Rows past the block (last tile only)
-      // are set to -inf first: they add exp2(-inf) = 0.
+      // taken per j on the raw scores. Rows past the block (partial tile
+      // only) are set to -inf first: they add exp2(-inf) = 0.
       auto fold = [&](int c, f32x16_t& acc) {
-        if (!full) {
+        if constexpr (kPartial) {
 #pragma unroll
           for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -212,13 +214,32 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
           for (int j = 0; j < 4; ++j) s4[j] += fast_exp2(fmaf(acc[4 * i + j], cs[j], nb));
         E[c] += (s4[0] + s4[1]) + (s4[2] + s4[3]);
       };
+      // chunks 0 .. NC-1 of every wave (NC uniform over the workgroup, so the
+      // waves stay balanced between barriers and the scores of chunk c+1 are
+      // issued to the matrix cores before chunk c is folded on the vector
+      // ALUs); a chunk past the unit's last block scores zero keys and is
+      // dropped at the end
+      auto run = [&](auto nc) {
+        constexpr int NC = decltype(nc)::value;
+        f32x16_t acc = score(0);
 #pragma unroll
-      for (int c = 0; c < kChunksPerWave; ++c) {
-        if (!act[c]) continue;
-        f32x16_t acc = score(c);
-        fold(c, acc);
+        for (int c = 0; c < NC; ++c) {
+          f32x16_t nxt;
+          if (c + 1 < NC) nxt = score(c + 1);
+          fold(c, acc);
+          if (c + 1 < NC) acc = nxt;
+        }
+      };
+      switch (ncw) {
+        case 1: run(std::integral_constant<int, 1>{}); break;
+        case 2: run(std::integral_constant<int, 2>{}); break;
+        case 3: run(std::integral_constant<int, 3>{}); break;
+        default: run(std::integral_constant<int, 4>{}); break;
       }
-    }
+    };
+    const int nfull = nrows >> 5;
+    for (int t = 0; t < nfull; ++t) tile(t, std::false_type{});
+    if (nfull < ntiles) tile(nfull, std::true_type{});
 
     // merge the two lane halves (same key block, different rows)
 #pragma unroll
