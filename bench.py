@@ -45,8 +45,9 @@ def parse():
                     help="also measure the other 128K variants (not part of the headline line)")
     ap.add_argument("--no-variants", action="store_true", help="(default; kept for old scripts)")
     ap.add_argument("--chunked", action="store_true",
-                    help="also measure chunked prefill of the default workload (prefix KV) and "
-                         "its short tail chunks with and without KV splits")
+                    help="also measure chunked prefill of the default workload through the "
+                         "serving backend (prefix KV), its short tail chunks with and without KV "
+                         "splits, and a continuous-batching forward of four requests")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=160,
                     help="(sequence, KV head, query block) units the oracle runs for the CPU baseline")
@@ -194,59 +195,81 @@ def measure(cfg, steps, warmup):
 
 
 def chunked(cfg, steps, warmup):
-    """Chunked prefill of the headline sequence: the same 128K tokens as
-    sequential calls over chunks of C tokens, chunk c attending to the c*C
-    tokens before it as a prefix KV (the serving mode of the paper's
-    chunked-prefill experiments), each chunk's total latency against the one
-    call; and short tail chunks (the last T tokens after a 128K - T prefix)
-    with the cost-balanced KV splits against kv_splits = 1."""
+    """Chunked prefill of the headline sequence through the serving backend
+    (paper_2608_19758_amd.serving): the same 128K tokens as sequential
+    forwards over chunks of C tokens, chunk c attending to the c*C tokens
+    before it as a cached prefix (the serving mode of the paper's
+    chunked-prefill experiments), timed as the sum of the per-layer
+    forward_extend calls with the per-forward metadata prepared beforehand;
+    short tail chunks (the last T tokens after a 128K - T prefix) with the
+    cost-balanced KV splits against kv_splits = 1; and one continuous-batching
+    forward mixing four requests at different prefix lengths."""
     import torch
-    import paper_2608_19758_amd as fp2
+    import paper_2608_19758_amd.serving as serving
     sp, wl, d = cfg["spec"], cfg["wl"], cfg["d"]
     L = sp.seqlens[0]
-    bt = d["block_table"] if sp.page_size else None
     dev = d["q"].device
 
-    def make(q0, q1, splits=0):
-        # queries q0..q1-1 after the q0 tokens before them
-        p = fp2.make_params(batch=1, num_q_heads=sp.num_q_heads, num_kv_heads=sp.num_kv_heads,
-                            max_seq_len=q1 - q0, page_size=sp.page_size,
-                            max_pages_per_seq=wl.max_pages, alpha=cfg["alpha"],
-                            sink_blocks=sp.sink_blocks, window_blocks=sp.window_blocks,
-                            recent_blocks=sp.recent_blocks, mean_correction=sp.mean_correction,
-                            dtype=sp.dtype, max_kv_len=q1, kv_splits=splits)
-        cu = torch.tensor([0, q1 - q0], dtype=torch.int32, device=dev)
-        cuk = torch.tensor([0, q1], dtype=torch.int32, device=dev)
-        q = d["q"][q0:q1]
-        out, mask, _ = fp2.alloc_outputs(p, q1 - q0)
-        ws = fp2.alloc_workspace(p)
+    def backend(max_batch, max_ext, splits=0):
+        c = serving.BackendConfig(num_q_heads=sp.num_q_heads, num_kv_heads=sp.num_kv_heads,
+                                  page_size=sp.page_size, max_batch=max_batch,
+                                  max_extend_len=max_ext, max_kv_len=L, dtype=sp.dtype,
+                                  alpha=cfg["alpha"], sink_blocks=sp.sink_blocks,
+                                  window_blocks=sp.window_blocks,
+                                  recent_blocks=sp.recent_blocks,
+                                  mean_correction=bool(sp.mean_correction), kv_splits=splits)
+        return serving.PrefillBackend(c)
 
-        def run():
-            fp2.prefill(p, q, d["k_cache"], d["v_cache"], cu, bt, cu_seqlens_k=cuk, out=out,
-                        block_mask=mask, workspace=ws, q_scale=d["q_scale"],
-                        k_scale=d["k_scale"], v_scale=d["v_scale"])
-        return run, p
+    def table(be, rows):
+        bt = torch.zeros((rows, be.cfg.max_pages_per_seq), dtype=torch.int32, device=dev)
+        bt[:, :d["block_table"].shape[1]] = d["block_table"][0]
+        return bt
 
-    res = {"chunks": [], "tails": []}
+    kw = dict(q_scale=d["q_scale"], k_scale=d["k_scale"], v_scale=d["v_scale"])
+    res = {"chunks": [], "tails": [], "batched": None}
     for C in (16384, 8192):
-        runs = [make(c, c + C)[0] for c in range(0, L, C)]
+        be = backend(1, C)
+        bt = table(be, 1)
+        calls = []
+        for c0 in range(0, L, C):
+            meta = be.init_forward_metadata([C], [c0], bt)
+            calls.append((meta, d["q"][c0:c0 + C]))
+        out = torch.empty((C, sp.num_q_heads, sp.head_dim), dtype=torch.bfloat16, device=dev)
 
         def all_chunks():
-            for r in runs:
-                r()
+            for meta, q in calls:
+                be.forward_extend(q, d["k_cache"], d["v_cache"], meta, out=out, **kw)
         t, _ = time_loop(all_chunks, max(3, steps // 4), max(1, warmup // 2))
-        res["chunks"].append({"chunk": C, "calls": len(runs), "total_ms": round(t, 4)})
-        print("[bench] chunked %d x %d: %.3f ms" % (len(runs), C, t), file=sys.stderr, flush=True)
-        del runs
+        res["chunks"].append({"chunk": C, "calls": len(calls), "total_ms": round(t, 4)})
+        print("[bench] chunked %d x %d: %.3f ms" % (len(calls), C, t), file=sys.stderr, flush=True)
+        del be, calls
     for T in (128, 1024, 4096):
-        run_auto, p = make(L - T, L)
-        run_one, _ = make(L - T, L, splits=1)
-        ta, _ = time_loop(run_auto, steps, warmup)
-        t1, _ = time_loop(run_one, steps, warmup)
-        res["tails"].append({"tail_tokens": T, "prefix": L - T,
-                             "ms_planned_splits": round(ta, 4), "ms_no_splits": round(t1, 4)})
-        print("[bench] tail %d: planned splits %.3f ms, none %.3f ms" % (T, ta, t1),
-              file=sys.stderr, flush=True)
+        r = {"tail_tokens": T, "prefix": L - T}
+        for splits, key in ((0, "ms_planned_splits"), (1, "ms_no_splits")):
+            be = backend(1, T, splits)
+            meta = be.init_forward_metadata([T], [L - T], table(be, 1))
+            q = d["q"][L - T:]
+            out = torch.empty((T, sp.num_q_heads, sp.head_dim), dtype=torch.bfloat16, device=dev)
+            r[key] = round(time_loop(lambda: be.forward_extend(q, d["k_cache"], d["v_cache"], meta,
+                                                               out=out, **kw), steps, warmup)[0], 4)
+            del be
+        res["tails"].append(r)
+        print("[bench] tail %d: planned splits %.3f ms, none %.3f ms"
+              % (T, r["ms_planned_splits"], r["ms_no_splits"]), file=sys.stderr, flush=True)
+    # four requests of the same sequence data at different stages of their
+    # prefill, in one forward (continuous batching)
+    ext, pre = [8192, 8192, 4096, 1024], [0, 32768, 90112, 130048]
+    be = backend(4, 8192)
+    meta = be.init_forward_metadata(ext, pre, table(be, 4))
+    q = torch.cat([d["q"][p:p + e] for e, p in zip(ext, pre)])
+    out = torch.empty((q.shape[0], sp.num_q_heads, sp.head_dim), dtype=torch.bfloat16, device=dev)
+    t, _ = time_loop(lambda: be.forward_extend(q, d["k_cache"], d["v_cache"], meta, out=out, **kw),
+                     steps, warmup)
+    dense = sum(sp.num_q_heads * 4 * sp.head_dim * (e * p + e * (e + 1) / 2) for e, p in zip(ext, pre))
+    res["batched"] = {"extend": ext, "prefix": pre, "ms": round(t, 4),
+                      "dense_equiv_tflops": round(dense / (t * 1e-3) / 1e12, 1)}
+    print("[bench] batched forward %s after %s: %.3f ms" % (ext, pre, t), file=sys.stderr, flush=True)
+    del be
     torch.cuda.empty_cache()
     return res
 

@@ -1,0 +1,90 @@
+"""The serving backend on the GPU: two layers, two forwards of a chunked
+prefill (a first chunk per sequence, then the rest after a cached prefix),
+through per-forward metadata shared by the layers and one workspace.
+
+Without KV splits every forward reproduces, bit for bit, the rows of one
+whole-sequence fp2_prefill call (outputs, LSE and mask rows); with the default
+cost-balanced splits it agrees within the output tolerance."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_19758_amd as fp2
+import synth
+from paper_2608_19758_amd import serving
+from tests import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+KV = [1324, 1028]                        # whole sequences
+CHUNK1 = [1024, 768]                     # first forward: prefix 0
+ALPHA = 0.98
+
+
+def layer(seed, dtype):
+    # one page table for every layer (identity order), as in an engine
+    sp = synth.Spec("serve", KV, 8, 2, dtype=dtype, page_size=64, salient_frac=0.1,
+                    salient_min=2, seed=seed)
+    return synth.generate(sp)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("kv_splits", [1, 0])
+def test_backend_chunked_forwards(dtype, kv_splits):
+    layers = [layer(s, dtype) for s in (11, 12)]
+    sp = layers[0].spec
+    cfg = serving.BackendConfig(num_q_heads=8, num_kv_heads=2, page_size=64, max_batch=2,
+                                max_extend_len=1024, max_kv_len=2048, dtype=dtype, alpha=ALPHA,
+                                sink_blocks=sp.sink_blocks, window_blocks=sp.window_blocks,
+                                kv_splits=kv_splits)
+    be = serving.PrefillBackend(cfg)
+    dev = [gu.device_tensors(wl) for wl in layers]
+    # the engine's page table: the workload's, widened to the configured stride
+    bt = torch.zeros((2, cfg.max_pages_per_seq), dtype=torch.int32, device="cuda")
+    bt[:, :dev[0]["block_table"].shape[1]] = dev[0]["block_table"]
+    for wl in layers[1:]:
+        assert np.array_equal(wl.block_table, layers[0].block_table)
+    # reference: one whole-sequence call per layer, without splits
+    ref = [gu.gpu_prefill(wl, gu.params_for(wl, ALPHA, kv_splits=1)) for wl in layers]
+    cu = layers[0].cu_seqlens
+    forwards = [(CHUNK1, [0, 0]), ([k - c for k, c in zip(KV, CHUNK1)], CHUNK1)]
+    for ext, pre in forwards:
+        meta = be.init_forward_metadata(ext, pre, bt)
+        rows = np.concatenate([np.arange(cu[b] + p, cu[b] + p + e) for b, (e, p) in
+                               enumerate(zip(ext, pre))])
+        ridx = torch.from_numpy(rows).cuda()
+        for li, (wl, d) in enumerate(zip(layers, dev)):
+            out, lse = be.forward_extend(d["q"][ridx].contiguous(), d["k_cache"], d["v_cache"],
+                                         meta, q_scale=d["q_scale"], k_scale=d["k_scale"],
+                                         v_scale=d["v_scale"], want_lse=True)
+            torch.cuda.synchronize()
+            o = out.float().cpu().numpy().astype(np.float64)
+            l = lse.cpu().numpy().astype(np.float64)
+            ro, rm, rl = ref[li]
+            mask = be.block_mask(meta).cpu().numpy()
+            for b, (e, p) in enumerate(zip(ext, pre)):
+                nq, nk = (e + 127) // 128, (p + e + 127) // 128
+                np.testing.assert_array_equal(mask[b, :, :nq, :nk],
+                                              rm[b, :, p // 128:p // 128 + nq, :nk])
+            d_out = np.abs(o - ro[rows]).max()
+            print("dtype %s splits %d forward %s layer %d: max |backend - whole| %.3g"
+                  % (dtype, kv_splits, ext, li, d_out))
+            if kv_splits == 1:
+                np.testing.assert_array_equal(o, ro[rows])
+                np.testing.assert_array_equal(l, rl[rows])
+            else:
+                assert d_out <= gu.TOL[dtype]
+                assert np.abs(l - rl[rows]).max() <= gu.LSE_TOL[dtype]
+
+
+def test_backend_rejects_oversized_forward():
+    cfg = serving.BackendConfig(num_q_heads=8, num_kv_heads=2, page_size=64, max_batch=1,
+                                max_extend_len=256, max_kv_len=512)
+    be = serving.PrefillBackend(cfg)
+    bt = torch.zeros((1, cfg.max_pages_per_seq), dtype=torch.int32, device="cuda")
+    with pytest.raises(ValueError):
+        be.init_forward_metadata([300], [0], bt)
+    with pytest.raises(ValueError):
+        be.init_forward_metadata([128], [128], bt[:, :2])
+    with pytest.raises(NotImplementedError):
+        be.forward_decode()
