@@ -45,7 +45,7 @@ class Params(ctypes.Structure):
         ("recent_blocks", ctypes.c_int32), ("mean_correction", ctypes.c_int32),
         ("softmax_scale", ctypes.c_double),
         ("dtype", ctypes.c_int32), ("nthreads", ctypes.c_int32),
-        ("max_kv_len", ctypes.c_int32),
+        ("max_kv_len", ctypes.c_int32), ("tile_rows", ctypes.c_int32),
     ]
 
 
@@ -115,7 +115,9 @@ class Inputs:
         self.vs = np.ascontiguousarray(wl.v_scale, dtype=np.float32)
 
     def params(self, alpha, sink=None, window=None, recent=None, correction=None,
-               softmax_scale=0.0, nthreads=None) -> Params:
+               softmax_scale=0.0, nthreads=None, tile_rows=0) -> Params:
+        """tile_rows: packed rows per query tile (0: a query block of B
+        positions with all g heads)."""
         sp = self.spec
         return Params(
             batch=sp.batch, num_q_heads=sp.num_q_heads, num_kv_heads=sp.num_kv_heads,
@@ -129,13 +131,24 @@ class Inputs:
             softmax_scale=float(softmax_scale),
             dtype=1 if sp.dtype == "fp8" else 0,
             nthreads=nthreads_default() if nthreads is None else nthreads,
-            max_kv_len=sp.max_kv_len)
+            max_kv_len=sp.max_kv_len, tile_rows=int(tile_rows))
 
     @property
     def nbmax(self):
-        """Query blocks (mask rows)."""
+        """Query blocks (mask rows with the default tile)."""
         sp = self.spec
         return (sp.max_seq_len + sp.block_size - 1) // sp.block_size
+
+    def tile_positions(self, p: Params) -> int:
+        """Positions per query tile under ``p``."""
+        sp = self.spec
+        g = sp.num_q_heads // sp.num_kv_heads
+        return p.tile_rows // g if p.tile_rows > 0 else sp.block_size
+
+    def ntiles(self, p: Params) -> int:
+        """Query tiles per sequence bound (mask rows) under ``p``."""
+        pt = self.tile_positions(p)
+        return (self.spec.max_seq_len + pt - 1) // pt
 
     @property
     def nbk(self):
@@ -174,7 +187,7 @@ def estimate(inp: Inputs, p: Params, units=None, want_scores=False):
     ell [b, Hkv, nbq, nbk] (block log-energies, NaN past the diagonal) and
     mu [b, Hkv, nbq] (row maxima). Without a prefix nbq == nbk."""
     sp = inp.spec
-    nb, nk = max(1, inp.nbmax), max(1, inp.nbk)
+    nb, nk = max(1, inp.ntiles(p)), max(1, inp.nbk)
     mask = np.zeros((sp.batch, sp.num_kv_heads, nb, nk), np.uint8)
     ell = np.full((sp.batch, sp.num_kv_heads, nb, nk), np.nan) if want_scores else None
     mu = np.full((sp.batch, sp.num_kv_heads, nb), np.nan) if want_scores else None

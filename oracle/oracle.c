@@ -44,6 +44,15 @@
  * fp8 inputs (OCP e4m3fn) are decoded exactly and multiplied by their per-head
  * fp32 scale in fp64 before any of the above (Sec. 3.3, Eq. fp8 dequantisation).
  *
+ * Query tiles (Sec. 3.3 PackGQA; the selection tile of Eq. csr): by default a
+ * query "block" I is the B positions [I*B, (I+1)*B) with all g heads of the
+ * KV group (g*B packed rows). With tile_rows = R > 0 it is instead one M-tile
+ * of R packed rows, i.e. the Pt = R/g positions [I*Pt, (I+1)*Pt) with all g
+ * heads; Pt divides B, so a tile lies inside the single key block
+ * Ia = (P0 + I*Pt)/B, and every rule above reads with that Ia (score and
+ * select over J <= Ia, diagonal J == Ia, corrected J < Ia). Everything else is
+ * unchanged; with R = g*B the two agree.
+ *
  * Work is spread over POSIX threads by (b, h, I) unit; every unit is computed
  * independently, so the thread count does not change any result.
  */
@@ -62,6 +71,7 @@ typedef struct {
   int32_t dtype;            /* 0: bf16, 1: fp8 e4m3fn */
   int32_t nthreads;         /* <= 0: 1 */
   int32_t max_kv_len;       /* bound of the KV lengths (<= 0: max_seq_len) */
+  int32_t tile_rows;        /* packed rows per query tile (<= 0: g * block_size) */
 } oracle_params;
 
 /* ---------------- codecs ---------------- */
@@ -122,7 +132,8 @@ typedef struct {
   const float* qs;
   const float* ks;
   const float* vs;
-  int g, d, B, nbmax;       /* nbmax: query blocks (mask rows) */
+  int g, d, B, nbmax;       /* nbmax: query tiles (mask rows) */
+  int Pt;                   /* positions per query tile (B, or tile_rows / g) */
   int nbk;                  /* key blocks (mask columns, pooled rows) */
   double scale;
   /* pooled statistics [b][Hkv][nbk][d] */
@@ -222,12 +233,12 @@ static int forced_block(const ctx_t* c, int n, int I, int J) {
 
 static void estimate_unit(ctx_t* c, int b, int h, int I) {
   const oracle_params* P = c->P;
-  int L = seq_len(c, b), d = c->d, B = c->B, g = c->g;
-  int n = (L + B - 1) / B;
+  int L = seq_len(c, b), d = c->d, B = c->B, g = c->g, Pt = c->Pt;
+  int n = (L + Pt - 1) / Pt;                 /* query tiles of the sequence */
   if (I >= n) return;
   int nk = (kv_len(c, b) + B - 1) / B;
-  int Ia = I + prefix_of(c, b) / B;          /* absolute query block */
-  int p0 = I * B, p1 = p0 + B < L ? p0 + B : L;
+  int p0 = I * Pt, p1 = p0 + Pt < L ? p0 + Pt : L;
+  int Ia = (prefix_of(c, b) + p0) / B;       /* key block holding the tile's positions */
   int rows = (p1 - p0) * g;
   double* qrows = malloc(sizeof(double) * (size_t)rows * d);
   double* x = malloc(sizeof(double) * rows);
@@ -271,13 +282,13 @@ static void estimate_unit(ctx_t* c, int b, int h, int I) {
 
 static void attend_unit(ctx_t* c, int b, int h, int I) {
   const oracle_params* P = c->P;
-  int Lq = seq_len(c, b), d = c->d, B = c->B, g = c->g;
-  int n = (Lq + B - 1) / B;
+  int Lq = seq_len(c, b), d = c->d, B = c->B, g = c->g, Pt = c->Pt;
+  int n = (Lq + Pt - 1) / Pt;
   if (I >= n) return;
   int L = kv_len(c, b), P0 = prefix_of(c, b);
-  int Ia = I + P0 / B;                       /* absolute query block */
   const uint8_t* mrow = c->mask_in + (((size_t)b * P->num_kv_heads + h) * c->nbmax + I) * c->nbk;
-  int p0 = I * B, p1 = p0 + B < Lq ? p0 + B : Lq;
+  int p0 = I * Pt, p1 = p0 + Pt < Lq ? p0 + Pt : Lq;
+  int Ia = (P0 + p0) / B;                    /* key block holding the tile's positions */
   /* keys of the kept blocks, gathered once per unit */
   int nkeys = 0;
   for (int J = 0; J <= Ia; ++J)
@@ -384,7 +395,11 @@ static int setup(ctx_t* c, const oracle_params* P, const void* q, const int32_t*
   c->g = P->num_q_heads / P->num_kv_heads;
   c->d = P->head_dim;
   c->B = P->block_size;
-  c->nbmax = (P->max_seq_len + P->block_size - 1) / P->block_size;
+  c->Pt = P->tile_rows > 0 ? P->tile_rows / c->g : P->block_size;
+  if (c->Pt <= 0 || c->Pt * c->g != (P->tile_rows > 0 ? P->tile_rows : c->Pt * c->g) ||
+      P->block_size % c->Pt != 0)
+    return 1;
+  c->nbmax = (P->max_seq_len + c->Pt - 1) / c->Pt;
   int maxkv = P->max_kv_len > 0 ? P->max_kv_len : P->max_seq_len;
   c->nbk = (maxkv + P->block_size - 1) / P->block_size;
   c->scale = P->softmax_scale > 0 ? P->softmax_scale : 1.0 / sqrt((double)P->head_dim);
@@ -415,16 +430,16 @@ static void teardown(ctx_t* c) {
   pthread_mutex_destroy(&c->lock);
 }
 
-/* all (b, h, I) with I < n_b, heaviest (largest I) first */
+/* all (b, h, I) with I < n_b (query tiles), heaviest (largest I) first */
 static int32_t* all_units(const ctx_t* c, int* count) {
   const oracle_params* P = c->P;
   int tot = 0;
-  for (int b = 0; b < P->batch; ++b) tot += (seq_len(c, b) + c->B - 1) / c->B * P->num_kv_heads;
+  for (int b = 0; b < P->batch; ++b) tot += (seq_len(c, b) + c->Pt - 1) / c->Pt * P->num_kv_heads;
   int32_t* u = malloc(sizeof(int32_t) * 3 * (tot > 0 ? tot : 1));
   int i = 0;
   for (int I = c->nbmax - 1; I >= 0; --I)
     for (int b = 0; b < P->batch; ++b) {
-      if (I >= (seq_len(c, b) + c->B - 1) / c->B) continue;
+      if (I >= (seq_len(c, b) + c->Pt - 1) / c->Pt) continue;
       for (int h = 0; h < P->num_kv_heads; ++h) {
         u[3 * i] = b; u[3 * i + 1] = h; u[3 * i + 2] = I; ++i;
       }

@@ -69,8 +69,12 @@ def forced_set(n, I, sink, window, recent):
     return {J for J in range(I + 1) if J < sink or I - J < window or J == I or J >= n - recent}
 
 
-def brute(wl, alpha, sink=None, window=None, recent=None, correction=None, scale=None):
-    """mask [b, Hkv, nb, nb], ell (same shape, NaN above diag), out [total, Hq, d], lse."""
+def brute(wl, alpha, sink=None, window=None, recent=None, correction=None, scale=None,
+          tile_rows=0):
+    """mask [b, Hkv, nt, nb], ell (same shape, NaN above diag), out [total, Hq, d], lse.
+
+    tile_rows > 0: a query tile is tile_rows packed rows (tile_rows / g
+    positions with all g heads) instead of a block of B positions."""
     sp = wl.spec
     sink = sp.sink_blocks if sink is None else sink
     window = sp.window_blocks if window is None else window
@@ -80,8 +84,10 @@ def brute(wl, alpha, sink=None, window=None, recent=None, correction=None, scale
     g = Hq // Hkv
     scale = 1.0 / np.sqrt(d) if scale is None else scale
     Q, K, V = decode(wl)
+    Pt = tile_rows // g if tile_rows else B          # positions per query tile
     nbmax = max(1, (sp.max_seq_len + B - 1) // B)
-    mask = np.zeros((sp.batch, Hkv, nbmax, nbmax), np.uint8)
+    ntmax = max(1, (sp.max_seq_len + Pt - 1) // Pt)
+    mask = np.zeros((sp.batch, Hkv, ntmax, nbmax), np.uint8)
     ell = np.full(mask.shape, np.nan)
     out = np.full(Q.shape, np.nan)
     lse = np.full(Q.shape[:2], np.nan)
@@ -99,10 +105,12 @@ def brute(wl, alpha, sink=None, window=None, recent=None, correction=None, scale
             khat = bf16_bits_to_f64(bf16_round_bits(kbar))
             Qg = Q[cu[b]:cu[b] + L, h * g:(h + 1) * g]          # [L, g, d]
             S = np.einsum("lgd,jd->lgj", Qg, khat) * scale     # [L, g, n]
-            for I in range(n):
-                rows = S[blk == I].reshape(-1, n)[:, :I + 1]
+            tile = np.arange(L) // Pt
+            for t in range((L + Pt - 1) // Pt):
+                I = t * Pt // B                               # key block of the tile
+                rows = S[tile == t].reshape(-1, n)[:, :I + 1]
                 e = logsumexp(rows, axis=0)
-                ell[b, h, I, :I + 1] = e
+                ell[b, h, t, :I + 1] = e
                 order = np.argsort(-e, kind="stable")
                 top = e[order[0]]
                 kept = set()
@@ -117,9 +125,9 @@ def brute(wl, alpha, sink=None, window=None, recent=None, correction=None, scale
                 forced = forced_set(n, I, sink, window, recent)
                 for J in range(I + 1):
                     kb = J in kept or J in forced
-                    mask[b, h, I, J] = int(kb) | (int(J in forced) << 1)
-                # attention rows of block I: pruned blocks -> mean tokens
-                keptb = mask[b, h, I, :n] & 1
+                    mask[b, h, t, J] = int(kb) | (int(J in forced) << 1)
+                # attention rows of the tile: pruned blocks -> mean tokens
+                keptb = mask[b, h, t, :n] & 1
                 Km, Vm = Kb.copy(), Vb.copy()
                 allowed_blk = np.zeros(n, bool)
                 for J in range(I + 1):
@@ -129,7 +137,7 @@ def brute(wl, alpha, sink=None, window=None, recent=None, correction=None, scale
                         Km[blk == J] = kbar[J]
                         Vm[blk == J] = vbar[J]
                         allowed_blk[J] = True
-                pos = np.arange(I * B, min(L, (I + 1) * B))
+                pos = np.arange(t * Pt, min(L, (t + 1) * Pt))
                 for j in range(g):
                     qrow = Q[cu[b] + pos, h * g + j]            # [P, d]
                     lg = qrow @ Km.T * scale                   # [P, L]
