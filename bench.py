@@ -100,7 +100,7 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes": n, "copies": 3}), flush=True)
 
 
-def setup(name, target, correction=None):
+def setup(name, target, correction=None, tile_rows=0):
     import torch
     import numpy as np  # noqa: F401
     import paper_2608_19758_amd as fp2
@@ -120,7 +120,7 @@ def setup(name, target, correction=None):
                         page_size=spec.page_size, max_pages_per_seq=wl.max_pages, alpha=alpha,
                         sink_blocks=spec.sink_blocks, window_blocks=spec.window_blocks,
                         recent_blocks=spec.recent_blocks, mean_correction=spec.mean_correction,
-                        dtype=spec.dtype)
+                        dtype=spec.dtype, query_tile_rows=tile_rows)
     out, mask, _ = fp2.alloc_outputs(p, spec.total_tokens)
     mask2 = torch.empty_like(mask)
     ws = fp2.alloc_workspace(p)
@@ -137,8 +137,11 @@ def setup(name, target, correction=None):
         fp2.estimate(p, d["q"], d["k_cache"], d["v_cache"], d["cu_seqlens"], bt,
                      block_mask=mask2, workspace=ws2, **kw)
 
+    def run_csr():
+        return fp2.mask_to_csr(p, mask, d["cu_seqlens"], workspace=ws2)
+
     return dict(spec=spec, wl=wl, alpha=alpha, p=p, d=d, out=out, mask=mask,
-                run_prefill=run_prefill, run_estimate=run_estimate)
+                run_prefill=run_prefill, run_estimate=run_estimate, run_csr=run_csr)
 
 
 def time_loop(fn, steps, warmup):
@@ -167,11 +170,19 @@ def measure(cfg, steps, warmup):
     t_est, _ = time_loop(cfg["run_estimate"], steps, warmup)
     cfg["run_prefill"]()
     mask = cfg["mask"].cpu().numpy()
-    kept_ratio = acc.block_counts(mask, sp.seqlens, sp.block_size, False)[0] / max(
-        1, sum(((L + 127) // 128) * ((L + 127) // 128 + 1) // 2 for L in sp.seqlens) * sp.num_kv_heads)
+    if cfg["p"].query_tile_rows:
+        # kept pairs over visible (tile, key block) pairs of the 128-row tiles
+        pt = cfg["p"].query_tile_rows // (sp.num_q_heads // sp.num_kv_heads)
+        vis = sum(sum(t * pt // 128 + 1 for t in range((L + pt - 1) // pt)) for L in sp.seqlens)
+        kept_ratio = float((mask & 1).sum()) / max(1, vis * sp.num_kv_heads)
+    else:
+        kept_ratio = acc.block_counts(mask, sp.seqlens, sp.block_size, False)[0] / max(
+            1, sum(((L + 127) // 128) * ((L + 127) // 128 + 1) // 2 for L in sp.seqlens)
+            * sp.num_kv_heads)
     dense = acc.dense_equiv_flops(sp.seqlens, sp.num_q_heads)
     fk, fc = acc.attention_flops(mask, sp.seqlens, sp.num_q_heads, sp.num_kv_heads,
-                                 correction=bool(sp.mean_correction))
+                                 correction=bool(sp.mean_correction),
+                                 tile_rows=cfg["p"].query_tile_rows)
     t_attn = max(1e-6, t_pre - t_est)
     main_peak = PEAK_TFLOPS[sp.dtype]
     # time-weighted peak: kept tiles run at the dtype's MFMA peak, the
@@ -339,17 +350,21 @@ def main():
 
     variants = []
     if args.variants:
-        vlist = [("llama128k_fp8", "0.10", None), ("llama128k_fp8", "0.02", None),
-                 ("llama128k_fp8", "0.05", 0), ("llama128k_bf16", "0.05", None),
-                 ("wide128k_bf16", "0.009", None), ("wide128k_fp8", "0.009", None)]
+        vlist = [("llama128k_fp8", "0.10", None, 0), ("llama128k_fp8", "0.02", None, 0),
+                 ("llama128k_fp8", "0.05", 0, 0), ("llama128k_bf16", "0.05", None, 0),
+                 ("wide128k_bf16", "0.009", None, 0), ("wide128k_fp8", "0.009", None, 0),
+                 ("llama128k_fp8", "0.05", None, 128)]
+        csr_ms = time_loop(cfg["run_csr"], max(5, args.steps // 2), 2)[0]
+        print("[bench] mask to CSR: %.3f ms" % csr_ms, file=sys.stderr, flush=True)
         del cfg
         torch.cuda.empty_cache()
-        for name, tgt, corr in vlist:
-            if name == args.workload and tgt == args.target and corr is None:
+        for name, tgt, corr, tile in vlist:
+            if name == args.workload and tgt == args.target and corr is None and not tile:
                 continue
-            c = setup(name, tgt, corr)
+            c = setup(name, tgt, corr, tile)
             r = measure(c, max(5, args.steps // 2), max(2, args.warmup // 2))
             variants.append({"workload": name, "kept_target": float(tgt),
+                             "query_tile_rows": tile,
                              "mean_correction": c["spec"].mean_correction,
                              "ms": round(r["ms_per_step"], 4),
                              "dense_tflops": round(r["dense_tflops"], 2),
@@ -405,6 +420,7 @@ def main():
     }
     if variants:
         line["variants"] = variants
+        line["mask_to_csr_ms"] = round(csr_ms, 4)
     if chunk_res:
         line["chunked_prefill"] = chunk_res
     print(json.dumps(line), flush=True)

@@ -62,6 +62,18 @@
  * chunk after a long prefix, or a few dense heads, no longer bound the run
  * time). kv_splits == n >= 1 cuts every unit into n parts (1 = no splits).
  *
+ * Query tiles (Sec. 3.3 PackGQA and the per-tile index of Eq. csr)
+ * --------------------------------------------------------------
+ * Selection, attention and the index are per (sequence, KV head, query tile).
+ * By default a query tile is a query block: the B = 128 positions
+ * [I*B, (I+1)*B) with all g = num_q_heads/num_kv_heads heads of the KV group
+ * (g*B packed rows). With query_tile_rows = 128 it is the paper's M-tile of
+ * 128 packed rows: the Pt = 128/g positions [I*Pt, (I+1)*Pt) with all g
+ * heads. Pt divides B, so tile I lies inside key block
+ * Ia = (prefix + I*Pt)/B, and every rule below that names "query block I"
+ * (J <= I, J == I, J < I, I - J) reads with that Ia. With g = 1 the two
+ * tiles coincide.
+ *
  * Layouts (row-major, innermost last)
  * -----------------------------------
  *   q, out       [total_tokens, num_q_heads, head_dim]; sequence b occupies
@@ -84,8 +96,9 @@
  *                is scale * code, Sec. 3.3 Eq. fp8; a per-tensor scale is the
  *                all-equal case).
  *   block_mask   uint8 [batch, num_kv_heads, nbq, nbk], nbq = ceil(max_seq_len
- *                / block_size) query blocks, nbk = ceil(max_kv_len / block_size)
- *                key blocks (nbk == nbq without a prefix). Entry (b, h, I, J):
+ *                / Pt) query tiles (Pt = B by default), nbk = ceil(max_kv_len /
+ *                block_size) key blocks (nbk == nbq by default without a
+ *                prefix). Entry (b, h, I, J):
  *                bit 0 = key block J is attended exactly by query block I of
  *                KV head h (kept); bit 1 = J is a forced block (sink, window,
  *                diagonal or recent). Zero for J > Ia and for blocks past the
@@ -160,6 +173,10 @@ typedef struct {
                                  device; n in 1..32 = n parts for every
                                  (sequence, KV head, query block), 1 = none;
                                  see "KV splits" above */
+  int32_t query_tile_rows;    /* selection tile: 0 = a query block of B
+                                 positions with all g heads; 128 = one
+                                 M-tile of 128 packed rows (128/g positions
+                                 with all g heads); see "Query tiles" above */
 } fp2_params_t;
 
 /* Bytes of workspace the entry points need for `params` (0 for a null or
@@ -224,6 +241,30 @@ fp2_status_t fp2_pool(const fp2_params_t* params, const int32_t* cu_seqlens,
                       const int32_t* cu_seqlens_host, const void* k_cache, const void* v_cache,
                       const int32_t* block_table, const float* k_scale, const float* v_scale,
                       void* khat, void* vbar, void* stream);
+
+/* Entries of csr_indices that always suffice for fp2_mask_to_csr: two
+ * 64-token key tiles per key block and query tile, 2 * nbk * nbq * batch *
+ * num_kv_heads (0 for an invalid params). */
+size_t fp2_csr_capacity(const fp2_params_t* params);
+
+/* The selection as a CSR index of 64-token key tiles (Sec. 3.3 Eq. csr;
+ * Algorithm 1 step 5, logical blocks expanded to B/64 = 2 physical tiles per
+ * block): segment s = (b * num_kv_heads + h) * nbq + I, in block_mask row
+ * order, owns csr_indices[csr_offsets[s] .. csr_offsets[s+1]), which lists in
+ * ascending order the tiles j (keys 64j .. 64j+63 of sequence b) of every key
+ * block J with bit 0 of block_mask[b][h][I][J] set and J <= Ia: 2J, and 2J+1
+ * when 64(2J+1) < L_kv. Segments of query tiles past their sequence are
+ * empty. Inputs: params, cu_seqlens / cu_seqlens_k (device; host copies
+ * optional, validated when given), block_mask (device, the layout above).
+ * Outputs (device): csr_offsets int32 [batch * num_kv_heads * nbq + 1]
+ * (csr_offsets[0] = 0), csr_indices int32 [capacity], capacity >=
+ * fp2_csr_capacity(params) (FP2_EINVAL otherwise). Uses the workspace of
+ * fp2_workspace_bytes(params) bytes as scratch. */
+fp2_status_t fp2_mask_to_csr(const fp2_params_t* params, const int32_t* cu_seqlens,
+                             const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                             const int32_t* cu_seqlens_k_host, const uint8_t* block_mask,
+                             int32_t* csr_offsets, int32_t* csr_indices, size_t capacity,
+                             void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* fp2_status_str(fp2_status_t status);

@@ -42,11 +42,12 @@ class Params(ctypes.Structure):
         ("recent_blocks", ctypes.c_int32), ("mean_correction", ctypes.c_int32),
         ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
         ("max_kv_len", ctypes.c_int32), ("kv_splits", ctypes.c_int32),
+        ("query_tile_rows", ctypes.c_int32),
     ]
 
 
 EXPORTS = ["fp2_workspace_bytes", "fp2_prefill", "fp2_estimate", "fp2_attend", "fp2_pool",
-           "fp2_status_str", "fp2_last_error"]
+           "fp2_csr_capacity", "fp2_mask_to_csr", "fp2_status_str", "fp2_last_error"]
 
 
 def lib():
@@ -68,6 +69,10 @@ def lib():
         L.fp2_attend.argtypes = [P] + [vp] * 15 + [ctypes.c_size_t, vp]
         L.fp2_pool.restype = ctypes.c_int
         L.fp2_pool.argtypes = [P] + [vp] * 10
+        L.fp2_csr_capacity.restype = ctypes.c_size_t
+        L.fp2_csr_capacity.argtypes = [P]
+        L.fp2_mask_to_csr.restype = ctypes.c_int
+        L.fp2_mask_to_csr.argtypes = [P] + [vp] * 7 + [ctypes.c_size_t, vp, ctypes.c_size_t, vp]
         L.fp2_status_str.restype = ctypes.c_char_p
         L.fp2_status_str.argtypes = [ctypes.c_int]
         L.fp2_last_error.restype = ctypes.c_char_p
@@ -92,10 +97,12 @@ def _check(fn: str, st: int) -> None:
 def make_params(*, batch, num_q_heads, num_kv_heads, max_seq_len, page_size=0,
                 max_pages_per_seq=0, alpha=0.0, sink_blocks=1, window_blocks=2,
                 recent_blocks=0, mean_correction=1, softmax_scale=0.0, dtype="bf16",
-                head_dim=HEAD_DIM, block_size=BLOCK, max_kv_len=0, kv_splits=0) -> Params:
+                head_dim=HEAD_DIM, block_size=BLOCK, max_kv_len=0, kv_splits=0,
+                query_tile_rows=0) -> Params:
     """fp2_params_t; max_kv_len bounds the KV lengths with a prefix (0: max_seq_len);
     kv_splits: 0 = cost-balanced KV splits planned on the device, n = n parts per unit
-    (1 = none)."""
+    (1 = none); query_tile_rows: 0 = query blocks of 128 positions x g heads,
+    128 = tiles of 128 packed rows (128 / g positions x g heads)."""
     dt = {"bf16": BF16, "fp8": FP8_E4M3}.get(dtype, dtype)
     return Params(batch=batch, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
                   head_dim=head_dim, block_size=block_size, page_size=page_size,
@@ -103,12 +110,19 @@ def make_params(*, batch, num_q_heads, num_kv_heads, max_seq_len, page_size=0,
                   alpha=alpha, sink_blocks=sink_blocks, window_blocks=window_blocks,
                   recent_blocks=recent_blocks, mean_correction=int(mean_correction),
                   softmax_scale=softmax_scale, dtype=dt, max_kv_len=max_kv_len,
-                  kv_splits=kv_splits)
+                  kv_splits=kv_splits, query_tile_rows=query_tile_rows)
+
+
+def tile_positions(p: Params) -> int:
+    """Positions per query tile (block_size, or 128 / g for 128-row tiles)."""
+    if p.query_tile_rows > 0:
+        return p.query_tile_rows // (p.num_q_heads // p.num_kv_heads)
+    return p.block_size
 
 
 def num_blocks(p: Params) -> int:
-    """Query blocks per sequence bound (block_mask rows)."""
-    return (p.max_seq_len + p.block_size - 1) // p.block_size
+    """Query tiles per sequence bound (block_mask rows)."""
+    return (p.max_seq_len + tile_positions(p) - 1) // tile_positions(p)
 
 
 def num_key_blocks(p: Params) -> int:
@@ -231,3 +245,25 @@ def pool(p: Params, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_seqlen
                         _ptr(v_scale), _ptr(khat), _ptr(vbar), _stream(stream))
     _check("fp2_pool", st)
     return khat, vbar
+
+
+def csr_capacity(p: Params) -> int:
+    return int(lib().fp2_csr_capacity(ctypes.byref(p)))
+
+
+def mask_to_csr(p: Params, block_mask, cu_seqlens, *, cu_seqlens_k=None, cu_seqlens_host=None,
+                cu_seqlens_k_host=None, workspace=None, stream=None):
+    """fp2_mask_to_csr: returns (offsets int32 [nseg + 1], indices int32 [capacity]);
+    the index has offsets[-1] valid entries."""
+    nseg = p.batch * p.num_kv_heads * max(1, num_blocks(p))
+    offsets = torch.empty(nseg + 1, dtype=torch.int32, device=block_mask.device)
+    cap = max(1, csr_capacity(p))
+    indices = torch.empty(cap, dtype=torch.int32, device=block_mask.device)
+    if workspace is None:
+        workspace = alloc_workspace(p, block_mask.device)
+    st = lib().fp2_mask_to_csr(ctypes.byref(p), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
+                               _ptr(cu_seqlens_k), _host_ptr(cu_seqlens_k_host), _ptr(block_mask),
+                               _ptr(offsets), _ptr(indices), cap, _ptr(workspace),
+                               workspace.numel(), _stream(stream))
+    _check("fp2_mask_to_csr", st)
+    return offsets, indices

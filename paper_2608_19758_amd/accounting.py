@@ -31,10 +31,31 @@ def block_counts(mask, seqlens, block_size=128, correction=True):
     return kept, corr
 
 
+def tile_counts(mask, seqlens, positions, block_size=128, correction=True):
+    """Per (b, h): kept and corrected (tile, key block) pairs for query tiles of
+    ``positions`` positions (tile t lies in key block t * positions / B)."""
+    kept = corr = 0
+    for b, L in enumerate(seqlens):
+        nt = (L + positions - 1) // positions
+        nb = (L + block_size - 1) // block_size
+        m = (mask[b, :, :nt, :nb] & 1).astype(bool)
+        kept += int(m.sum())
+        if correction:
+            own = np.arange(nt) * positions // block_size
+            strict = np.arange(nb)[None, :] < own[:, None]
+            corr += int((strict[None] & ~m).sum())
+    return kept, corr
+
+
 def attention_flops(mask, seqlens, num_q_heads, num_kv_heads, head_dim=128, block_size=128,
-                    correction=True):
-    """(kept-block FLOPs, correction FLOPs) executed by the attention kernel."""
+                    correction=True, tile_rows=0):
+    """(kept-block FLOPs, correction FLOPs) executed by the attention kernel.
+    tile_rows > 0: the mask rows are tiles of tile_rows packed rows."""
     g = num_q_heads // num_kv_heads
+    if tile_rows:
+        kept, corr = tile_counts(mask, seqlens, tile_rows // g, block_size, correction)
+        return (4.0 * head_dim * tile_rows * block_size * kept,
+                4.0 * head_dim * tile_rows * corr)
     kept, corr = block_counts(mask, seqlens, block_size, correction)
     return (4.0 * head_dim * g * block_size * block_size * kept,
             4.0 * head_dim * g * block_size * corr)

@@ -33,7 +33,13 @@ constexpr int kMaxSeqLen = fp2::kMaxBlocks * fp2::kBlock;   // 1M tokens
 
 int max_kv_of(const fp2_params_t* p) { return p->max_kv_len > 0 ? p->max_kv_len : p->max_seq_len; }
 // query blocks (mask rows) and key blocks (mask columns, pooled rows)
-int nbq_of(const fp2_params_t* p) { return (p->max_seq_len + fp2::kBlock - 1) / fp2::kBlock; }
+// positions per query tile: a block of B positions, or one 128-packed-row
+// M-tile of 128 / g positions
+int qtile_of(const fp2_params_t* p) {
+  return p->query_tile_rows > 0 ? p->query_tile_rows / (p->num_q_heads / p->num_kv_heads)
+                                : fp2::kBlock;
+}
+int nbq_of(const fp2_params_t* p) { return (p->max_seq_len + qtile_of(p) - 1) / qtile_of(p); }
 int nbk_of(const fp2_params_t* p) { return (max_kv_of(p) + fp2::kBlock - 1) / fp2::kBlock; }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -58,8 +64,8 @@ Layout layout_of(const fp2_params_t* p) {
   const size_t rows = heads * nbq_of(p);    // (sequence, KV head, query block)
   const size_t krows = heads * nbk_of(p);   // (sequence, KV head, key block)
   const int g = p->num_q_heads / p->num_kv_heads;
-  const size_t rpu = (size_t)g * fp2::kBlock;
-  const size_t wpu = (size_t)fp2::attend_items_per_unit(g);
+  const size_t rpu = (size_t)g * qtile_of(p);
+  const size_t wpu = (size_t)fp2::attend_items_per_unit(g, qtile_of(p));
   size_t slots, items;
   if (p->kv_splits == 0) {
     slots = kPartialRows / rpu;
@@ -137,6 +143,8 @@ fp2_status_t validate_params(const fp2_params_t* p) {
     return fail(FP2_EINVAL, "dtype %d unknown", p->dtype);
   if (p->kv_splits < 0 || p->kv_splits > kMaxSplits)
     return fail(FP2_EINVAL, "kv_splits %d not in [0, %d]", p->kv_splits, kMaxSplits);
+  if (p->query_tile_rows != 0 && p->query_tile_rows != 128)
+    return fail(FP2_EUNSUPPORTED, "query_tile_rows %d not 0 or 128", p->query_tile_rows);
   return FP2_OK;
 }
 
@@ -226,6 +234,7 @@ fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* c
   pr.hkv = p->num_kv_heads;
   pr.g = p->num_q_heads / p->num_kv_heads;
   pr.nbmax = nbq_of(p);
+  pr.qtile = qtile_of(p);
   pr.nbk = nbk_of(p);
   pr.sink = p->sink_blocks;
   pr.window = p->window_blocks;
@@ -377,6 +386,41 @@ fp2_status_t fp2_pool(const fp2_params_t* params, const int32_t* cu_seqlens,
                                        block_table, nullptr, k_scale, v_scale);
   fp2::Pooled pooled{(uint16_t*)khat, (uint16_t*)vbar};
   return hip_status(fp2::launch_pool(pr, pooled, (hipStream_t)stream), "fp2_pool launch");
+}
+
+size_t fp2_csr_capacity(const fp2_params_t* params) {
+  if (validate_params(params) != FP2_OK) return 0;
+  return (size_t)params->batch * params->num_kv_heads * nbq_of(params) * 2 * nbk_of(params);
+}
+
+fp2_status_t fp2_mask_to_csr(const fp2_params_t* params, const int32_t* cu_seqlens,
+                             const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                             const int32_t* cu_seqlens_k_host, const uint8_t* block_mask,
+                             int32_t* csr_offsets, int32_t* csr_indices, size_t capacity,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  fp2_status_t st = validate_params(params);
+  if (st != FP2_OK) return st;
+  if (params->batch == 0 || params->max_seq_len == 0) return ok();
+  if (!cu_seqlens) return fail(FP2_EINVAL, "cu_seqlens is null");
+  if (cu_seqlens_k_host && !cu_seqlens_k)
+    return fail(FP2_EINVAL, "cu_seqlens_k_host given without cu_seqlens_k");
+  if (cu_seqlens_host &&
+      (st = check_cu(cu_seqlens_host, params->batch, params->max_seq_len, "cu_seqlens", "max_seq_len")))
+    return st;
+  if (cu_seqlens_k_host && (st = check_cu(cu_seqlens_k_host, params->batch, max_kv_of(params),
+                                          "cu_seqlens_k", "max_kv_len")))
+    return st;
+  if (!block_mask || !csr_offsets || !csr_indices)
+    return fail(FP2_EINVAL, "block_mask, csr_offsets or csr_indices is null");
+  const size_t need = fp2_csr_capacity(params);
+  if (capacity < need) return fail(FP2_EINVAL, "csr capacity %zu < %zu", capacity, need);
+  if ((st = validate_ws(params, workspace, workspace_bytes)) != FP2_OK) return st;
+  const fp2::Problem pr = make_problem(params, nullptr, cu_seqlens, cu_seqlens_k, nullptr, nullptr,
+                                       nullptr, nullptr, nullptr, nullptr);
+  const Views vw = views_of(params, workspace);
+  return hip_status(fp2::launch_mask_to_csr(pr, block_mask, vw.kl.cnt, csr_offsets, csr_indices,
+                                            (hipStream_t)stream),
+                    "fp2_mask_to_csr launch");
 }
 
 const char* fp2_status_str(fp2_status_t status) {

@@ -617,7 +617,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
 
   constexpr int M = 32 * RT * W;            // packed rows per work item
   constexpr int NPRE = W > 4 ? 2 : 4;       // V^T key groups read ahead of the softmax
-  const int wpu = p0.g * kBlock / M;        // row slices per unit
+  const int wpu = p0.g * p0.qtile / M;      // row slices per unit
   const int nbh = p0.batch * p0.hkv;
   const int tid0 = threadIdx.x;
 
@@ -662,13 +662,13 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     const int bh = u % nbh;
     const int b = bh / p.hkv, h = bh % p.hkv;
     const int Lq = p.cu[b + 1] - p.cu[b];
-    if (I * kBlock >= Lq) continue;
+    if (I * p.qtile >= Lq) continue;
     // KV tokens of the sequence (a prefix included) and the absolute key
     // block Ia of query block I; positions below are absolute, and query
     // position x is packed row qbase + x
     const int64_t tok0 = p.cuk[b];
     const int L = p.cuk[b + 1] - (int)tok0;
-    const int Ia = I + (L - Lq) / kBlock;
+    const int Ia = (L - Lq + I * p.qtile) / kBlock;   // key block holding the unit's rows
     const int64_t qbase = (int64_t)p.cu[b] - (L - Lq);
 
     const int lane = tid & 63, w = tid >> 6;
@@ -685,7 +685,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     int64_t qoff[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      pos[rt] = Ia * kBlock + (pr0 + 32 * rt) / G;
+      pos[rt] = (L - Lq) + I * p.qtile + (pr0 + 32 * rt) / G;
       qvalid[rt] = pos[rt] < L;
       qoff[rt] = ((qbase + pos[rt]) * p.hq + hq) * kHeadDim;   // element index
     }
@@ -911,7 +911,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       for (int rt = 0; rt < RT; ++rt) {
         const float l_tot = rs.l[rt] + __shfl_xor(rs.l[rt], 32, 64);
         if (!qvalid[rt]) continue;
-        const int64_t prow = slot * (G * kBlock) + pr0 + 32 * rt;
+        const int64_t prow = slot * (G * p.qtile) + pr0 + 32 * rt;
         float* po = plan.part_o + prow * kHeadDim;
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt)
@@ -959,21 +959,22 @@ hipError_t launch_cfg(const Problem& p, const Pooled& pooled, const uint8_t* mas
   return hipSuccess;
 }
 
-// 32 query rows per wave; 8 waves (two per SIMD) when the unit has at least
-// 256 packed rows, else 4.
-constexpr int waves_for(int g) { return g == 1 ? 4 : ATT_W; }
+// 32 query rows per wave; 8 waves (two per SIMD) when the unit (query tile)
+// has at least 256 packed rows, else 4 (a 128-row tile is one work item).
+constexpr int waves_for(int rows) { return rows < 256 ? 4 : ATT_W; }
 
 template <int FP8>
 hipError_t launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask,
                      const KeptLists& kl, const Plan& plan, void* out, float* lse,
                      hipStream_t s) {
-  if (p.g == 1) return launch_cfg<FP8, waves_for(1), 1, 0>(p, pooled, mask, kl, plan, out, lse, s);
+  if (p.g * p.qtile < 256)
+    return launch_cfg<FP8, waves_for(128), 1, 0>(p, pooled, mask, kl, plan, out, lse, s);
   return launch_cfg<FP8, ATT_W, 1, ATT_PIPE>(p, pooled, mask, kl, plan, out, lse, s);
 }
 
 }  // namespace
 
-int attend_items_per_unit(int g) { return g * kBlock / (32 * waves_for(g)); }
+int attend_items_per_unit(int g, int qtile) { return g * qtile / (32 * waves_for(g * qtile)); }
 
 hipError_t launch_attend(const Problem& p, const Pooled& pooled, const uint8_t* mask,
                          const KeptLists& kl, const Plan& plan, void* out, float* lse,

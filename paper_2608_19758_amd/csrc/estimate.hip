@@ -74,11 +74,11 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
   const int half = lane >> 5, l32 = lane & 31;
   const int64_t tok0 = p.cu[b];
   const int L = p.cu[b + 1] - (int)tok0;
-  const int n = (L + kBlock - 1) / kBlock;
-  // KV tokens and key blocks; with a prefix query block I is key block Ia
+  const int n = (L + p.qtile - 1) / p.qtile;   // query tiles of the sequence
+  // KV tokens and key blocks; query tile I lies in key block Ia
   const int Lk = p.cuk[b + 1] - p.cuk[b];
   const int nk = (Lk + kBlock - 1) / kBlock;
-  const int Ia = I + (Lk - L) / kBlock;
+  const int Ia = (Lk - L + I * p.qtile) / kBlock;
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
   uint8_t* mrow = mask + row * p.nbk;
 
@@ -88,7 +88,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     continue;
   }
 
-  const int npos = min(kBlock, L - I * kBlock);
+  const int npos = min(p.qtile, L - I * p.qtile);
   const int nrows = npos * G;
   const int ntiles = (nrows + 31) / 32;
 
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     const int r = FP8 ? tid >> 3 : tid >> 4;
     const int pr = t * 32 + r;
     if (t < ntiles && pr < nrows && (!FP8 || tid < 256)) {
-      const int pos = I * kBlock + pr / G, hq = h * G + pr % G;
+      const int pos = I * p.qtile + pr / G, hq = h * G + pr % G;
       if (FP8)
         v = *(const uint4*)((const uint8_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + (tid & 7) * 16);
       else
@@ -306,8 +306,8 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
   const int b = bh / p.hkv, h = bh % p.hkv;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int L = p.cu[b + 1] - p.cu[b];
-  const int n = (L + kBlock - 1) / kBlock;
-  const int Ia = I + (p.cuk[b + 1] - p.cuk[b] - L) / kBlock;   // key block of query block I
+  const int n = (L + p.qtile - 1) / p.qtile;
+  const int Ia = (p.cuk[b + 1] - p.cuk[b] - L + I * p.qtile) / kBlock;   // key block of tile I
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
   if (I >= n) {
     if (tid == 0) kl.cnt[row] = 0;

@@ -20,7 +20,10 @@ struct Problem {
   const float* k_scale;
   const float* v_scale;
   int32_t batch, hq, hkv, g;
-  int32_t nbmax;            // query blocks per sequence bound (mask rows)
+  int32_t nbmax;            // query tiles per sequence bound (mask rows)
+  int32_t qtile;            // positions per query tile: kBlock, or 128 / g for the
+                            // 128-packed-row tile; it divides kBlock, so tile I lies
+                            // in key block (prefix + I * qtile) / kBlock
   int32_t nbk;              // key blocks per sequence bound (mask columns, pooled rows)
   int32_t sink, window, recent, corr;
   int32_t splits;           // KV splits: 0 = cost-balanced plan, n >= 1 = n per unit
@@ -58,7 +61,7 @@ struct Plan {
 
 // Work items of the attention kernel per (sequence, KV head, query block),
 // before splitting: row slices of 32 * waves packed rows.
-int attend_items_per_unit(int g);
+int attend_items_per_unit(int g, int qtile);
 
 // Compute units of the current device (0 if it cannot be queried).
 int device_compute_units();
@@ -73,5 +76,7 @@ hipError_t launch_attend(const Problem& p, const Pooled& pooled, const uint8_t* 
                          hipStream_t s);
 hipError_t launch_combine(const Problem& p, const Plan& plan, void* out, float* lse,
                           hipStream_t s);
+hipError_t launch_mask_to_csr(const Problem& p, const uint8_t* mask, int32_t* counts,
+                              int32_t* offsets, int32_t* indices, hipStream_t s);
 
 }  // namespace fp2

@@ -110,8 +110,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, KeptLists
     const int row = row_of(p, q, nbh, I, b);
     const int Lq = p.cu[b + 1] - p.cu[b];
     int cost = -1;
-    if (I * kBlock < Lq) {
-      const int Ia = I + (p.cuk[b + 1] - p.cuk[b] - Lq) / kBlock;
+    if (I * p.qtile < Lq) {
+      const int Ia = (p.cuk[b + 1] - p.cuk[b] - Lq + I * p.qtile) / kBlock;
       const int cnt = kl.cnt[row];
       const int pruned = p.corr ? max(0, Ia + 1 - cnt) : 0;
       cost = 2 * cnt + (pruned + 63) / 64 + kItemSteps;
@@ -183,7 +183,7 @@ template <int FP8>
 __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan plan,
                                                       uint16_t* __restrict__ out,
                                                       float* __restrict__ lse) {
-  const int G = p.g, rpu = G * kBlock, groups = rpu / 8;
+  const int G = p.g, rpu = G * p.qtile, groups = rpu / 8;
   const int work = plan.counts[2] * groups;
   const int lane = threadIdx.x & 31, sub = threadIdx.x >> 5;
   const int c = lane * 4;
@@ -197,7 +197,7 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan plan,
     const int I = row % p.nbmax, bh = row / p.nbmax;
     const int b = bh / p.hkv, h = bh % p.hkv;
     const int pr = grp * 8 + sub;              // packed row of this half-wave
-    const int pos = I * kBlock + pr / G;
+    const int pos = I * p.qtile + pr / G;
     if (pos >= p.cu[b + 1] - p.cu[b]) continue;
     // lane u < U holds part u's {m, l}
     float m = -INFINITY, l = 0.f;
@@ -248,14 +248,14 @@ int device_compute_units() {
 
 hipError_t launch_plan(const Problem& p, const KeptLists& kl, const Plan& plan, hipStream_t s) {
   if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
-  plan_kernel<<<1, kPlanThreads, 0, s>>>(p, kl, plan, attend_items_per_unit(p.g));
+  plan_kernel<<<1, kPlanThreads, 0, s>>>(p, kl, plan, attend_items_per_unit(p.g, p.qtile));
   return hipGetLastError();
 }
 
 hipError_t launch_combine(const Problem& p, const Plan& plan, void* out, float* lse,
                           hipStream_t s) {
   if (p.batch == 0 || p.nbmax == 0 || plan.cap_slots == 0) return hipSuccess;
-  const int64_t bound = (int64_t)(plan.cap_slots / 2) * (p.g * kBlock / 8);
+  const int64_t bound = (int64_t)(plan.cap_slots / 2) * (p.g * p.qtile / 8);
   const unsigned grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(bound, 1024));
   if (p.fp8)
     combine_kernel<1><<<grid, 256, 0, s>>>(p, plan, (uint16_t*)out, lse);

@@ -19,7 +19,8 @@ BAND = 1e-4                         # relative distance of a block energy from t
 LSE_TOL = {"bf16": 1e-2, "fp8": 0.0625}
 
 
-def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=0.0, kv_splits=0):
+def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=0.0, kv_splits=0,
+               query_tile_rows=0):
     sp = wl.spec
     return fp2.make_params(
         batch=sp.batch, num_q_heads=sp.num_q_heads, num_kv_heads=sp.num_kv_heads,
@@ -29,7 +30,8 @@ def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=
         recent_blocks=sp.recent_blocks if recent is None else recent,
         mean_correction=sp.mean_correction if corr is None else corr,
         softmax_scale=scale, dtype=sp.dtype,
-        max_kv_len=sp.max_kv_len if sp.prefix is not None else 0, kv_splits=kv_splits)
+        max_kv_len=sp.max_kv_len if sp.prefix is not None else 0, kv_splits=kv_splits,
+        query_tile_rows=query_tile_rows)
 
 
 def device_tensors(wl):
@@ -64,13 +66,19 @@ def oracle_params(inp, alpha, corr=None, sink=None, window=None, recent=None):
     return inp.params(alpha, sink=sink, window=window, recent=recent, correction=corr)
 
 
-def units_of(wl, sample=None, seed=0):
-    """All (b, h, I) units, or a deterministic sample containing each
-    sequence's last block and first block."""
+def tile_positions(wl, query_tile_rows=0):
     sp = wl.spec
+    return query_tile_rows // (sp.num_q_heads // sp.num_kv_heads) if query_tile_rows else sp.block_size
+
+
+def units_of(wl, sample=None, seed=0, query_tile_rows=0):
+    """All (b, h, I) units (query tiles), or a deterministic sample containing
+    each sequence's last tile and first tile."""
+    sp = wl.spec
+    Pt = tile_positions(wl, query_tile_rows)
     allu = []
     for b, L in enumerate(sp.seqlens):
-        n = (L + sp.block_size - 1) // sp.block_size
+        n = (L + Pt - 1) // Pt
         for h in range(sp.num_kv_heads):
             for I in range(n):
                 allu.append((b, h, I))
@@ -79,7 +87,7 @@ def units_of(wl, sample=None, seed=0):
     rng = np.random.default_rng(seed)
     pick = set()
     for b, L in enumerate(sp.seqlens):
-        n = (L + sp.block_size - 1) // sp.block_size
+        n = (L + Pt - 1) // Pt
         if n:
             pick.add((b, int(rng.integers(sp.num_kv_heads)), n - 1))
             pick.add((b, int(rng.integers(sp.num_kv_heads)), 0))
@@ -88,15 +96,16 @@ def units_of(wl, sample=None, seed=0):
     return sorted(pick | {rest[i] for i in idx})
 
 
-def unit_rows(wl, units):
+def unit_rows(wl, units, query_tile_rows=0):
     """Token rows (into q/out) and Q-head ranges of the given units."""
     sp = wl.spec
     g = sp.num_q_heads // sp.num_kv_heads
+    Pt = tile_positions(wl, query_tile_rows)
     rows = []
     for b, h, I in units:
         L = sp.seqlens[b]
-        t0 = int(wl.cu_seqlens[b]) + I * sp.block_size
-        t1 = int(wl.cu_seqlens[b]) + min(L, (I + 1) * sp.block_size)
+        t0 = int(wl.cu_seqlens[b]) + I * Pt
+        t1 = int(wl.cu_seqlens[b]) + min(L, (I + 1) * Pt)
         rows.append((slice(t0, t1), slice(h * g, (h + 1) * g)))
     return rows
 

@@ -89,6 +89,8 @@ def call_prefill(p, **over):
     (dict(max_kv_len=(1 << 20) + 1, max_pages_per_seq=1 << 15), fp2.EUNSUPPORTED),
     (dict(kv_splits=-1), fp2.EINVAL),
     (dict(kv_splits=33), fp2.EINVAL),
+    (dict(query_tile_rows=64), fp2.EUNSUPPORTED),
+    (dict(query_tile_rows=-1), fp2.EUNSUPPORTED),
 ])
 def test_invalid_params(kw, status):
     assert call_prefill(base(**kw)) == status
@@ -127,8 +129,8 @@ def ws_parts(p):
     g = p.num_q_heads // p.num_kv_heads
     rows = p.batch * p.num_kv_heads * fp2.num_blocks(p)
     krows = p.batch * p.num_kv_heads * fp2.num_key_blocks(p)
-    wpu = {1: 1, 2: 1, 4: 2, 8: 4}[g]
-    rpu = g * 128
+    rpu = g * fp2.tile_positions(p)
+    wpu = max(1, rpu // 256)
     if p.kv_splits == 0:
         slots = 65536 // rpu
         items = wpu * (rows + slots)
@@ -144,7 +146,9 @@ def ws_parts(p):
 
 @pytest.mark.parametrize("kw", [dict(), dict(kv_splits=1), dict(kv_splits=4),
                                 dict(num_q_heads=64, kv_splits=0), dict(num_q_heads=8),
-                                dict(max_kv_len=12288, max_pages_per_seq=192, kv_splits=3)])
+                                dict(max_kv_len=12288, max_pages_per_seq=192, kv_splits=3),
+                                dict(query_tile_rows=128), dict(query_tile_rows=128, kv_splits=2),
+                                dict(num_q_heads=64, query_tile_rows=128)])
 def test_workspace_sections(kw):
     p = base(**kw)
     assert fp2.workspace_bytes(p) == ws_parts(p)
@@ -180,3 +184,20 @@ def test_status_strings():
     for s in range(5):
         assert fp2.status_str(s)
     assert fp2.status_str(99) == "unknown status"
+
+
+def test_mask_to_csr_validation():
+    p = base(query_tile_rows=128)
+    lib = fp2.lib()
+    cap = fp2.csr_capacity(p)
+    # 2 * 8 heads * 128 tiles of 32 positions * 2 * 32 key blocks
+    assert cap == 2 * 8 * (4096 // 32) * 2 * 32
+    call = lambda **o: lib.fp2_mask_to_csr(
+        ctypes.byref(p), o.get("cu", FAKE), None, None, None, o.get("mask", FAKE),
+        o.get("off", FAKE), o.get("idx", FAKE), o.get("cap", cap), o.get("ws", None),
+        o.get("wsb", 0), None)
+    assert call(cap=cap - 1) == fp2.EINVAL and "capacity" in fp2.last_error()
+    assert call(mask=None) == fp2.EINVAL
+    assert call(cu=None) == fp2.EINVAL
+    assert call() == fp2.EWORKSPACE
+    assert fp2.csr_capacity(base(query_tile_rows=7)) == 0
