@@ -64,9 +64,6 @@ constexpr int kPlist = 8 * kRec;     // pruned blocks per correction chunk (u16,
 #ifndef ATT_W
 #define ATT_W 8
 #endif
-#ifndef ATT_PIPE
-#define ATT_PIPE 0
-#endif
 
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 typedef __attribute__((address_space(3))) i32x2_t lds_i32x2_t;
@@ -204,45 +201,6 @@ __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb,
       if (ni < n) ad.get(ni);   // lands while the step is computed
     }
     body(ring + (s % P::NST) * P::STAGE, s);
-  }
-  lds_barrier();
-}
-
-// Ring over steps 0 .. n-1 with the scores of step s+1 issued to the matrix
-// cores before the rest of step s runs: qk(stage, S) starts the score MFMAs
-// of a step, fin(stage, S, s) finishes step s from its scores. The vector
-// work of step s then overlaps the MFMAs of step s+1 within the wave.
-template <int W, int FP8, class SC, class Fetch, class Addr, class QK, class Fin>
-__device__ __forceinline__ void pipe_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
-                                          Fetch fetch, Addr addr, QK qk, Fin fin, int tid) {
-  using P = CopyPlan<W, FP8>;
-  static_assert(P::NST >= 3, "the ring holds steps s-1 (refill), s and s+1");
-  Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
-  int ni = 0;
-#pragma unroll 1
-  for (; ni < P::NST - 1 && ni < n; ++ni) {
-    ad.get(ni);
-    ad.convert(ni);
-    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, ad.off, tid);
-  }
-  if (ni < n) ad.get(ni);
-  wait_ahead<P::D>(ni - 1);
-  lds_barrier();   // step 0 visible to all
-  SC sc, sn;
-  qk(ring, sc);
-#pragma unroll 1
-  for (int s = 0; s < n; ++s) {
-    if (s + 1 < n) wait_ahead<P::D>(ni - 2 - s);
-    lds_barrier();   // step s+1 visible; every wave is done with step s-1
-    const bool more = ni < n;
-    if (more) {
-      ad.convert(ni);
-      issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, ad.off, tid);
-    }
-    if (s + 1 < n) qk(ring + ((s + 1) % P::NST) * P::STAGE, sn);
-    fin(ring + (s % P::NST) * P::STAGE, sc, s);
-    if (more && ni < n) ad.get(ni);
-    sc = sn;
   }
   lds_barrier();
 }
@@ -541,70 +499,19 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
   }
 }
 
-// Ring over steps 0 .. n-1 with the two waves of each SIMD half a step
-// apart: waves 0 .. W/2-1 run qk(s) then fin(s); waves W/2 .. W-1 run
-// fin(s-1), whose scores they started in the previous step, then qk(s). On
-// every SIMD one wave then works on the vector ALUs while the other keeps the
-// matrix cores busy. Step s-1 is still read in step s, so the ring refills the
-// stage of step s-2.
-template <int W, int FP8, class SC, class Fetch, class Addr, class QK, class Fin>
-__device__ __forceinline__ void pingpong_loop(uint4* ring, int n, const uint8_t* Kb,
-                                              const uint8_t* Vb, Fetch fetch, Addr addr, QK qk,
-                                              Fin fin, int tid) {
-  using P = CopyPlan<W, FP8>;
-  static_assert(P::NST >= 3, "the ring holds steps s-2 (refill), s-1 and s");
-  Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
-  const bool late = (tid >> 6) >= W / 2;
-  int ni = 0;
-#pragma unroll 1
-  for (; ni < P::NST - 2 && ni < n; ++ni) {
-    ad.get(ni);
-    ad.convert(ni);
-    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, ad.off, tid);
-  }
-  if (ni < n) ad.get(ni);
-  SC sc;
-#pragma unroll 1
-  for (int s = 0; s < n; ++s) {
-    wait_ahead<P::D>(ni - 1 - s);
-    lds_barrier();   // step s visible; every wave is done with step s-2
-    const bool more = ni < n;
-    if (more) {
-      ad.convert(ni);
-      issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, ad.off, tid);
-    }
-    if (!late) {
-      qk(ring + (s % P::NST) * P::STAGE, sc);
-      fin(ring + (s % P::NST) * P::STAGE, sc, s);
-    } else {
-      if (s > 0) fin(ring + ((s - 1) % P::NST) * P::STAGE, sc, s - 1);
-      qk(ring + (s % P::NST) * P::STAGE, sc);
-    }
-    if (more && ni < n) ad.get(ni);
-  }
-  if (late && n > 0) fin(ring + ((n - 1) % P::NST) * P::STAGE, sc, n - 1);
-  lds_barrier();
-}
-
-// Steps 0 .. n-1 of a ring: PIPE 0 plain, 1 cross-step overlap within a
-// wave, 2 ping-pong between the two waves of a SIMD.
-template <int W, int FP8, int PIPE, int RT, class Fetch, class Addr, class QK, class Fin>
+// Steps 0 .. n-1 of a ring: the scores of a step (qk) then the rest of it
+// (fin). The two waves of a SIMD overlap each other's matrix and vector work.
+template <int W, int FP8, int RT, class Fetch, class Addr, class QK, class Fin>
 __device__ __forceinline__ void run_steps(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
                                           Fetch fetch, Addr addr, QK qk, Fin fin, int tid) {
-  if constexpr (PIPE == 2) {
-    pingpong_loop<W, FP8, Scores<RT>>(ring, n, Kb, Vb, fetch, addr, qk, fin, tid);
-  } else if constexpr (PIPE == 1) {
-    pipe_loop<W, FP8, Scores<RT>>(ring, n, Kb, Vb, fetch, addr, qk, fin, tid);
-  } else {
-    ring_loop<W, FP8>(ring, n, Kb, Vb, fetch, addr, [&](const uint4* st, int s) {
-      Scores<RT> S;
-      qk(st, S);
-      fin(st, S, s);
-    }, tid);
-  }
+  ring_loop<W, FP8>(ring, n, Kb, Vb, fetch, addr, [&](const uint4* st, int s) {
+    Scores<RT> S;
+    qk(st, S);
+    fin(st, S, s);
+  }, tid);
 }
 
-template <int FP8, int W, int RT, int PIPE>
+template <int FP8, int W, int RT>
 __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled pooled,
                                                            const uint8_t* __restrict__ mask,
                                                            KeptLists kl, Plan plan,
@@ -801,7 +708,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
 #pragma unroll
           for (int k = 0; k < 8; ++k) ones[k] = 0x38383838;
           asm volatile("" : "+v"(ones));
-          run_steps<W, 1, PIPE, RT>(
+          run_steps<W, 1, RT>(
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
@@ -810,7 +717,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
               },
               tid);
         } else {
-          run_steps<W, 0, PIPE, RT>(
+          run_steps<W, 0, RT>(
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
@@ -892,7 +799,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
           (void)r;
           return (int64_t)J * kHeadDim * 2;
         };
-        run_steps<W, 0, PIPE, RT>(
+        run_steps<W, 0, RT>(
             ring, (np + kStep - 1) / kStep, Kh, Vh, fetch, addr,
             [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
             [&](const uint4* st, Scores<RT>& S, int s) {
@@ -947,14 +854,14 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
   }
 }
 
-template <int FP8, int W, int RT, int PIPE>
+template <int FP8, int W, int RT>
 hipError_t launch_cfg(const Problem& p, const Pooled& pooled, const uint8_t* mask,
                       const KeptLists& kl, const Plan& plan, void* out, float* lse,
                       hipStream_t s) {
   const int cus = device_compute_units();
   if (cus <= 0) return hipErrorInvalidDevice;
   const unsigned grid = (unsigned)std::min<int64_t>(plan.cap_items, cus);
-  attend_kernel<FP8, W, RT, PIPE><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, plan,
+  attend_kernel<FP8, W, RT><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, plan,
                                                           (uint16_t*)out, lse);
   return hipSuccess;
 }
@@ -968,8 +875,8 @@ hipError_t launch_dt(const Problem& p, const Pooled& pooled, const uint8_t* mask
                      const KeptLists& kl, const Plan& plan, void* out, float* lse,
                      hipStream_t s) {
   if (p.g * p.qtile < 256)
-    return launch_cfg<FP8, waves_for(128), 1, 0>(p, pooled, mask, kl, plan, out, lse, s);
-  return launch_cfg<FP8, ATT_W, 1, ATT_PIPE>(p, pooled, mask, kl, plan, out, lse, s);
+    return launch_cfg<FP8, waves_for(128), 1>(p, pooled, mask, kl, plan, out, lse, s);
+  return launch_cfg<FP8, ATT_W, 1>(p, pooled, mask, kl, plan, out, lse, s);
 }
 
 }  // namespace
