@@ -10,13 +10,17 @@
  * T_J = [J*B, min((J+1)*B, L))), per KV head h (group size g = Hq/Hkv) and
  * scale = softmax_scale (1/sqrt(d) by default):
  *
- * Prefix KV (chunked prefill): a sequence may hold L_kv >= L keys, of which
- * the L queries are the last ones (query i sits at absolute position
- * P0 + i, P0 = L_kv - L, a multiple of B). Key blocks are then those of the
- * L_kv keys, query block I sits at absolute block Ia = I + P0/B, and every
- * "J <= I" / "J == I" / "J < I" / "t <= p" below reads with Ia and absolute
- * positions; without a prefix P0 = 0 and Ia = I (Sec. 3.3 Eq. page, the
- * request's KV length; Sec. 4 chunked prefill).
+ * Prefix KV (chunked prefill, prefix caching): a sequence may hold L_kv >= L
+ * keys, of which the L queries are the last ones (query i sits at absolute
+ * position P0 + i, P0 = L_kv - L >= 0). Key blocks are then those of the L_kv
+ * keys. Query block I covers absolute positions a0 .. a1 (the first and last
+ * of its rows), which lie in key blocks Ja = a0/B and Jb = a1/B (Jb = Ja + 1
+ * when the block straddles a key-block boundary, which happens when P0 is not
+ * a multiple of B). Below, "J <= I" reads J <= Jb, "J == I" (the diagonal)
+ * reads Ja <= J <= Jb, "I - J" reads Jb - J, "J < I" (blocks fully visible to
+ * every row of the block) reads J < Ja, and "t <= p" uses absolute positions;
+ * without a prefix Ja = Jb = I (Sec. 3.3 Eq. page and the varlen execution
+ * from (L_q, L_kv); Sec. 4 chunked prefill).
  *
  *  1. Gather k_t, v_t (t < L_kv) through the page table:
  *     slot(b, t) = page_table[b][t / p] * p + t mod p            (Sec. 3.3, Eq. page)
@@ -48,9 +52,9 @@
  * query "block" I is the B positions [I*B, (I+1)*B) with all g heads of the
  * KV group (g*B packed rows). With tile_rows = R > 0 it is instead one M-tile
  * of R packed rows, i.e. the Pt = R/g positions [I*Pt, (I+1)*Pt) with all g
- * heads; Pt divides B, so a tile lies inside the single key block
- * Ia = (P0 + I*Pt)/B, and every rule above reads with that Ia (score and
- * select over J <= Ia, diagonal J == Ia, corrected J < Ia). Everything else is
+ * heads. Its rows lie in key blocks Ja .. Jb exactly as for a query block (one
+ * block when P0 is a multiple of B, since Pt divides B; at most two
+ * otherwise), and every rule above reads with them. Everything else is
  * unchanged; with R = g*B the two agree.
  *
  * Work is spread over POSIX threads by (b, h, I) unit; every unit is computed
@@ -225,10 +229,11 @@ static void pool_bh(ctx_t* c, int b, int h) {
 
 /* ---------------- steps 3-5: score, threshold, force ---------------- */
 
-static int forced_block(const ctx_t* c, int n, int I, int J) {
+/* forced blocks of a query block whose rows lie in key blocks Ja .. Jb */
+static int forced_block(const ctx_t* c, int n, int Ja, int Jb, int J) {
   const oracle_params* P = c->P;
-  if (J > I) return 0;
-  return J < P->sink_blocks || I - J < P->window_blocks || J == I || J >= n - P->recent_blocks;
+  if (J > Jb) return 0;
+  return J < P->sink_blocks || Jb - J < P->window_blocks || J >= Ja || J >= n - P->recent_blocks;
 }
 
 static void estimate_unit(ctx_t* c, int b, int h, int I) {
@@ -238,15 +243,16 @@ static void estimate_unit(ctx_t* c, int b, int h, int I) {
   if (I >= n) return;
   int nk = (kv_len(c, b) + B - 1) / B;
   int p0 = I * Pt, p1 = p0 + Pt < L ? p0 + Pt : L;
-  int Ia = (prefix_of(c, b) + p0) / B;       /* key block holding the tile's positions */
+  int Ja = (prefix_of(c, b) + p0) / B;       /* key blocks of the first and last row */
+  int Jb = (prefix_of(c, b) + p1 - 1) / B;
   int rows = (p1 - p0) * g;
   double* qrows = malloc(sizeof(double) * (size_t)rows * d);
   double* x = malloc(sizeof(double) * rows);
-  double* ell = malloc(sizeof(double) * (Ia + 1));
+  double* ell = malloc(sizeof(double) * (Jb + 1));
   for (int p = p0; p < p1; ++p)
     for (int j = 0; j < g; ++j) load_q(c, b, p, h * g + j, qrows + ((size_t)(p - p0) * g + j) * d);
   double mu = -INFINITY;
-  for (int J = 0; J <= Ia; ++J) {
+  for (int J = 0; J <= Jb; ++J) {
     const double* kh = c->khat + pool_index(c, b, h, J);
     double m = -INFINITY;
     for (int r = 0; r < rows; ++r) {
@@ -262,9 +268,9 @@ static void estimate_unit(ctx_t* c, int b, int h, int I) {
   double la = P->alpha > 0 ? log(P->alpha) : 0.0;
   for (int J = 0; J < c->nbk; ++J) {
     uint8_t byte = 0;
-    if (J <= Ia) {
+    if (J <= Jb) {
       int thr = P->alpha == 0.0 ? 1 : (ell[J] >= la + mu);
-      int f = forced_block(c, nk, Ia, J);
+      int f = forced_block(c, nk, Ja, Jb, J);
       byte = (uint8_t)((thr || f) | (f << 1));
       if (c->ell) c->ell[row + J] = ell[J];
     } else if (c->ell) {
@@ -288,16 +294,16 @@ static void attend_unit(ctx_t* c, int b, int h, int I) {
   int L = kv_len(c, b), P0 = prefix_of(c, b);
   const uint8_t* mrow = c->mask_in + (((size_t)b * P->num_kv_heads + h) * c->nbmax + I) * c->nbk;
   int p0 = I * Pt, p1 = p0 + Pt < Lq ? p0 + Pt : Lq;
-  int Ia = (P0 + p0) / B;                    /* key block holding the tile's positions */
+  int Ja = (P0 + p0) / B, Jb = (P0 + p1 - 1) / B;   /* key blocks of the first and last row */
   /* keys of the kept blocks, gathered once per unit */
   int nkeys = 0;
-  for (int J = 0; J <= Ia; ++J)
+  for (int J = 0; J <= Jb; ++J)
     if (mrow[J] & 1) nkeys += (J * B + B < L ? B : L - J * B);
   int* kt = malloc(sizeof(int) * (nkeys + 1));
   double* kk = malloc(sizeof(double) * ((size_t)nkeys + 1) * d);
   double* vv = malloc(sizeof(double) * ((size_t)nkeys + 1) * d);
   int idx = 0;
-  for (int J = 0; J <= Ia; ++J) {
+  for (int J = 0; J <= Jb; ++J) {
     if (!(mrow[J] & 1)) continue;
     int t1 = J * B + B < L ? J * B + B : L;
     for (int t = J * B; t < t1; ++t, ++idx) {
@@ -306,11 +312,11 @@ static void attend_unit(ctx_t* c, int b, int h, int I) {
       load_kv(c, c->v, c->vs, b, h, t, vv + (size_t)idx * d);
     }
   }
-  /* corrected blocks: J < Ia, not kept */
+  /* corrected blocks: J < Ja (fully visible to every row), not kept */
   int ncorr = 0;
-  int* cj = malloc(sizeof(int) * (Ia + 1));
+  int* cj = malloc(sizeof(int) * (Ja + 1));
   if (P->mean_correction)
-    for (int J = 0; J < Ia; ++J)
+    for (int J = 0; J < Ja; ++J)
       if (!(mrow[J] & 1)) cj[ncorr++] = J;
   double* q = malloc(sizeof(double) * d);
   double* lg = malloc(sizeof(double) * ((size_t)nkeys + ncorr + 1));
@@ -387,9 +393,9 @@ static int setup(ctx_t* c, const oracle_params* P, const void* q, const int32_t*
       P->num_q_heads % P->num_kv_heads != 0 || P->batch < 0)
     return 1;
   c->P = P; c->q = q; c->cu = cu; c->cuk = cuk ? cuk : cu; c->k = k; c->v = v; c->bt = bt;
-  for (int b = 0; b < P->batch; ++b) {       /* block-aligned prefixes only */
+  for (int b = 0; b < P->batch; ++b) {       /* at least as many keys as queries */
     int pre = c->cuk[b + 1] - c->cuk[b] - (c->cu ? c->cu[b + 1] - c->cu[b] : 0);
-    if (c->cu && (pre < 0 || pre % P->block_size != 0)) return 1;
+    if (c->cu && pre < 0) return 1;
   }
   c->qs = qs; c->ks = ks; c->vs = vs;
   c->g = P->num_q_heads / P->num_kv_heads;

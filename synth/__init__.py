@@ -71,9 +71,9 @@ class Spec:
     recent_blocks: int = 0
     mean_correction: int = 1
     seed: int = 0
-    # KV tokens before the queries of each sequence (chunked prefill): the
-    # queries are the last seqlens[b] of prefix[b] + seqlens[b] KV tokens.
-    # Multiples of block_size; None = no prefix.
+    # KV tokens before the queries of each sequence (chunked prefill, prefix
+    # caching): the queries are the last seqlens[b] of prefix[b] + seqlens[b]
+    # KV tokens; None = no prefix.
     prefix: Optional[List[int]] = None
 
     @property
@@ -267,7 +267,7 @@ def generate(spec: Spec) -> Workload:
     g = Hq // Hkv
     seed = sp.seed
     pre = sp.prefixes
-    assert all(x >= 0 and x % B == 0 for x in pre), "prefix lengths must be multiples of the block"
+    assert all(x >= 0 for x in pre), "prefix lengths must be non-negative"
     kvl = sp.kvlens
     # Q, K and V are drawn for all KV positions of a sequence; Q then keeps
     # its last seqlens[b] rows, so a chunk reproduces the rows of the whole

@@ -65,16 +65,20 @@ def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
-def forced_set(n, I, sink, window, recent):
-    return {J for J in range(I + 1) if J < sink or I - J < window or J == I or J >= n - recent}
+def forced_set(n, Ja, Jb, sink, window, recent):
+    """Forced blocks of a query block whose rows lie in key blocks Ja .. Jb."""
+    return {J for J in range(Jb + 1)
+            if J < sink or Jb - J < window or J >= Ja or J >= n - recent}
 
 
 def brute(wl, alpha, sink=None, window=None, recent=None, correction=None, scale=None,
           tile_rows=0):
-    """mask [b, Hkv, nt, nb], ell (same shape, NaN above diag), out [total, Hq, d], lse.
+    """mask [b, Hkv, nt, nbk], ell (same shape, NaN above the last visible
+    block), out [total, Hq, d], lse.
 
     tile_rows > 0: a query tile is tile_rows packed rows (tile_rows / g
-    positions with all g heads) instead of a block of B positions."""
+    positions with all g heads) instead of a block of B positions. With a
+    prefix the queries sit at absolute positions prefix + i."""
     sp = wl.spec
     sink = sp.sink_blocks if sink is None else sink
     window = sp.window_blocks if window is None else window
@@ -85,63 +89,65 @@ def brute(wl, alpha, sink=None, window=None, recent=None, correction=None, scale
     scale = 1.0 / np.sqrt(d) if scale is None else scale
     Q, K, V = decode(wl)
     Pt = tile_rows // g if tile_rows else B          # positions per query tile
-    nbmax = max(1, (sp.max_seq_len + B - 1) // B)
+    nbk = max(1, (sp.max_kv_len + B - 1) // B)
     ntmax = max(1, (sp.max_seq_len + Pt - 1) // Pt)
-    mask = np.zeros((sp.batch, Hkv, ntmax, nbmax), np.uint8)
+    mask = np.zeros((sp.batch, Hkv, ntmax, nbk), np.uint8)
     ell = np.full(mask.shape, np.nan)
     out = np.full(Q.shape, np.nan)
     lse = np.full(Q.shape[:2], np.nan)
-    cu = wl.cu_seqlens
-    for b, L in enumerate(sp.seqlens):
-        if L == 0:
+    cu, ck = wl.cu_seqlens, wl.cu_seqlens_k
+    for b, Lq in enumerate(sp.seqlens):
+        if Lq == 0:
             continue
-        n = (L + B - 1) // B
-        blk = np.arange(L) // B
+        Lk = sp.kvlens[b]
+        P0 = Lk - Lq
+        n = (Lk + B - 1) // B
+        blk = np.arange(Lk) // B
+        tile = np.arange(Lq) // Pt
         for h in range(Hkv):
-            Kb = K[cu[b]:cu[b] + L, h]
-            Vb = V[cu[b]:cu[b] + L, h]
+            Kb = K[ck[b]:ck[b] + Lk, h]
+            Vb = V[ck[b]:ck[b] + Lk, h]
             kbar = np.stack([Kb[blk == J].mean(0) for J in range(n)])
             vbar = np.stack([Vb[blk == J].mean(0) for J in range(n)])
             khat = bf16_bits_to_f64(bf16_round_bits(kbar))
-            Qg = Q[cu[b]:cu[b] + L, h * g:(h + 1) * g]          # [L, g, d]
-            S = np.einsum("lgd,jd->lgj", Qg, khat) * scale     # [L, g, n]
-            tile = np.arange(L) // Pt
-            for t in range((L + Pt - 1) // Pt):
-                I = t * Pt // B                               # key block of the tile
-                rows = S[tile == t].reshape(-1, n)[:, :I + 1]
+            Qg = Q[cu[b]:cu[b] + Lq, h * g:(h + 1) * g]         # [Lq, g, d]
+            S = np.einsum("lgd,jd->lgj", Qg, khat) * scale     # [Lq, g, n]
+            for t in range((Lq + Pt - 1) // Pt):
+                pos = np.arange(t * Pt, min(Lq, (t + 1) * Pt))  # local positions
+                Ja, Jb = (P0 + pos[0]) // B, (P0 + pos[-1]) // B
+                rows = S[tile == t].reshape(-1, n)[:, :Jb + 1]
                 e = logsumexp(rows, axis=0)
-                ell[b, h, t, :I + 1] = e
+                ell[b, h, t, :Jb + 1] = e
                 order = np.argsort(-e, kind="stable")
                 top = e[order[0]]
                 kept = set()
                 if alpha == 0:
-                    kept = set(range(I + 1))
+                    kept = set(range(Jb + 1))
                 else:
                     for J in order:
                         if e[J] >= np.log(alpha) + top:
                             kept.add(int(J))
                         else:
                             break
-                forced = forced_set(n, I, sink, window, recent)
-                for J in range(I + 1):
+                forced = forced_set(n, Ja, Jb, sink, window, recent)
+                for J in range(Jb + 1):
                     kb = J in kept or J in forced
                     mask[b, h, t, J] = int(kb) | (int(J in forced) << 1)
                 # attention rows of the tile: pruned blocks -> mean tokens
                 keptb = mask[b, h, t, :n] & 1
                 Km, Vm = Kb.copy(), Vb.copy()
                 allowed_blk = np.zeros(n, bool)
-                for J in range(I + 1):
+                for J in range(Jb + 1):
                     if keptb[J]:
                         allowed_blk[J] = True
-                    elif corr and J < I:
+                    elif corr and J < Ja:
                         Km[blk == J] = kbar[J]
                         Vm[blk == J] = vbar[J]
                         allowed_blk[J] = True
-                pos = np.arange(t * Pt, min(L, (t + 1) * Pt))
                 for j in range(g):
                     qrow = Q[cu[b] + pos, h * g + j]            # [P, d]
-                    lg = qrow @ Km.T * scale                   # [P, L]
-                    ok = allowed_blk[blk][None, :] & (np.arange(L)[None, :] <= pos[:, None])
+                    lg = qrow @ Km.T * scale                   # [P, Lk]
+                    ok = allowed_blk[blk][None, :] & (np.arange(Lk)[None, :] <= P0 + pos[:, None])
                     lg = np.where(ok, lg, -np.inf)
                     m = lg.max(1, keepdims=True)
                     w = np.exp(lg - m)

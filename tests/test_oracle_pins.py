@@ -86,7 +86,7 @@ def test_p2_alpha_above_one_keeps_forced_only(sink, window, recent):
         n = (L + B - 1) // B
         for h in range(2):
             for I in range(n):
-                f = brute.forced_set(n, I, sink, window, recent)
+                f = brute.forced_set(n, I, I, sink, window, recent)
                 for J in range(mask.shape[-1]):
                     want = (1 | 2) if J in f else 0
                     assert mask[b, h, I, J] == want, (b, h, I, J)
