@@ -36,13 +36,16 @@
  * ---------------------------
  * A sequence may hold more keys than queries: its L_q queries (cu_seqlens)
  * are the last L_q of its L_kv keys (cu_seqlens_k), i.e. query i sits at
- * absolute position P + i with P = L_kv - L_q, the tokens already in the KV
- * cache from earlier chunks. P must be a multiple of block_size, so query
- * block I is key block Ia = I + P / block_size, and every rule below that
- * compares a query block or position with a key block or position uses Ia
- * and the absolute position. With cu_seqlens_k == NULL, L_kv = L_q (P = 0).
- * The selection of a query block depends only on its own rows and the keys
- * before it, so a chunked prefill gives, row for row, the output of one call
+ * absolute position P + i with P = L_kv - L_q >= 0, the tokens already in
+ * the KV cache (earlier chunks, a cached prefix). The rows of query block I
+ * then lie in key blocks Ja (that of its first row) to Jb (that of its last
+ * row): Jb = Ja when P is a multiple of block_size, else possibly Ja + 1. In
+ * every rule below, "J <= I" reads J <= Jb, the diagonal "J == I" reads
+ * Ja <= J <= Jb, "I - J" reads Jb - J, and "J < I" (blocks every row sees in
+ * full) reads J < Ja; positions are absolute. With cu_seqlens_k == NULL,
+ * L_kv = L_q (P = 0, Ja = Jb = I). The selection of a query block depends
+ * only on its own rows and the keys before them, so with P a multiple of
+ * block_size a chunked prefill gives, row for row, the output of one call
  * over the whole sequence.
  *
  * KV splits and the work plan (Sec. 3.3 Eq. split and Eq. cost)
@@ -89,8 +92,7 @@
  *   cu_seqlens   int32 [batch + 1], cu_seqlens[0] == 0, non-decreasing:
  *                the query rows.
  *   cu_seqlens_k int32 [batch + 1] or NULL: the KV lengths, same rules;
- *                cu_seqlens_k[b+1] - cu_seqlens_k[b] >= the query length,
- *                the difference a multiple of block_size.
+ *                cu_seqlens_k[b+1] - cu_seqlens_k[b] >= the query length.
  *   q/k/v_scale  fp32 per head ([num_q_heads] / [num_kv_heads] / [num_kv_heads]);
  *                only read when dtype == FP2_FP8_E4M3 (the dequantised value
  *                is scale * code, Sec. 3.3 Eq. fp8; a per-tensor scale is the

@@ -42,11 +42,13 @@
 // dtypes), logits shifted by log2|B_J| = 7 (Sec. 3.2 implementation
 // paragraph).
 //
-// Prefix KV (chunked prefill): the queries of a sequence may be the last
-// L_q of its L_kv keys. Keys, key blocks and the pooled means are then those
-// of the L_kv tokens, query block I is key block Ia = I + (L_kv - L_q)/B, and
-// the causal mask, the diagonal and the correction range J < Ia use absolute
-// positions; query rows and the LSE are indexed by the local position.
+// Prefix KV (chunked prefill, prefix caching): the queries of a sequence may
+// be the last L_q of its L_kv keys. Keys, key blocks and the pooled means are
+// then those of the L_kv tokens; the rows of query block (or tile) I lie in
+// key blocks Ja .. Jb (two blocks when the prefix is not a multiple of B). The
+// causal mask applies to the kept blocks J >= Ja and the correction to the
+// pruned J < Ja, with absolute positions; query rows and the LSE are indexed
+// by the local position.
 #include <algorithm>
 #include <utility>
 
@@ -570,12 +572,12 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     const int b = bh / p.hkv, h = bh % p.hkv;
     const int Lq = p.cu[b + 1] - p.cu[b];
     if (I * p.qtile >= Lq) continue;
-    // KV tokens of the sequence (a prefix included) and the absolute key
-    // block Ia of query block I; positions below are absolute, and query
-    // position x is packed row qbase + x
+    // KV tokens of the sequence (a prefix included) and the key blocks Ja,
+    // Jb of the unit's first and last row; positions below are absolute, and
+    // query position x is packed row qbase + x
     const int64_t tok0 = p.cuk[b];
     const int L = p.cuk[b + 1] - (int)tok0;
-    const int Ia = (L - Lq + I * p.qtile) / kBlock;   // key block holding the unit's rows
+    const int Ja = (L - Lq + I * p.qtile) / kBlock;
     const int64_t qbase = (int64_t)p.cu[b] - (L - Lq);
 
     const int lane = tid & 63, w = tid >> 6;
@@ -619,7 +621,10 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       constexpr int esz = FP8 ? 1 : 2;
       const int cnt = kl.cnt[row];
       const int32_t* kidx = kl.idx + row * p.nbk;
-      const bool has_diag = cnt > 0 && kidx[cnt - 1] == Ia;
+      // Kept blocks J >= Ja hold keys after some row of the unit and need the
+      // causal mask: at most two (Ja and Jb), the first of the descending walk.
+      const int e0 = cnt > 0 ? kidx[cnt - 1] : -1, e1 = cnt > 1 ? kidx[cnt - 2] : -1;
+      const int nmask = (e0 >= Ja) + (e1 >= Ja);
       // Eq. split: part sp walks list positions [lo, hi) of the descending
       // walk, ceil(cnt / nsp) each
       const int per = (cnt + nsp - 1) / nsp;
@@ -700,7 +705,6 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
           return sl * rowbytes + hbytes;
         };
         const int nst = 2 * nbc;
-        const int ndiag = (c0 == 0 && has_diag) ? 2 : 0;   // the diagonal block comes first
         if constexpr (FP8) {
           // all-ones A operand of the row-sum MFMA (e4m3 1.0 = 0x38), opaque so
           // that it stays in registers instead of being rebuilt every step
@@ -712,8 +716,9 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
-                fin_fp8<RT>(st, S, rs, cs, Ia * kBlock + kStep * (s & 1), pos, s < ndiag, lane,
-                            ones);
+                const int wp = c0 + (s >> 1);   // walk position of the step's block
+                fin_fp8<RT>(st, S, rs, cs, (wp == 0 ? e0 : e1) * kBlock + kStep * (s & 1), pos,
+                            wp < nmask, lane, ones);
               },
               tid);
         } else {
@@ -721,8 +726,10 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
-                fin_bf16<0, RT, NPRE>(st, S, rs, cs, off, 1.f, Ia * kBlock + kStep * (s & 1), pos,
-                                      s < ndiag, 0, lane);
+                const int wp = c0 + (s >> 1);   // walk position of the step's block
+                fin_bf16<0, RT, NPRE>(st, S, rs, cs, off, 1.f,
+                                      (wp == 0 ? e0 : e1) * kBlock + kStep * (s & 1), pos,
+                                      wp < nmask, 0, lane);
               },
               tid);
         }
@@ -734,10 +741,11 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
       for (int rt = 0; rt < RT; ++rt) rs.l[rt] += half == 0 ? rs.ls[rt][0] : 0.f;
     }
 
-    // ---- mean correction over the pruned blocks J < Ia, compacted into a
-    // list; split sp takes the blocks J in [jlo, jhi)
-    const int perj = (Ia + nsp - 1) / nsp;
-    const int jlo = min(Ia, sp * perj), jhi = min(Ia, jlo + perj);
+    // ---- mean correction over the pruned blocks J < Ja (fully visible to
+    // every row of the unit), compacted into a list; split sp takes the
+    // blocks J in [jlo, jhi)
+    const int perj = (Ja + nsp - 1) / nsp;
+    const int jlo = min(Ja, sp * perj), jhi = min(Ja, jlo + perj);
     if (p.corr && jhi > jlo) {
       const uint8_t* mrow = mask + row * p.nbk;
       uint16_t* plist = (uint16_t*)aux;

@@ -19,8 +19,9 @@
 // row is written in full (zeros past I) and the kept blocks are compacted in
 // ascending order with wave ballots into the per-row list of the workspace.
 // With a prefix KV (the queries are the last keys of the sequence) the key
-// blocks are those of the KV tokens and query block I is key block
-// Ia = I + prefix/B; every comparison of I with a key block uses Ia.
+// blocks are those of the KV tokens, and the rows of query tile I lie in key
+// blocks Ja .. Ia: blocks up to Ia are scored, the band Ja .. Ia is forced
+// (the diagonal) and the window counts back from Ia.
 //
 // Precision: fp8 queries are widened to bf16 exactly, the per-head fp8 scale
 // is applied in fp32 after the MFMA, and exponentials use the hardware
@@ -75,10 +76,12 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
   const int64_t tok0 = p.cu[b];
   const int L = p.cu[b + 1] - (int)tok0;
   const int n = (L + p.qtile - 1) / p.qtile;   // query tiles of the sequence
-  // KV tokens and key blocks; query tile I lies in key block Ia
+  // KV tokens and key blocks; the rows of query tile I lie in key blocks
+  // Ja .. Ib (Ib = Ja + 1 when the tile straddles a key-block boundary)
   const int Lk = p.cuk[b + 1] - p.cuk[b];
   const int nk = (Lk + kBlock - 1) / kBlock;
-  const int Ia = (Lk - L + I * p.qtile) / kBlock;
+  const int Ja = (Lk - L + I * p.qtile) / kBlock;
+  const int Ia = (Lk - L + min(L, (I + 1) * p.qtile) - 1) / kBlock;   // last visible key block
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
   uint8_t* mrow = mask + row * p.nbk;
 
@@ -273,7 +276,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
   for (int J0 = 0; J0 < p.nbk; J0 += kThreads) {
     const int J = J0 + tid;
     const bool valid = J <= Ia;
-    const bool forced = valid && (J < p.sink || Ia - J < p.window || J == Ia || J >= nk - p.recent);
+    const bool forced = valid && (J < p.sink || Ia - J < p.window || J >= Ja || J >= nk - p.recent);
     const bool keep = valid && (keep_all || forced || ell[J] >= thr);
     if (J < p.nbk) mrow[J] = (uint8_t)((keep ? 1 : 0) | (forced ? 2 : 0));
     if (J0 <= Ia) {
@@ -307,7 +310,8 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int L = p.cu[b + 1] - p.cu[b];
   const int n = (L + p.qtile - 1) / p.qtile;
-  const int Ia = (p.cuk[b + 1] - p.cuk[b] - L + I * p.qtile) / kBlock;   // key block of tile I
+  // last key block visible to tile I (that of its last row)
+  const int Ia = (p.cuk[b + 1] - p.cuk[b] - L + min(L, (I + 1) * p.qtile) - 1) / kBlock;
   const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
   if (I >= n) {
     if (tid == 0) kl.cnt[row] = 0;

@@ -17,14 +17,14 @@ namespace {
 
 constexpr int kTile = 64;   // keys per physical tile
 
-// Unit row -> (b, h, I), the number of key blocks visible to the tile and the
-// KV length; false for a tile past its sequence.
+// Segment -> the last key block visible to its tile (that of its last row)
+// and the KV length; false for a tile past its sequence.
 __device__ __forceinline__ bool segment(const Problem& p, int s, int& Ia, int& Lk) {
   const int I = s % p.nbmax, bh = s / p.nbmax, b = bh / p.hkv;
   const int Lq = p.cu[b + 1] - p.cu[b];
   if (I * p.qtile >= Lq) return false;
   Lk = p.cuk[b + 1] - p.cuk[b];
-  Ia = (Lk - Lq + I * p.qtile) / kBlock;
+  Ia = (Lk - Lq + min(Lq, (I + 1) * p.qtile) - 1) / kBlock;   // block of the tile's last row
   return true;
 }
 

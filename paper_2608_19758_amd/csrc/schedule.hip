@@ -111,9 +111,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, KeptLists
     const int Lq = p.cu[b + 1] - p.cu[b];
     int cost = -1;
     if (I * p.qtile < Lq) {
-      const int Ia = (p.cuk[b + 1] - p.cuk[b] - Lq + I * p.qtile) / kBlock;
+      const int Ia = (p.cuk[b + 1] - p.cuk[b] - Lq + min(Lq, (I + 1) * p.qtile) - 1) / kBlock;
       const int cnt = kl.cnt[row];
-      const int pruned = p.corr ? max(0, Ia + 1 - cnt) : 0;
+      const int pruned = p.corr ? max(0, Ia + 1 - cnt) : 0;   // at most, below the last block
       cost = 2 * cnt + (pruned + 63) / 64 + kItemSteps;
       tot += (double)cost * wpu;
       mx = max(mx, cost);

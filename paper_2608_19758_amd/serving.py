@@ -16,9 +16,9 @@ while decode attention stays dense):
 - ``forward_extend``: one layer's attention over the paged cache, through the
   C ABI. The K/V of the new tokens must already be in the cache.
 
-Cached prefixes must be multiples of the 128-token selection block (chunked
-prefill with block-multiple chunk sizes); ``plan_forward`` rejects other
-lengths before anything reaches the GPU.
+Cached prefixes may have any length (a prefix-cache hit is page-granular);
+``plan_forward`` checks the lengths against the configured bounds before
+anything reaches the GPU.
 """
 from __future__ import annotations
 
@@ -48,6 +48,7 @@ class BackendConfig:
     mean_correction: bool = True
     kv_splits: int = 0             # 0: cost-balanced plan on the device
     softmax_scale: float = 0.0     # <= 0: 1/sqrt(128)
+    query_tile_rows: int = 0       # 0: query blocks of 128 positions; 128: 128-row tiles
 
     @property
     def max_pages_per_seq(self) -> int:
@@ -61,7 +62,7 @@ class BackendConfig:
             sink_blocks=self.sink_blocks, window_blocks=self.window_blocks,
             recent_blocks=self.recent_blocks, mean_correction=int(self.mean_correction),
             softmax_scale=self.softmax_scale, dtype=self.dtype, max_kv_len=max_kv,
-            kv_splits=self.kv_splits)
+            kv_splits=self.kv_splits, query_tile_rows=self.query_tile_rows)
 
     def worst_case_params(self) -> "fp2.Params":
         return self.params(self.max_batch, self.max_extend_len, self.max_kv_len)
@@ -94,9 +95,6 @@ def plan_forward(cfg: BackendConfig, extend_lens: Sequence[int],
         if p + e > cfg.max_kv_len:
             raise ValueError("sequence %d: %d cached + %d new > max_kv_len %d"
                              % (b, p, e, cfg.max_kv_len))
-        if p % BLOCK:
-            raise ValueError("sequence %d: cached prefix %d is not a multiple of %d"
-                             % (b, p, BLOCK))
     cu_q = np.zeros(len(ext) + 1, np.int32)
     cu_k = np.zeros(len(ext) + 1, np.int32)
     cu_q[1:] = np.cumsum(ext)
@@ -132,8 +130,7 @@ class PrefillBackend:
         if need == 0 and cfg.max_batch > 0:
             raise ValueError("configuration rejected by the library: " + fp2.last_error())
         self.workspace = torch.empty(max(1, need), dtype=torch.uint8, device=self.device)
-        nq = (cfg.max_extend_len + BLOCK - 1) // BLOCK
-        nk = (cfg.max_kv_len + BLOCK - 1) // BLOCK
+        nq, nk = fp2.num_blocks(worst), fp2.num_key_blocks(worst)
         self._mask = torch.empty(max(1, cfg.max_batch * cfg.num_kv_heads * nq * nk),
                                  dtype=torch.uint8, device=self.device)
 

@@ -162,13 +162,13 @@ def test_host_kv_lengths_checked():
     assert call_prefill(p, cuh=host(cu), cuk=FAKE, cukh=host(good)) == fp2.EWORKSPACE
     # host KV lengths without the device array
     assert call_prefill(p, cuh=host(cu), cukh=host(good)) == fp2.EINVAL
-    # a prefix that is not a multiple of the block size
-    bad = np.array([0, 300 + 100, 400 + 700], dtype=np.int32)        # prefix 100
-    assert call_prefill(p, cuh=host(cu), cuk=FAKE, cukh=host(bad)) == fp2.EINVAL
-    assert "block_size" in fp2.last_error()
+    # a prefix that is not a multiple of the block size is accepted
+    odd = np.array([0, 300 + 100, 400 + 700 + 1], dtype=np.int32)    # prefixes 100 and 1
+    assert call_prefill(p, cuh=host(cu), cuk=FAKE, cukh=host(odd)) == fp2.EWORKSPACE
     # fewer keys than queries
     bad = np.array([0, 200, 900], dtype=np.int32)                    # 200 keys < 300 queries
     assert call_prefill(p, cuh=host(cu), cuk=FAKE, cukh=host(bad)) == fp2.EINVAL
+    assert "KV length < query length" in fp2.last_error()
     # a KV length over max_kv_len
     bad = np.array([0, 300 + 8192, 8492 + 700], dtype=np.int32)
     assert call_prefill(p, cuh=host(cu), cuk=FAKE, cukh=host(bad)) == fp2.EINVAL

@@ -46,6 +46,12 @@ CASES = {
     "fp8_paged": dict(lens=[800, 200], prefix=[640, 128], hq=8, hkv=2, dtype="fp8", page=64),
     "fp8_perm": dict(lens=[333], prefix=[1152], hq=8, hkv=1, dtype="fp8", page=16,
                      order="permuted"),
+    # prefixes that are not block multiples: query blocks straddle two key blocks
+    "bf16_unaligned": dict(lens=[300, 129, 5, 0], prefix=[100, 1, 1000, 77], hq=4, hkv=2,
+                           page=16),
+    "fp8_unaligned": dict(lens=[420], prefix=[127], hq=8, hkv=2, dtype="fp8", page=64,
+                          window=1, recent=1),
+    "g1_unaligned_contig": dict(lens=[260, 64], prefix=[65, 129], hq=2, hkv=2, page=0),
 }
 
 
@@ -95,11 +101,12 @@ def test_prefix_prefill_parity(name, alpha):
     assert ob == 0
     B = sp.block_size
     for b, (L, P) in enumerate(zip(sp.seqlens, sp.prefixes)):
-        nq, nk, off = (L + B - 1) // B, (L + P + B - 1) // B, P // B
+        nq, nk = (L + B - 1) // B, (L + P + B - 1) // B
         assert (gmask[b, :, nq:, :] == 0).all() and (gmask[b, :, :, nk:] == 0).all()
-        for I in range(nq):   # nothing past the query block's own key block
-            assert (gmask[b, :, I, I + off + 1:] == 0).all()
-            assert (gmask[b, :, I, I + off] == 3).all()   # the diagonal is forced and kept
+        for I in range(nq):   # nothing past the block of the last row; the band is forced
+            Ja, Jb = (P + I * B) // B, (P + min(L, (I + 1) * B) - 1) // B
+            assert (gmask[b, :, I, Jb + 1:] == 0).all()
+            assert (gmask[b, :, I, Ja:Jb + 1] == 3).all()
     oout, olse = oracle.attend(inp, op, gmask)
     err = np.abs(out - oout).max() if out.size else 0.0
     lerr = np.abs(lse - olse).max() if lse.size else 0.0
@@ -108,7 +115,7 @@ def test_prefix_prefill_parity(name, alpha):
     assert lerr <= gu.LSE_TOL[sp.dtype]
 
 
-@pytest.mark.parametrize("name", ["bf16_paged_ragged", "fp8_perm"])
+@pytest.mark.parametrize("name", ["bf16_paged_ragged", "fp8_perm", "bf16_unaligned"])
 @pytest.mark.parametrize("corr", [0, 1])
 def test_prefix_attend_external_mask(name, corr):
     """fp2_attend under the oracle's mask equals the oracle under that mask."""

@@ -40,6 +40,7 @@ CASES = {
     "fp8_paged": dict(lens=[1800, 333], hq=8, hkv=2, dtype="fp8", page=64),
     "fp8_g8_prefix": dict(lens=[300], prefix=[2048], hq=8, hkv=1, dtype="fp8", page=16,
                           order="permuted"),
+    "bf16_unaligned": dict(lens=[500, 70], prefix=[1000, 31], hq=4, hkv=2, page=32),
 }
 
 

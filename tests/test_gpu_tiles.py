@@ -39,6 +39,7 @@ CASES = {
                            order="permuted"),
     "g4_fp8": dict(lens=[1200], hq=8, hkv=2, dtype="fp8", page=64, recent=1),
     "g8_fp8_prefix": dict(lens=[333, 130], prefix=[256, 0], hq=8, hkv=1, dtype="fp8", page=32),
+    "g4_unaligned": dict(lens=[400, 90], prefix=[50, 300], hq=8, hkv=2, page=64),
 }
 
 
@@ -113,8 +114,8 @@ def csr_reference(mask, wl, Pt):
         for h in range(sp.num_kv_heads):
             for t in range(mask.shape[2]):
                 if t * Pt < Lq:
-                    Ia = (Lk - Lq + t * Pt) // B
-                    for J in range(Ia + 1):
+                    Jb = (Lk - Lq + min(Lq, (t + 1) * Pt) - 1) // B   # block of the last row
+                    for J in range(Jb + 1):
                         if mask[b, h, t, J] & 1:
                             idx.append(2 * J)
                             if (2 * J + 1) * 64 < Lk:
@@ -123,7 +124,7 @@ def csr_reference(mask, wl, Pt):
     return np.array(offs, np.int32), np.array(idx, np.int32)
 
 
-@pytest.mark.parametrize("name", ["g4_paged", "g2_perm_prefix", "g8_fp8_prefix"])
+@pytest.mark.parametrize("name", ["g4_paged", "g2_perm_prefix", "g8_fp8_prefix", "g4_unaligned"])
 @pytest.mark.parametrize("tile", [0, R])
 @pytest.mark.parametrize("alpha", [0.0, 0.99])
 def test_mask_to_csr(name, tile, alpha):

@@ -10,6 +10,11 @@ CFG = serving.BackendConfig(num_q_heads=32, num_kv_heads=8, page_size=64, max_ba
                             max_extend_len=8192, max_kv_len=65536, dtype="fp8")
 
 
+def test_plan_forward_unaligned_prefix():
+    plan = serving.plan_forward(CFG, [100, 64], [100, 4097])
+    assert plan.cu_k.tolist() == [0, 200, 4361]
+
+
 def test_plan_forward_arrays():
     plan = serving.plan_forward(CFG, [300, 8192, 1], [1024, 0, 4096])
     assert plan.cu_q.tolist() == [0, 300, 8492, 8493]
@@ -21,7 +26,6 @@ def test_plan_forward_arrays():
 
 
 @pytest.mark.parametrize("ext,pre,msg", [
-    ([100], [100], "multiple of 128"),
     ([9000], [0], "max_extend_len"),
     ([8192], [65536 - 4096], "max_kv_len"),
     ([1, 1, 1, 1, 1], None, "max_batch"),
@@ -40,7 +44,7 @@ def test_worst_case_workspace_bounds_every_forward():
     for _ in range(200):
         b = int(rng.integers(1, CFG.max_batch + 1))
         ext = rng.integers(0, CFG.max_extend_len + 1, size=b)
-        pre = rng.integers(0, (CFG.max_kv_len - ext) // 128 + 1) * 128
+        pre = rng.integers(0, CFG.max_kv_len - ext + 1)
         plan = serving.plan_forward(CFG, ext.tolist(), pre.tolist())
         assert 0 <= fp2.workspace_bytes(plan.params) <= worst
     # fixed split counts scale the partial outputs with the problem, still bounded
