@@ -72,10 +72,10 @@
  * [I*B, (I+1)*B) with all g = num_q_heads/num_kv_heads heads of the KV group
  * (g*B packed rows). With query_tile_rows = 128 it is the paper's M-tile of
  * 128 packed rows: the Pt = 128/g positions [I*Pt, (I+1)*Pt) with all g
- * heads. Pt divides B, so tile I lies inside key block
- * Ia = (prefix + I*Pt)/B, and every rule below that names "query block I"
- * (J <= I, J == I, J < I, I - J) reads with that Ia. With g = 1 the two
- * tiles coincide.
+ * heads. Everything said of a query block holds for a tile: its rows lie in
+ * key blocks Ja .. Jb (a single block when the prefix is a multiple of B,
+ * since Pt divides B), and the rules below read with them. With g = 1 the
+ * two tiles coincide.
  *
  * Layouts (row-major, innermost last)
  * -----------------------------------
