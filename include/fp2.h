@@ -155,7 +155,7 @@ typedef enum {
 typedef struct {
   int32_t batch;              /* number of sequences, >= 0 */
   int32_t num_q_heads;        /* H_q, a multiple of num_kv_heads */
-  int32_t num_kv_heads;       /* H_kv >= 1; g = H_q / H_kv must be 1, 2, 4 or 8 */
+  int32_t num_kv_heads;       /* 1 <= H_kv <= 1024; g = H_q / H_kv must be 1, 2, 4 or 8 */
   int32_t head_dim;           /* d: must be 128 */
   int32_t block_size;         /* selection block B in tokens: must be 128 */
   int32_t page_size;          /* p >= 1 tokens per page, or 0 for contiguous KV */

@@ -107,6 +107,8 @@ fp2_status_t validate_params(const fp2_params_t* p) {
   if (!p) return fail(FP2_EINVAL, "params is null");
   if (p->batch < 0) return fail(FP2_EINVAL, "batch %d < 0", p->batch);
   if (p->num_kv_heads < 1) return fail(FP2_EINVAL, "num_kv_heads %d < 1", p->num_kv_heads);
+  if (p->num_kv_heads > 1024)
+    return fail(FP2_EUNSUPPORTED, "num_kv_heads %d > 1024", p->num_kv_heads);
   if (p->num_q_heads < 1 || p->num_q_heads % p->num_kv_heads)
     return fail(FP2_EINVAL, "num_q_heads %d is not a positive multiple of num_kv_heads %d",
                 p->num_q_heads, p->num_kv_heads);

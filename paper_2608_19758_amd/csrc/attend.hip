@@ -678,11 +678,12 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
 #pragma unroll 1
       for (int c0 = lo; c0 < hi; c0 += chunk) {
         const int nbc = min(chunk, hi - c0);
-        // Record (block i, half hf, group e) = {slot of its first row, that
-        // row's index in the half, last valid row index}: row r of the half
-        // then lives at slot + min(r, last) - first. Rows past the sequence
-        // thus repeat its last token (finite data; those keys are masked); a
-        // group that starts past it points at that token directly.
+        // Record (block i, half hf, group e) = {byte offset at which row 0 of
+        // the half would lie if the group's page continued down to it (64-bit,
+        // may be negative), last valid row index}: row r of the half then
+        // lies at base + min(r, last) * rowbytes. Rows past the sequence thus
+        // repeat its last token (finite data; those keys are masked); a group
+        // that starts past it points at that token directly.
         for (int k = tid; k < nbc * 2 * rph; k += 64 * W) {
           const int i = k / (2 * rph), hk = k - i * 2 * rph;
           const int key0 = kidx[cnt - 1 - (c0 + i)] * kBlock + kStep * (hk >= rph);
@@ -695,14 +696,16 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
             slot = slot_of(L - 1);
             first = last;
           }
-          aux[k] = make_uint4(slot, (uint32_t)first, (uint32_t)last, 0u);
+          const int64_t base = ((int64_t)slot - first) * rowbytes + hbytes;
+          aux[k] = make_uint4((uint32_t)base, (uint32_t)((uint64_t)base >> 32), (uint32_t)last, 0u);
         }
         __syncthreads();
         auto fetch = [&](int s, int r) -> uint4 { return aux[(s * rph) + (r >> gshift)]; };
+        const int rowb = (int)rowbytes;   // <= 2^18 (Hkv <= 1024), so 63 * rowb fits int32
         auto addr = [&](uint4 rec, int s, int r) -> int64_t {
           (void)s;
-          const int64_t sl = (int64_t)rec.x + (min(r, (int)rec.z) - (int)rec.y);
-          return sl * rowbytes + hbytes;
+          const int64_t base = (int64_t)(((uint64_t)rec.y << 32) | rec.x);
+          return base + min(r, (int)rec.z) * rowb;
         };
         const int nst = 2 * nbc;
         if constexpr (FP8) {

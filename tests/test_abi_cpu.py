@@ -67,6 +67,7 @@ def call_prefill(p, **over):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(num_kv_heads=0), fp2.EINVAL),
+    (dict(num_kv_heads=2048, num_q_heads=2048), fp2.EUNSUPPORTED),
     (dict(num_q_heads=30), fp2.EINVAL),
     (dict(num_q_heads=48, num_kv_heads=8), fp2.EUNSUPPORTED),      # g = 6
     (dict(num_q_heads=128, num_kv_heads=8), fp2.EUNSUPPORTED),     # g = 16
