@@ -75,3 +75,37 @@ def test_fullsize_attention_flops_accounting():
     fk, fc = acc.attention_flops(gmask, sp.seqlens, 32, 8)
     assert fk == 4 * 128 * 4 * 128 * 128 * kept
     assert fc == 4 * 128 * 4 * 128 * corr
+
+
+def test_maximum_sequence_length():
+    """One sequence of 1,048,576 tokens, the largest the library admits (8192
+    key blocks: the longest energy row, kept lists and correction lists),
+    fp8, 4 query heads on 1 KV head, paged; sampled units against the oracle
+    and the closed-form forced bits everywhere."""
+    sp = synth.Spec("max1m", [1 << 20], 4, 1, dtype="fp8", page_size=64, salient_frac=0.005,
+                    salient_min=1, sink_blocks=1, window_blocks=2, seed=17)
+    print("workload 1M tokens", flush=True)
+    wl = synth.generate(sp)
+    alpha = 0.98
+    out, gmask, lse = gu.gpu_prefill(wl, gu.params_for(wl, alpha))
+    assert np.isfinite(out).all() and np.isfinite(lse).all()
+    n = (1 << 20) // 128
+    assert gmask.shape == (1, 1, n, n)
+    f = forced_closed_form(n, 1, 2, 0)
+    assert ((gmask[0, 0] & 2).astype(bool) == f).all()
+    kept = oracle.kept_ratio(gmask, sp.seqlens, 128)
+    print("kept ratio %.5f" % kept)
+    units = [(0, 0, n - 1), (0, 0, 3)]
+    inp = oracle.Inputs(wl)
+    op = gu.oracle_params(inp, alpha)
+    omask, ell, mu = oracle.estimate(inp, op, units=units, want_scores=True)
+    ob, ibm, ib = gu.compare_masks(gmask, omask, ell, mu, alpha, units)
+    print("mask on %d units: outside-band mismatches %d, in-band %d of %d" % (len(units), ob, ibm, ib))
+    assert ob == 0
+    oout, olse = oracle.attend(inp, op, gmask, units=units)
+    worst = 0.0
+    for rs, hs in gu.unit_rows(wl, units):
+        worst = max(worst, float(np.abs(out[rs, hs] - oout[rs, hs]).max()))
+        assert np.abs(lse[rs, hs] - olse[rs, hs]).max() <= gu.LSE_TOL["fp8"]
+    print("same-mask max-abs err on sampled units %.3g" % worst)
+    assert worst <= gu.TOL["fp8"]
