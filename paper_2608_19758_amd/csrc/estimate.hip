@@ -46,7 +46,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
                                                             uint8_t* __restrict__ mask,
                                                             KeptLists kl) {
   extern __shared__ float ell[];            // [nbk] block log2-energies of this row
-  __shared__ uint4 qt[2][32 * kQRow];       // Q tiles (double buffer): 32 rows x 16 chunks of 8 bf16
+  __shared__ uint4 qt[2][64 * kQRow];       // Q tile pairs (double buffer): 2 x 32 rows x 16 chunks of 8 bf16
   __shared__ float redf[kWaves];
   __shared__ int redi[kWaves];
 
@@ -157,18 +157,14 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       }
     }
 
-    // Q tiles stream through two LDS buffers; the global loads of tile t+2
-    // are in flight while tile t is scored. Only the last tile can be
-    // partial: it runs as a separate instance of the tile body, so the row
-    // validity tests stay out of the full tiles.
+    // Q tiles stream through two LDS buffers of two tiles each, one barrier
+    // per pair; the global loads of the next pair are in flight while a pair
+    // is scored. Only the last tile can be partial: it runs as a separate
+    // instance of the tile body, so the row validity tests stay out of the
+    // full tiles.
     uint4 qa_next = qload(0), qa_next2 = qload(1);
-    auto tile = [&](int t, auto partial) {
+    auto tile = [&](const uint4* qb, int t, auto partial) {
       constexpr bool kPartial = decltype(partial)::value;
-      qstore(qt[t & 1], qa_next);
-      __syncthreads();   // tile t visible; every wave is done with tile t-1
-      qa_next = qa_next2;
-      qa_next2 = qload(t + 2);
-      const uint4* qb = qt[t & 1];
 
       bf16x8_t qa[8];
 #pragma unroll
@@ -241,8 +237,20 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       }
     };
     const int nfull = nrows >> 5;
-    for (int t = 0; t < nfull; ++t) tile(t, std::false_type{});
-    if (nfull < ntiles) tile(nfull, std::true_type{});
+    for (int t0 = 0; t0 < ntiles; t0 += 2) {
+      uint4* buf = qt[(t0 >> 1) & 1];
+      qstore(buf, qa_next);
+      qstore(buf + 32 * kQRow, qa_next2);
+      __syncthreads();   // tiles t0, t0+1 visible; every wave is done with the pair before
+      qa_next = qload(t0 + 2);
+      qa_next2 = qload(t0 + 3);
+      for (int k = 0; k < 2 && t0 + k < ntiles; ++k) {
+        if (t0 + k < nfull)
+          tile(buf + k * 32 * kQRow, t0 + k, std::false_type{});
+        else
+          tile(buf + k * 32 * kQRow, t0 + k, std::true_type{});
+      }
+    }
 
     // merge the two lane halves (same key block, different rows)
 #pragma unroll
