@@ -49,7 +49,7 @@ def parse():
                          "serving backend (prefix KV), its short tail chunks with and without KV "
                          "splits, and a continuous-batching forward of four requests")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=512,
+    ap.add_argument("--cpu-units", type=int, default=768,
                     help="(sequence, KV head, query block) units the oracle runs for the CPU baseline")
     ap.add_argument("--profile-only", action="store_true",
                     help="only run the timed loop of the default workload (for rocprofv3)")

@@ -182,9 +182,11 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
         return acc;
       };
       // Fold one chunk's scores into its running (m, E): rows of head
-      // offset j carry the scale cs[j] (> 0), so the maximum of cs * s is
-      // taken per j on the raw scores. Rows past the block (partial tile
-      // only) are set to -inf first: they add exp2(-inf) = 0.
+      // offset j carry the scale cs[j] (> 0). Rows past the block (partial
+      // tile only) are set to -inf first: they add exp2(-inf) = 0. Once m is
+      // set, the sum is taken against it as it stands (E only has to stay
+      // finite, so m need not be the exact running maximum); only a tile
+      // whose sum exceeds 2^64 moves m to its maximum and is summed again.
       auto fold = [&](int c, f32x16_t& acc) {
         if constexpr (kPartial) {
 #pragma unroll
@@ -193,25 +195,30 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
             for (int j = 0; j < 4; ++j)
               acc[4 * i + j] = rbase + 8 * i + j < nrows ? acc[4 * i + j] : -INFINITY;
         }
-        float g[4];
+        auto sum_at = [&](float nb) -> float {
+          float s4[4];                                  // four independent partial sums
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          g[j] = fmaxf(fmaxf(acc[j], acc[4 + j]), fmaxf(acc[8 + j], acc[12 + j])) * cs[j];
-        const float mx = fmaxf(fmaxf(g[0], g[1]), fmaxf(g[2], g[3]));
-        const float mn = fmaxf(m[c], mx);
-        if (mn > m[c]) {
-          E[c] *= fast_exp2(m[c] - mn);
-          m[c] = mn;
+          for (int j = 0; j < 4; ++j) s4[j] = fast_exp2(fmaf(acc[j], cs[j], nb));
+#pragma unroll
+          for (int i = 1; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) s4[j] += fast_exp2(fmaf(acc[4 * i + j], cs[j], nb));
+          return (s4[0] + s4[1]) + (s4[2] + s4[3]);
+        };
+        float e = m[c] == -INFINITY ? INFINITY : sum_at(-m[c]);
+        if (!(e <= 0x1p64f)) {   // no m yet, or the sum grew too large: move m up
+          float g[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            g[j] = fmaxf(fmaxf(acc[j], acc[4 + j]), fmaxf(acc[8 + j], acc[12 + j])) * cs[j];
+          const float mn = fmaxf(m[c], fmaxf(fmaxf(g[0], g[1]), fmaxf(g[2], g[3])));
+          if (mn > m[c]) {
+            E[c] *= fast_exp2(m[c] - mn);
+            m[c] = mn;
+          }
+          e = mn == -INFINITY ? 0.f : sum_at(-mn);   // no valid row yet: every term is 0
         }
-        const float nb = mn == -INFINITY ? 0.f : -mn;   // no valid row yet: every term is 0
-        float s4[4];                                    // four independent partial sums
-#pragma unroll
-        for (int j = 0; j < 4; ++j) s4[j] = fast_exp2(fmaf(acc[j], cs[j], nb));
-#pragma unroll
-        for (int i = 1; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) s4[j] += fast_exp2(fmaf(acc[4 * i + j], cs[j], nb));
-        E[c] += (s4[0] + s4[1]) + (s4[2] + s4[3]);
+        E[c] += e;
       };
       // chunks 0 .. NC-1 of every wave (NC uniform over the workgroup, so the
       // waves stay balanced between barriers and the scores of chunk c+1 are
