@@ -113,9 +113,8 @@ __device__ __forceinline__ void lds_barrier() {
 // assembly so that the compiler does not order every later LDS read behind
 // it; completion is tracked explicitly with wait_vmcnt before the barrier
 // that publishes a stage.
-__device__ __forceinline__ void dma16(const void* g, uint4* lds) {
-  const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)lds);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(base)
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds)
                : "memory", "m0");
 }
 #pragma clang diagnostic pop
@@ -137,10 +136,11 @@ struct CopyPlan {
 // Start the copies of one step: row row(j) of K / V lies at byte offset
 // off[j] from Kb / Vb.
 template <int W, int FP8>
-__device__ __forceinline__ void issue_copies(uint4* st, const uint8_t* Kb, const uint8_t* Vb,
+__device__ __forceinline__ void issue_copies(uint32_t st, const uint8_t* Kb, const uint8_t* Vb,
                                              const int64_t (&off)[CopyPlan<W, FP8>::PER], int tid) {
   using P = CopyPlan<W, FP8>;
   const int w = tid >> 6, lane = tid & 63;
+  const uint32_t wu = __builtin_amdgcn_readfirstlane(w);   // wave index, uniform
   const int pc = lane % P::CPR;
 #pragma unroll
   for (int j = 0; j < P::PER; ++j) {
@@ -148,8 +148,9 @@ __device__ __forceinline__ void issue_copies(uint4* st, const uint8_t* Kb, const
     const int r = P::RPG * g + lane / P::CPR;
     const int kc = FP8 ? (pc ^ ((r >> 1) & 7)) : (pc ^ (r & 15));
     const int vc = FP8 ? (pc ^ (2 * ((r >> 1) & 3))) : (pc ^ (4 * (r & 3)));
-    dma16(Kb + off[j] + 16 * kc, st + g * 64);
-    dma16(Vb + off[j] + 16 * vc, st + 64 * P::CPR + g * 64);
+    const uint32_t gl = st + (wu + W * j) * 64 * 16;
+    dma16(Kb + off[j] + 16 * kc, gl);
+    dma16(Vb + off[j] + 16 * vc, gl + 64 * P::CPR * 16);
   }
 }
 
@@ -185,12 +186,13 @@ __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb,
                                           Fetch fetch, Addr addr, Body body, int tid) {
   using P = CopyPlan<W, FP8>;
   Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
+  const uint32_t ring_lds = (uint32_t)(uintptr_t)(lds_void_t*)ring;   // LDS byte address
   int ni = 0;
 #pragma unroll 1
   for (; ni < P::NST - 1 && ni < n; ++ni) {
     ad.get(ni);
     ad.convert(ni);
-    issue_copies<W, FP8>(ring + ni * P::STAGE, Kb, Vb, ad.off, tid);
+    issue_copies<W, FP8>(ring_lds + ni * P::STAGE * 16, Kb, Vb, ad.off, tid);
   }
   if (ni < n) ad.get(ni);
 #pragma unroll 1
@@ -199,7 +201,7 @@ __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb,
     lds_barrier();   // step s visible to all; every wave is done with step s-1
     if (ni < n) {
       ad.convert(ni);
-      issue_copies<W, FP8>(ring + (ni++ % P::NST) * P::STAGE, Kb, Vb, ad.off, tid);
+      issue_copies<W, FP8>(ring_lds + (ni++ % P::NST) * P::STAGE * 16, Kb, Vb, ad.off, tid);
       if (ni < n) ad.get(ni);   // lands while the step is computed
     }
     body(ring + (s % P::NST) * P::STAGE, s);

@@ -140,8 +140,10 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     bf16x8_t kf[kChunksPerWave][8];
     float m[kChunksPerWave], E[kChunksPerWave];
     bool act[kChunksPerWave];
-    // 32-block chunks per wave in this group (the most any wave has)
-    const int ncw = min(kChunksPerWave, ((Ia - grp) / 32 + kWaves) / kWaves);
+    // 32-block chunks of this wave in this group that hold a visible block
+    // (chunk c of wave w starts at block grp + 32 (w + 8 c)); a wave without
+    // any only takes part in the barriers
+    const int ncw = min(kChunksPerWave, max(0, ((Ia - grp) / 32 - w + kWaves) / kWaves));
 #pragma unroll
     for (int c = 0; c < kChunksPerWave; ++c) {
       const int J0 = grp + 32 * (w + kWaves * c);
@@ -220,11 +222,10 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
         }
         E[c] += e;
       };
-      // chunks 0 .. NC-1 of every wave (NC uniform over the workgroup, so the
-      // waves stay balanced between barriers and the scores of chunk c+1 are
-      // issued to the matrix cores before chunk c is folded on the vector
-      // ALUs); a chunk past the unit's last block scores zero keys and is
-      // dropped at the end
+      // the wave's chunks 0 .. NC-1 that hold visible blocks (NC a compile-time
+      // count, so the scores of chunk c+1 are issued to the matrix cores
+      // before chunk c is folded on the vector ALUs); blocks past the unit's
+      // last one score zero keys and are dropped at the end
       auto run = [&](auto nc) {
         constexpr int NC = decltype(nc)::value;
         f32x16_t acc = score(0);
@@ -237,6 +238,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
         }
       };
       switch (ncw) {
+        case 0: break;
         case 1: run(std::integral_constant<int, 1>{}); break;
         case 2: run(std::integral_constant<int, 2>{}); break;
         case 3: run(std::integral_constant<int, 3>{}); break;
