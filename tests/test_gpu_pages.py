@@ -1,0 +1,99 @@
+"""GPU parity over page sizes of the paged KV pool (Sec. 3.3 Eq. page), through
+the C ABI.
+
+The copy addresses of a 64-key step come from records of rows that share a
+page: 64 rows per record for contiguous KV, p rows for a power-of-two page
+p < 64, one record per 64 rows for p >= 64 that is a power of two, and one
+per row otherwise. These cases cover the pages the other GPU tests leave out:
+sizes that are not powers of two (3, 48, 100), and pages larger than a step
+(128, 256), each with permuted page order and a batch with a prefix, an empty
+and a one-token sequence.
+
+Bars: block means bit-exact; mask bit-exact outside the 1e-4 margin band;
+outputs within max-abs 2e-2 (bf16) / 6e-2 (fp8) of the fp64 oracle under the
+GPU's own mask, LSE within 1e-2 / 0.0625. The same tokens in any page layout
+give the contiguous call's mask, outputs and LSE bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_19758_amd as fp2
+import synth
+from tests import brute, gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+
+
+def spec(lens, prefix, page, hq=8, hkv=2, dtype="bf16", seed=21, order="permuted"):
+    kvl = [L + p for L, p in zip(lens, prefix)]
+    pool = sum((L + page - 1) // page for L in kvl) + 7 if page else 0
+    return synth.Spec("pages", list(lens), hq, hkv, dtype=dtype, page_size=page,
+                      page_order=order if page else "identity", pool_pages=pool,
+                      salient_frac=0.1, salient_min=2, sink_blocks=1, window_blocks=2,
+                      recent_blocks=0, mean_correction=1, seed=seed, prefix=prefix)
+
+
+LENS, PREFIX = [900, 0, 1, 333], [0, 128, 700, 200]
+PAGES = [3, 48, 100, 128, 256]
+
+
+def _wl(page, dtype):
+    print("pages case: page %d dtype %s lens %s prefix %s" % (page, dtype, LENS, PREFIX), flush=True)
+    return synth.generate(spec(LENS, PREFIX, page, dtype=dtype))
+
+
+@pytest.mark.parametrize("page", PAGES)
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_pages_pool_bit_exact(page, dtype):
+    wl = _wl(page, dtype)
+    p = gu.params_for(wl, 0.5)
+    d = gu.device_tensors(wl)
+    khat, vbar = fp2.pool(p, d["k_cache"], d["v_cache"], d["cu_seqlens_k"], d["block_table"],
+                          cu_seqlens_host=wl.cu_seqlens_k, k_scale=d["k_scale"],
+                          v_scale=d["v_scale"])
+    torch.cuda.synchronize()
+    inp = oracle.Inputs(wl)
+    _, vb, khat_o = oracle.pool(inp, inp.params(0.5))
+    np.testing.assert_array_equal(khat.view(torch.int16).cpu().numpy().view(np.uint16), khat_o)
+    want_v = np.zeros(vb.shape, np.uint16)
+    nz = vb != 0
+    want_v[nz] = brute.bf16_round_bits(vb[nz])
+    np.testing.assert_array_equal(vbar.view(torch.int16).cpu().numpy().view(np.uint16), want_v)
+
+
+@pytest.mark.parametrize("page", PAGES)
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_pages_prefill_parity(page, dtype):
+    wl = _wl(page, dtype)
+    alpha = 0.98
+    out, gmask, lse = gu.gpu_prefill(wl, gu.params_for(wl, alpha))
+    inp = oracle.Inputs(wl)
+    op = gu.oracle_params(inp, alpha)
+    omask, ell, mu = oracle.estimate(inp, op, want_scores=True)
+    ob, ibm, ib = gu.compare_masks(gmask, omask, ell, mu, alpha, gu.units_of(wl))
+    print("mask: outside-band mismatches %d, in-band mismatches %d of %d in-band" % (ob, ibm, ib))
+    assert ob == 0
+    oout, olse = oracle.attend(inp, op, gmask)
+    err = np.abs(out - oout).max()
+    lerr = np.abs(lse - olse).max()
+    print("same-mask max-abs err %.3g (tol %g), lse err %.3g" % (err, gu.TOL[dtype], lerr))
+    assert err <= gu.TOL[dtype]
+    assert lerr <= gu.LSE_TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_page_layouts_equal_contiguous(dtype):
+    """One set of tokens stored contiguously and in pools of several page
+    sizes (permuted pages): the same mask, outputs and LSE, bit for bit."""
+    base = synth.generate(spec(LENS, PREFIX, 0, dtype=dtype))
+    want = gu.gpu_prefill(base, gu.params_for(base, 0.98))
+    for page in [1, 3, 48, 64, 100, 256]:
+        wl = synth.generate(spec(LENS, PREFIX, page, dtype=dtype))
+        np.testing.assert_array_equal(wl.q, base.q)
+        np.testing.assert_array_equal(wl.k_tok, base.k_tok)
+        got = gu.gpu_prefill(wl, gu.params_for(wl, 0.98))
+        print("page %d: layouts agree" % page, flush=True)
+        for a, b in zip(want, got):
+            np.testing.assert_array_equal(a, b)
