@@ -54,15 +54,6 @@ __device__ __forceinline__ uint16_t f64_to_bf16(double x) {
   return (uint16_t)(sign | ((uint32_t)e << 7) | (uint32_t)(keep & 0x7F));
 }
 
-// OCP e4m3fn code -> value * 512 as an exact integer (|.| <= 229376). Codes
-// with exponent field 0 are subnormal (m * 2^-9); 0x7F/0xFF are NaN and never
-// reach the arithmetic (the caller's inputs are finite).
-__device__ __forceinline__ int e4m3_times512(uint32_t code) {
-  int e = (code >> 3) & 15, m = code & 7;
-  int mag = e == 0 ? m : (8 + m) << (e - 1);
-  return (code & 0x80) ? -mag : mag;
-}
-
 typedef __attribute__((ext_vector_type(2))) float f32x2_t;
 
 // Four OCP e4m3fn codes (the bytes of w, lowest first) -> two packed bf16

@@ -8,9 +8,11 @@
 //    rg, rg+16, ... of the block for columns 8c..8c+7 in fp64. Every bf16
 //    value is exact in fp64 and so are the partial sums of realistic data, so
 //    the mean does not depend on the summation order.
-//  - fp8: each e4m3 code is an exact integer multiple of 2^-9; the sums are
-//    exact 32-bit integers, and the mean is (sum * 2^-9 * scale) / count in
-//    fp64 (the product is exact, the division rounds once).
+//  - fp8: each e4m3 value is an exact multiple of 2^-9 (the hardware decode
+//    v_cvt_pk_f32_fp8 is exact); per-thread sums of 4 rows are exact in fp32,
+//    the block sums exact 32-bit integers in units of 2^-9, and the mean is
+//    (sum * 2^-9 * scale) / count in fp64 (the product is exact, the
+//    division rounds once).
 // The rounded key mean khat (bf16, one rounding from fp64) is the scoring key
 // of Eq. fused_score and the surrogate key of the correction; vbar is the
 // value mean in bf16.
@@ -92,9 +94,6 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
   } else {
     // 8 threads per token row (16 codes each), 32 row groups.
     const int c = tid & 7, rg = tid >> 3;
-    int ak[16], av[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) ak[i] = av[i] = 0;
     const uint8_t* K = (const uint8_t*)p.k;
     const uint8_t* V = (const uint8_t*)p.v;
     uint4 kv[4], vv[4];
@@ -108,15 +107,38 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
         vv[i] = *(const uint4*)(V + off);
       }
     }
+    // Codes decoded by the hardware (v_cvt_pk_f32_fp8, exact) and summed in
+    // fp32 over the thread's 4 rows: every e4m3 value is a multiple of 2^-9
+    // below 448 in magnitude, so a sum of 4 needs at most 20 significant
+    // bits and is exact; times 512 it is an exact integer.
+    float fk[16], fv[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) fk[i] = fv[i] = 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const uint32_t kw[4] = {kv[r].x, kv[r].y, kv[r].z, kv[r].w};
       const uint32_t vw[4] = {vv[r].x, vv[r].y, vv[r].z, vv[r].w};
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        ak[i] += e4m3_times512((kw[i >> 2] >> (8 * (i & 3))) & 0xFF);
-        av[i] += e4m3_times512((vw[i >> 2] >> (8 * (i & 3))) & 0xFF);
+      for (int q = 0; q < 4; ++q) {
+        const f32x2_t k0 = __builtin_amdgcn_cvt_pk_f32_fp8((int)kw[q], false);
+        const f32x2_t k1 = __builtin_amdgcn_cvt_pk_f32_fp8((int)kw[q], true);
+        const f32x2_t v0 = __builtin_amdgcn_cvt_pk_f32_fp8((int)vw[q], false);
+        const f32x2_t v1 = __builtin_amdgcn_cvt_pk_f32_fp8((int)vw[q], true);
+        fk[4 * q] += k0.x;
+        fk[4 * q + 1] += k0.y;
+        fk[4 * q + 2] += k1.x;
+        fk[4 * q + 3] += k1.y;
+        fv[4 * q] += v0.x;
+        fv[4 * q + 1] += v0.y;
+        fv[4 * q + 2] += v1.x;
+        fv[4 * q + 3] += v1.y;
       }
+    }
+    int ak[16], av[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      ak[i] = (int)(fk[i] * 512.f);
+      av[i] = (int)(fv[i] * 512.f);
     }
     // integer partial sums are exact in fp64
     int* redki = (int*)&redk[0][0];
