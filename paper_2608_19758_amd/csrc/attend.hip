@@ -221,7 +221,7 @@ __device__ __forceinline__ float xhalf_max(float v) {
 template <int RT>
 struct RowState {
   f32x16_t o[RT][4];   // O^T accumulators: o[rt][dt][4i+j] = O[row][32dt + 8i + 4*half + j]
-  f32x16_t ls[RT];     // fp8 kept keys: row sums of P~ from the matrix cores (element 0);
+  f32x4_t ls[RT];      // fp8 kept keys: row sums of P~ from the matrix cores (element 0);
                        // folded into l once the kept blocks are done
   float m[RT];         // running maximum (log2 units)
   float l[RT];         // row-sum part summed on the vector ALUs (this lane's keys)
@@ -460,13 +460,17 @@ __device__ __forceinline__ int pack_e4m3x4(float a, float b, float c, float d) {
 // Finish an fp8 step of 64 kept keys key0 .. key0+63 from its scores: per
 // row tile the softmax (diag: causal mask against pos) and
 // O^T += V^T P~^T with P~ = e4m3(2^8 exp(x - m)); the softmax of one tile
-// runs on the vector ALUs while the matrix cores work on the other tile. The row sums of P~ come from the matrix cores as well:
-// an all-ones A operand (e4m3 1.0 = 0x38) times P~^T puts sum_k P~[row][k]
-// in every element of the lane's column.
+// runs on the vector ALUs while the matrix cores work on the other tile.
+// The row sums of P~ come from the matrix cores as well, through one
+// v_mfma_f32_16x16x128_f8f6f4 per step: read as its B operand (128 x 16),
+// the P~ registers hold in column n the 64 keys of query n (k-groups 0 and 2)
+// and of query n+16 (k-groups 1 and 3), so a 0/1 selector A operand whose
+// row m picks the k-groups of parity (m/4)%2 leaves in every element of lane
+// l the row sum of the lane's own query l%32.
 template <int RT>
 __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState<RT>& rs, float cs,
                                         int key0, const int (&pos)[RT], bool diag, int lane,
-                                        const i32x8_t& ones) {
+                                        const i32x8_t& sel) {
   const int half = lane >> 5;
   auto& s = S.v;
   i32x8_t va[4];
@@ -499,7 +503,7 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
     for (int dt = 0; dt < 4; ++dt)
       rs.o[rt][dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(va[dt], pb, rs.o[rt][dt], 0, 0, 0,
                                                                      0, 0, 0);
-    rs.ls[rt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones, pb, rs.ls[rt], 0, 0, 0, 0, 0, 0);
+    rs.ls[rt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(sel, pb, rs.ls[rt], 0, 0, 0, 0, 0, 0);
   }
 }
 
@@ -606,7 +610,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
     for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) rs.o[rt][dt] = f32x16_t{};
-      rs.ls[rt] = f32x16_t{};
+      rs.ls[rt] = f32x4_t{};
       rs.m[rt] = -INFINITY;
       rs.l[rt] = 0.f;
     }
@@ -711,19 +715,22 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
         };
         const int nst = 2 * nbc;
         if constexpr (FP8) {
-          // all-ones A operand of the row-sum MFMA (e4m3 1.0 = 0x38), opaque so
-          // that it stays in registers instead of being rebuilt every step
-          i32x8_t ones;
+          // selector A operand of the row-sum MFMA: lane l holds row l%16,
+          // k-group l/16 of A, all e4m3 1.0 (0x38) where the row's parity
+          // (l%16)/4 matches the k-group's, else 0; opaque so that it stays in
+          // registers instead of being rebuilt every step
+          const int selw = (((lane & 15) >> 2) & 1) == ((lane >> 4) & 1) ? 0x38383838 : 0;
+          i32x8_t sel;
 #pragma unroll
-          for (int k = 0; k < 8; ++k) ones[k] = 0x38383838;
-          asm volatile("" : "+v"(ones));
+          for (int k = 0; k < 8; ++k) sel[k] = selw;
+          asm volatile("" : "+v"(sel));
           run_steps<W, 1, RT>(
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
                 const int wp = c0 + (s >> 1);   // walk position of the step's block
                 fin_fp8<RT>(st, S, rs, cs, (wp == 0 ? e0 : e1) * kBlock + kStep * (s & 1), pos,
-                            wp < nmask, lane, ones);
+                            wp < nmask, lane, sel);
               },
               tid);
         } else {
