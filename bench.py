@@ -12,8 +12,9 @@ kept-block ratio, a roofline entry for the attention kernel (the dominant
 kernel), and the oracle timed on the host cores on a bounded sample;
 --variants adds the other 128K variants (kept ratio, correction off, bf16,
 GQA 8:1). The roofline's HBM traffic comes from the committed rocprofv3
-counter summary of the attention kernel, and only while the kernel sources
-are the ones the counters were taken on (else null).
+counter summary of the attention kernel, and the estimation stage's traffic
+(pool + estimate kernels) from its own summary, each only while the kernel
+sources are the ones the counters were taken on (else null).
 """
 from __future__ import annotations
 
@@ -66,6 +67,38 @@ def kernel_sources_sha256():
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
+
+
+ESTIMATION_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "estimation_llama128k_fp8_pmc.txt")
+ESTIMATION_SOURCES = ["paper_2608_19758_amd/csrc/pool.hip", "paper_2608_19758_amd/csrc/estimate.hip",
+                      "paper_2608_19758_amd/csrc/kernels.h", "paper_2608_19758_amd/csrc/common.h"]
+
+
+def estimation_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in ESTIMATION_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def committed_estimation_traffic():
+    """HBM bytes per estimation call (pool + estimate kernels) from the
+    committed counter summary, scaled like the attention's; None if missing or
+    taken on other kernel sources."""
+    try:
+        with open(ESTIMATION_TRAFFIC_FILE) as f:
+            kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith("#"))
+    except OSError:
+        return None
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("source_sha256") != estimation_sources_sha256():
+        return None
+    try:
+        return float(kv["stage_traffic_bytes"])
+    except (KeyError, ValueError):
+        return None
 
 
 def committed_traffic():
@@ -377,7 +410,9 @@ def main():
             torch.cuda.empty_cache()
 
     att = m["attention"]
-    traffic = committed_traffic() if (args.workload, args.target) == ("llama128k_fp8", "0.05") else None
+    headline = (args.workload, args.target) == ("llama128k_fp8", "0.05")
+    traffic = committed_traffic() if headline else None
+    etraffic = committed_estimation_traffic() if headline else None
     line = {
         "metric": METRIC,
         "value": round(m["dense_tflops"], 3),
@@ -414,7 +449,13 @@ def main():
                        "hbm_gbs": round(m["estimation"]["gbs"], 1),
                        "hbm_frac": round(m["estimation"]["hbm_frac"], 4),
                        "scoring_mfma_frac": round(m["estimation"]["mfma_frac"], 4),
-                       "exps_per_s": float("%.4g" % m["estimation"]["exps_per_s"])},
+                       "exps_per_s": float("%.4g" % m["estimation"]["exps_per_s"]),
+                       # counter-measured bytes of the pool + estimate kernels per call
+                       # (committed rocprofv3 summary) and the rate they imply
+                       "traffic": None if etraffic is None else round(etraffic / 1e9, 4),
+                       "traffic_unit": "GB per call",
+                       "measured_gbs": None if etraffic is None
+                       else round(etraffic / 1e9 / (m["estimate_ms"] / 1e3), 1)},
         "cpu_baseline": None if cpu is None else {k: (round(v, 6) if isinstance(v, float) else v)
                                                   for k, v in cpu.items() if k != "seconds"},
     }
