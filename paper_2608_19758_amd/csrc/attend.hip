@@ -60,7 +60,11 @@ namespace {
 
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kStep = 64;            // keys per pipeline step
-constexpr int kRingU4 = 8192;        // LDS ring: 128 KiB in 16-byte slots
+// LDS ring in 16-byte slots: 128 KiB for one workgroup per CU; the fp8
+// kernel with 4 waves (one per SIMD) takes 64 KiB so that two workgroups
+// share a CU and every SIMD runs two waves.
+constexpr int ring_u4(int W, int FP8) { return W == 4 && FP8 ? 4096 : 8192; }
+constexpr int wgs_per_cu(int W, int FP8) { return W == 4 && FP8 ? 2 : 1; }
 constexpr int kRec = 768;            // copy-address records per chunk of kept blocks (12 KiB)
 constexpr int kPlist = 8 * kRec;     // pruned blocks per correction chunk (u16, same 12 KiB)
 #ifndef ATT_W
@@ -122,23 +126,23 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
 // Copy plan of one 64-row step (K and V): copy instruction j of wave w moves
 // rows RPG*(w + W*j) .. +RPG-1, lane i taking 16-byte slot i % CPR of row
 // RPG*(w + W*j) + i / CPR.
-template <int W, int FP8>
+template <int W, int FP8, int RING>
 struct CopyPlan {
   static constexpr int CPR = FP8 ? 8 : 16;          // 16-byte chunks per row
   static constexpr int RPG = 64 / CPR;              // rows per copy instruction
   static constexpr int PER = kStep / RPG / W;       // copies per wave and tensor
   static constexpr int D = 2 * PER;                 // copies per thread and step
   static constexpr int STAGE = 2 * kStep * CPR;     // 16-byte slots per stage
-  static constexpr int NST = kRingU4 / STAGE;       // ring depth
+  static constexpr int NST = RING / STAGE;          // ring depth
   __device__ static int row(int j, int tid) { return RPG * ((tid >> 6) + W * j) + (tid & 63) / CPR; }
 };
 
 // Start the copies of one step: row row(j) of K / V lies at byte offset
 // off[j] from Kb / Vb.
-template <int W, int FP8>
+template <int W, int FP8, int RING>
 __device__ __forceinline__ void issue_copies(uint32_t st, const uint8_t* Kb, const uint8_t* Vb,
-                                             const int64_t (&off)[CopyPlan<W, FP8>::PER], int tid) {
-  using P = CopyPlan<W, FP8>;
+                                             const int64_t (&off)[CopyPlan<W, FP8, RING>::PER], int tid) {
+  using P = CopyPlan<W, FP8, RING>;
   const int w = tid >> 6, lane = tid & 63;
   const uint32_t wu = __builtin_amdgcn_readfirstlane(w);   // wave index, uniform
   const int pc = lane % P::CPR;
@@ -159,9 +163,9 @@ __device__ __forceinline__ void issue_copies(uint32_t st, const uint8_t* Kb, con
 // offset. The entries of the next step are fetched before a step is computed
 // and converted after the next barrier, so their LDS latency is never waited
 // on.
-template <int W, int FP8, class Fetch, class Addr>
+template <int W, int FP8, int RING, class Fetch, class Addr>
 struct Addresser {
-  using P = CopyPlan<W, FP8>;
+  using P = CopyPlan<W, FP8, RING>;
   using Raw = decltype(std::declval<Fetch>()(0, 0));
   Fetch fetch;
   Addr addr;
@@ -181,18 +185,18 @@ struct Addresser {
 // Ring over steps 0 .. n-1 without cross-step overlap of the compute;
 // body(stage, s) consumes step s. Ends with a barrier (the ring may be
 // refilled).
-template <int W, int FP8, class Fetch, class Addr, class Body>
+template <int W, int FP8, int RING, class Fetch, class Addr, class Body>
 __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
                                           Fetch fetch, Addr addr, Body body, int tid) {
-  using P = CopyPlan<W, FP8>;
-  Addresser<W, FP8, Fetch, Addr> ad{fetch, addr, tid};
+  using P = CopyPlan<W, FP8, RING>;
+  Addresser<W, FP8, RING, Fetch, Addr> ad{fetch, addr, tid};
   const uint32_t ring_lds = (uint32_t)(uintptr_t)(lds_void_t*)ring;   // LDS byte address
   int ni = 0;
 #pragma unroll 1
   for (; ni < P::NST - 1 && ni < n; ++ni) {
     ad.get(ni);
     ad.convert(ni);
-    issue_copies<W, FP8>(ring_lds + ni * P::STAGE * 16, Kb, Vb, ad.off, tid);
+    issue_copies<W, FP8, RING>(ring_lds + ni * P::STAGE * 16, Kb, Vb, ad.off, tid);
   }
   if (ni < n) ad.get(ni);
 #pragma unroll 1
@@ -201,7 +205,7 @@ __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb,
     lds_barrier();   // step s visible to all; every wave is done with step s-1
     if (ni < n) {
       ad.convert(ni);
-      issue_copies<W, FP8>(ring_lds + (ni++ % P::NST) * P::STAGE * 16, Kb, Vb, ad.off, tid);
+      issue_copies<W, FP8, RING>(ring_lds + (ni++ % P::NST) * P::STAGE * 16, Kb, Vb, ad.off, tid);
       if (ni < n) ad.get(ni);   // lands while the step is computed
     }
     body(ring + (s % P::NST) * P::STAGE, s);
@@ -509,10 +513,10 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
 
 // Steps 0 .. n-1 of a ring: the scores of a step (qk) then the rest of it
 // (fin). The two waves of a SIMD overlap each other's matrix and vector work.
-template <int W, int FP8, int RT, class Fetch, class Addr, class QK, class Fin>
+template <int W, int FP8, int RT, int RING, class Fetch, class Addr, class QK, class Fin>
 __device__ __forceinline__ void run_steps(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
                                           Fetch fetch, Addr addr, QK qk, Fin fin, int tid) {
-  ring_loop<W, FP8>(ring, n, Kb, Vb, fetch, addr, [&](const uint4* st, int s) {
+  ring_loop<W, FP8, RING>(ring, n, Kb, Vb, fetch, addr, [&](const uint4* st, int s) {
     Scores<RT> S;
     qk(st, S);
     fin(st, S, s);
@@ -520,12 +524,13 @@ __device__ __forceinline__ void run_steps(uint4* ring, int n, const uint8_t* Kb,
 }
 
 template <int FP8, int W, int RT>
-__global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled pooled,
+__global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Problem p0, Pooled pooled,
                                                            const uint8_t* __restrict__ mask,
                                                            KeptLists kl, Plan plan,
                                                            uint16_t* __restrict__ out,
                                                            float* __restrict__ lse) {
-  __shared__ uint4 ring[kRingU4];
+  constexpr int RING = ring_u4(W, FP8);
+  __shared__ uint4 ring[RING];
   __shared__ uint4 aux[kRec];               // kept: copy-address records; correction: pruned list
   __shared__ int32_t wtot[W];
   __shared__ int4 s_item;
@@ -724,7 +729,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
 #pragma unroll
           for (int k = 0; k < 8; ++k) sel[k] = selw;
           asm volatile("" : "+v"(sel));
-          run_steps<W, 1, RT>(
+          run_steps<W, 1, RT, RING>(
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
@@ -734,7 +739,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
               },
               tid);
         } else {
-          run_steps<W, 0, RT>(
+          run_steps<W, 0, RT, RING>(
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
@@ -819,7 +824,7 @@ __global__ __launch_bounds__(64 * W, 1) void attend_kernel(Problem p0, Pooled po
           (void)r;
           return (int64_t)J * kHeadDim * 2;
         };
-        run_steps<W, 0, RT>(
+        run_steps<W, 0, RT, RING>(
             ring, (np + kStep - 1) / kStep, Kh, Vh, fetch, addr,
             [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
             [&](const uint4* st, Scores<RT>& S, int s) {
@@ -880,7 +885,7 @@ hipError_t launch_cfg(const Problem& p, const Pooled& pooled, const uint8_t* mas
                       hipStream_t s) {
   const int cus = device_compute_units();
   if (cus <= 0) return hipErrorInvalidDevice;
-  const unsigned grid = (unsigned)std::min<int64_t>(plan.cap_items, cus);
+  const unsigned grid = (unsigned)std::min<int64_t>(plan.cap_items, (int64_t)cus * wgs_per_cu(W, FP8));
   attend_kernel<FP8, W, RT><<<grid, 64 * W, 0, s>>>(p, pooled, mask, kl, plan,
                                                           (uint16_t*)out, lse);
   return hipSuccess;
