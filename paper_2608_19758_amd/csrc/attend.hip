@@ -3,16 +3,19 @@
 //
 // Work unit: (sequence b, KV head h, query block I) of the packed query rows
 // of Eq. packgqa. A work item is a slice of 32*W of the g*B packed rows of a
-// unit, taken by a workgroup of W waves (W = 8, or 4 when g = 1), so one K/V
-// tile in LDS serves all g query heads of the group. The grid is persistent:
-// one workgroup per compute unit (the LDS ring admits one), each taking items
-// from an atomic counter in order of decreasing query block (heaviest
-// first), so the run time of an item never holds up the dispatch of others.
+// unit, taken by a workgroup of W waves (W = 8, or 4 for units of 128 packed
+// rows: g = 1, or 128-row query tiles), so one K/V tile in LDS serves all g
+// query heads of the group. The grid is persistent: one 8-wave workgroup per
+// compute unit (its LDS ring admits one), or two 4-wave workgroups on half
+// the ring each, so that every SIMD runs two waves; each takes items from an
+// atomic counter in order of decreasing query block (heaviest first), so the
+// run time of an item never holds up the dispatch of others.
 //
 // The key sequence of a unit is a list of 64-key steps: both halves of every
 // kept block, walked from the last kept index down (Eq. csr), then the pooled
 // means of the pruned blocks J < I, 64 per step (the correction). Steps run
-// through a ring of LDS stages (128 KiB: 4 bf16 stages or 8 fp8 stages): the
+// through a ring of LDS stages (128 KiB: 4 bf16 stages or 8 fp8 stages;
+// half that for 4-wave workgroups): the
 // rows of step s+NST-1 are copied straight from the page-addressed pool
 // (Eq. page) into LDS with global_load_lds_dwordx4 while step s is computed,
 // with one workgroup barrier per step. The copy addresses come from small LDS
@@ -60,11 +63,11 @@ namespace {
 
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr int kStep = 64;            // keys per pipeline step
-// LDS ring in 16-byte slots: 128 KiB for one workgroup per CU; the fp8
-// kernel with 4 waves (one per SIMD) takes 64 KiB so that two workgroups
-// share a CU and every SIMD runs two waves.
-constexpr int ring_u4(int W, int FP8) { return W == 4 && FP8 ? 4096 : 8192; }
-constexpr int wgs_per_cu(int W, int FP8) { return W == 4 && FP8 ? 2 : 1; }
+// LDS ring in 16-byte slots: 128 KiB for one 8-wave workgroup per CU; a
+// 4-wave workgroup (128-row items) takes 64 KiB so that two of them share a
+// CU and every SIMD still runs two waves (4 fp8 / 2 bf16 stages).
+constexpr int ring_u4(int W, int FP8) { return W == 4 ? 4096 : 8192; }
+constexpr int wgs_per_cu(int W, int FP8) { return W == 4 ? 2 : 1; }
 constexpr int kRec = 768;            // copy-address records per chunk of kept blocks (12 KiB)
 constexpr int kPlist = 8 * kRec;     // pruned blocks per correction chunk (u16, same 12 KiB)
 #ifndef ATT_W
@@ -536,7 +539,8 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
   __shared__ int4 s_item;
 
   constexpr int M = 32 * RT * W;            // packed rows per work item
-  constexpr int NPRE = W > 4 ? 2 : 4;       // V^T key groups read ahead of the softmax
+  // V^T key groups read ahead of the softmax (all four only with a wave per SIMD)
+  constexpr int NPRE = W > 4 || wgs_per_cu(W, FP8) > 1 ? 2 : 4;
   const int wpu = p0.g * p0.qtile / M;      // row slices per unit
   const int nbh = p0.batch * p0.hkv;
   const int tid0 = threadIdx.x;
