@@ -36,6 +36,7 @@ constexpr int kPlanWaves = kPlanThreads / 64;
 constexpr int kMinSplitSteps = 16;   // smallest step budget of an item
 constexpr int kItemSteps = 2;        // fixed per-item cost (query load, set-up), in steps
 constexpr int kMaxRowSplits = 32;    // one part per lane of the combine's half-wave
+constexpr int kCostCache = 16384;    // units whose costs the plan keeps in LDS (64 KiB)
 
 __device__ double block_sum(double v, double* sh) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -81,18 +82,36 @@ __device__ int block_excl_scan(int v, int* sh, int& total) {
   return pre + inc - v;
 }
 
-// Attention-order index q -> unit row (b * Hkv + h) * nbmax + I.
-__device__ __forceinline__ int row_of(const Problem& p, int q, int nbh, int& I, int& b) {
-  I = p.nbmax - 1 - q / nbh;
-  const int bh = q % nbh;
-  b = bh / p.hkv;
-  return bh * p.nbmax + I;
-}
+// Walk over attention-order indices q = (nbmax - 1 - I) * nbh + bh from a
+// start index: unit row (b * Hkv + h) * nbmax + I, sequence b and query
+// block I, with one division at the start and none per step.
+struct UnitWalk {
+  int I, bh, b, h, nbh, hkv, nbmax;
+  __device__ UnitWalk(const Problem& p, int q0) : nbh(p.batch * p.hkv), hkv(p.hkv), nbmax(p.nbmax) {
+    I = nbmax - 1 - q0 / nbh;
+    bh = q0 % nbh;
+    b = bh / hkv;
+    h = bh - b * hkv;
+  }
+  __device__ int row() const { return bh * nbmax + I; }
+  __device__ void next() {
+    ++bh;
+    if (++h == hkv) {
+      h = 0;
+      ++b;
+    }
+    if (bh == nbh) {
+      bh = b = h = 0;
+      --I;
+    }
+  }
+};
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, KeptLists kl, Plan plan,
                                                             int wpu) {
   __shared__ double shd[kPlanWaves];
   __shared__ int shi[kPlanWaves];
+  __shared__ int sc[kCostCache];
   const int tid = threadIdx.x;
   const int nbh = p.batch * p.hkv;
   const int R = nbh * p.nbmax;
@@ -102,25 +121,49 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, KeptLists
   const int q0 = min(R, tid * per), q1 = min(R, q0 + per);
 
   // cost in steps of one row slice of every unit with queries (-1: none),
-  // kept in rowinfo.x until the plan overwrites it
+  // kept in LDS when the table is small enough (indexed by q), else in
+  // rowinfo.x until the plan overwrites it
+  const bool in_lds = R <= kCostCache;
+  auto cost_at = [&](int q, int row) -> int { return in_lds ? sc[q] : plan.rowinfo[row].x; };
   double tot = 0.0;
   int mx = 0;
-  for (int q = q0; q < q1; ++q) {
-    int I, b;
-    const int row = row_of(p, q, nbh, I, b);
-    const int Lq = p.cu[b + 1] - p.cu[b];
-    int cost = -1;
-    if (I * p.qtile < Lq) {
-      const int Ia = (p.cuk[b + 1] - p.cuk[b] - Lq + min(Lq, (I + 1) * p.qtile) - 1) / kBlock;
-      const int cnt = kl.cnt[row];
-      const int pruned = p.corr ? max(0, Ia + 1 - cnt) : 0;   // at most, below the last block
-      cost = 2 * cnt + (pruned + 63) / 64 + kItemSteps;
-      tot += (double)cost * wpu;
-      mx = max(mx, cost);
+  // eight units at a time: their loads are issued together
+  UnitWalk u(p, q0);
+  for (int qb = q0; qb < q1; qb += 8) {
+    int row[8], I[8], b[8], cnt[8], lq[8], lk[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      row[j] = u.row();
+      I[j] = u.I;
+      b[j] = u.b;
+      u.next();
     }
-    plan.rowinfo[row] = make_int2(cost, -1);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool v = qb + j < q1;
+      cnt[j] = v ? kl.cnt[row[j]] : 0;
+      lq[j] = v ? p.cu[b[j] + 1] - p.cu[b[j]] : 0;
+      lk[j] = v ? p.cuk[b[j] + 1] - p.cuk[b[j]] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (qb + j >= q1) break;
+      const int Lq = lq[j];
+      int cost = -1;
+      if (I[j] * p.qtile < Lq) {
+        const int Ia = (lk[j] - Lq + min(Lq, (I[j] + 1) * p.qtile) - 1) / kBlock;
+        const int pruned = p.corr ? max(0, Ia + 1 - cnt[j]) : 0;   // at most, below the last block
+        cost = 2 * cnt[j] + (pruned + 63) / 64 + kItemSteps;
+        tot += (double)cost * wpu;
+        mx = max(mx, cost);
+      }
+      if (in_lds)
+        sc[qb + j] = cost;
+      else
+        plan.rowinfo[row[j]] = make_int2(cost, -1);
+    }
   }
-  tot = block_sum(tot, shd);
+  tot = block_sum(tot, shd);   // (its barriers also publish sc)
   mx = block_max(mx, shi);
 
   // step budget of the cost-balanced mode
@@ -129,9 +172,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, KeptLists
     S = max(kMinSplitSteps, (int)ceil(tot / (double)max(1, plan.target_items)));
     while (S < mx) {   // grow S until the parts fit the partial-output slots
       int need = 0;
-      for (int q = q0; q < q1; ++q) {
-        int I, b;
-        const int cost = plan.rowinfo[row_of(p, q, nbh, I, b)].x;
+      UnitWalk w(p, q0);
+      for (int q = q0; q < q1; ++q, w.next()) {
+        const int cost = cost_at(q, w.row());
         if (cost > S) need += min(kMaxRowSplits, (cost + S - 1) / S);
       }
       need = (int)block_sum((double)need, shd);
@@ -148,22 +191,27 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, KeptLists
   // items in attention order, partial slots and split units: this thread's
   // totals, their exclusive scans over the threads, then the entries
   int ni = 0, ns = 0, nsr = 0;
-  for (int q = q0; q < q1; ++q) {
-    int I, b;
-    const int U = parts(plan.rowinfo[row_of(p, q, nbh, I, b)].x);
-    ni += U * wpu;
-    ns += U > 1 ? U : 0;
-    nsr += U > 1 ? 1 : 0;
+  {
+    UnitWalk w(p, q0);
+    for (int q = q0; q < q1; ++q, w.next()) {
+      const int U = parts(cost_at(q, w.row()));
+      ni += U * wpu;
+      ns += U > 1 ? U : 0;
+      nsr += U > 1 ? 1 : 0;
+    }
   }
   int ti, ts, tsr;
   int bi = block_excl_scan(ni, shi, ti);
   int bs = block_excl_scan(ns, shi, ts);
   int bsr = block_excl_scan(nsr, shi, tsr);
-  for (int q = q0; q < q1; ++q) {
-    int I, b;
-    const int row = row_of(p, q, nbh, I, b);
-    const int U = parts(plan.rowinfo[row].x);
-    if (U == 0) continue;
+  UnitWalk w(p, q0);
+  for (int q = q0; q < q1; ++q, w.next()) {
+    const int row = w.row();
+    const int U = parts(cost_at(q, row));
+    if (U == 0) {
+      if (in_lds) plan.rowinfo[row] = make_int2(-1, -1);
+      continue;
+    }
     plan.rowinfo[row] = make_int2(U, U > 1 ? bs : -1);
     if (U > 1) {
       plan.splitrows[bsr++] = row;
