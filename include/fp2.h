@@ -244,6 +244,48 @@ fp2_status_t fp2_pool(const fp2_params_t* params, const int32_t* cu_seqlens,
                       const int32_t* block_table, const float* k_scale, const float* v_scale,
                       void* khat, void* vbar, void* stream);
 
+/* Block means kept across calls (chunked prefill, prefix caching; Sec. 4
+ * runs the sparse operator on every extend of a request): the pooled means of
+ * a complete key block depend only on its tokens, so a serving engine can keep
+ * them beside its paged KV cache and each call pools only the blocks that are
+ * new or were incomplete before. One slot per key block of the pool:
+ *   page_size p > 0: slot = page_id * ceil(p / 128) + offset / 128, where
+ *     page_id = block_table[b][t / p] and offset = t % p for the block's first
+ *     token t = 128 J, so a pool of P pages needs P * ceil(p / 128) slots;
+ *   page_size == 0: slot = b * ceil(max_kv_len / 128) + J.
+ * khat and vbar are bf16 [slots, num_kv_heads, head_dim], device, owned by the
+ * caller, one pair per layer (the means are those of that layer's K/V).
+ * pooled_blocks is device int32 [batch]: the leading key blocks of sequence b
+ * whose slots already hold the means of the same tokens (written by an
+ * earlier call); it is clamped to the sequence's complete blocks, so a block
+ * that was partial then is pooled again. Blocks below it are copied from the
+ * cache; every block pooled by the call is written to its slot. The arrays
+ * must cover the slot of every page id that block_table holds (as k_cache and
+ * v_cache cover its tokens); the library does not check them. */
+typedef struct {
+  void* khat;
+  void* vbar;
+  const int32_t* pooled_blocks;
+} fp2_means_cache_t;
+
+/* Slots a means cache needs for `params` and a pool of num_pages pages
+ * (num_pages is ignored for contiguous KV); 0 for an invalid params or a
+ * negative num_pages. */
+size_t fp2_means_cache_slots(const fp2_params_t* params, int64_t num_pages);
+
+/* fp2_prefill with a means cache (cache non-null, all three pointers
+ * non-null, khat/vbar 16-byte aligned); results are bitwise those of
+ * fp2_prefill whenever the cached slots hold the means of the same tokens. */
+fp2_status_t fp2_prefill_cached(const fp2_params_t* params, const void* q,
+                                const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                                const int32_t* cu_seqlens_k, const int32_t* cu_seqlens_k_host,
+                                const void* k_cache, const void* v_cache,
+                                const int32_t* block_table, const float* q_scale,
+                                const float* k_scale, const float* v_scale,
+                                const fp2_means_cache_t* cache, void* out, float* lse,
+                                uint8_t* block_mask, void* workspace, size_t workspace_bytes,
+                                void* stream);
+
 /* Entries of csr_indices that always suffice for fp2_mask_to_csr: two
  * 64-token key tiles per key block and query tile, 2 * nbk * nbq * batch *
  * num_kv_heads (0 for an invalid params). */

@@ -47,7 +47,14 @@ class Params(ctypes.Structure):
 
 
 EXPORTS = ["fp2_workspace_bytes", "fp2_prefill", "fp2_estimate", "fp2_attend", "fp2_pool",
-           "fp2_csr_capacity", "fp2_mask_to_csr", "fp2_status_str", "fp2_last_error"]
+           "fp2_csr_capacity", "fp2_mask_to_csr", "fp2_means_cache_slots", "fp2_prefill_cached",
+           "fp2_status_str", "fp2_last_error"]
+
+
+class MeansCache(ctypes.Structure):
+    """fp2_means_cache_t: device pointers of a caller-owned block-means cache."""
+    _fields_ = [("khat", ctypes.c_void_p), ("vbar", ctypes.c_void_p),
+                ("pooled_blocks", ctypes.c_void_p)]
 
 
 def lib():
@@ -73,6 +80,11 @@ def lib():
         L.fp2_csr_capacity.argtypes = [P]
         L.fp2_mask_to_csr.restype = ctypes.c_int
         L.fp2_mask_to_csr.argtypes = [P] + [vp] * 7 + [ctypes.c_size_t, vp, ctypes.c_size_t, vp]
+        L.fp2_means_cache_slots.restype = ctypes.c_size_t
+        L.fp2_means_cache_slots.argtypes = [P, ctypes.c_int64]
+        L.fp2_prefill_cached.restype = ctypes.c_int
+        L.fp2_prefill_cached.argtypes = [P] + [vp] * 11 + [ctypes.POINTER(MeansCache)] + \
+            [vp] * 4 + [ctypes.c_size_t, vp]
         L.fp2_status_str.restype = ctypes.c_char_p
         L.fp2_status_str.argtypes = [ctypes.c_int]
         L.fp2_last_error.restype = ctypes.c_char_p
@@ -173,11 +185,14 @@ def alloc_outputs(p: Params, total_tokens: int, device="cuda", want_lse=False):
 
 def prefill(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_seqlens_host=None,
             cu_seqlens_k=None, cu_seqlens_k_host=None, q_scale=None, k_scale=None, v_scale=None,
-            out=None, lse=None, block_mask=None, workspace=None, want_lse=False, stream=None):
+            out=None, lse=None, block_mask=None, workspace=None, want_lse=False, stream=None,
+            means_cache=None):
     """fp2_prefill: returns (out [total, Hq, 128] bf16, block_mask uint8, lse or None).
 
     cu_seqlens_k (device) gives the KV lengths when the queries are the last
-    tokens of longer sequences (a prefix KV); None means no prefix."""
+    tokens of longer sequences (a prefix KV); None means no prefix.
+    means_cache = (khat, vbar, pooled_blocks) device tensors calls
+    fp2_prefill_cached (block means kept across calls)."""
     if out is None or block_mask is None:
         o2, m2, l2 = alloc_outputs(p, q.shape[0], q.device, want_lse and lse is None)
         out = o2 if out is None else out
@@ -185,13 +200,35 @@ def prefill(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_
         lse = l2 if lse is None else lse
     if workspace is None:
         workspace = alloc_workspace(p, q.device)
-    st = lib().fp2_prefill(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
-                           _ptr(cu_seqlens_k), _host_ptr(cu_seqlens_k_host), _ptr(k_cache),
-                           _ptr(v_cache), _ptr(block_table), _ptr(q_scale), _ptr(k_scale),
-                           _ptr(v_scale), _ptr(out), _ptr(lse), _ptr(block_mask),
-                           _ptr(workspace), workspace.numel(), _stream(stream))
-    _check("fp2_prefill", st)
+    head = (ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
+            _ptr(cu_seqlens_k), _host_ptr(cu_seqlens_k_host), _ptr(k_cache), _ptr(v_cache),
+            _ptr(block_table), _ptr(q_scale), _ptr(k_scale), _ptr(v_scale))
+    tail = (_ptr(out), _ptr(lse), _ptr(block_mask), _ptr(workspace), workspace.numel(),
+            _stream(stream))
+    if means_cache is None:
+        _check("fp2_prefill", lib().fp2_prefill(*head, *tail))
+    else:
+        kh, vb, pooled = means_cache
+        mc = MeansCache(_ptr(kh), _ptr(vb), _ptr(pooled))
+        _check("fp2_prefill_cached", lib().fp2_prefill_cached(*head, ctypes.byref(mc), *tail))
     return out, block_mask, lse
+
+
+def means_cache_slots(p: Params, num_pages: int) -> int:
+    """fp2_means_cache_slots: slots of a block-means cache for this params and
+    a pool of num_pages pages."""
+    return int(lib().fp2_means_cache_slots(ctypes.byref(p), int(num_pages)))
+
+
+def alloc_means_cache(p: Params, num_pages: int, device="cuda"):
+    """(khat, vbar) bf16 [slots, Hkv, 128] for fp2_prefill_cached."""
+    import torch
+    n = means_cache_slots(p, num_pages)
+    if n == 0:
+        raise ValueError("no means-cache slots for this configuration: " + last_error())
+    shape = (n, p.num_kv_heads, p.head_dim)
+    return (torch.zeros(shape, dtype=torch.bfloat16, device=device),
+            torch.zeros(shape, dtype=torch.bfloat16, device=device))
 
 
 def estimate(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *,

@@ -289,12 +289,16 @@ size_t fp2_workspace_bytes(const fp2_params_t* params) {
   return layout_of(params).total;
 }
 
-fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
-                         const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
-                         const int32_t* cu_seqlens_k_host, const void* k_cache, const void* v_cache,
-                         const int32_t* block_table, const float* q_scale, const float* k_scale,
-                         const float* v_scale, void* out, float* lse, uint8_t* block_mask,
-                         void* workspace, size_t workspace_bytes, void* stream) {
+namespace {
+
+fp2_status_t prefill_impl(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
+                          const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                          const int32_t* cu_seqlens_k_host, const void* k_cache,
+                          const void* v_cache, const int32_t* block_table, const float* q_scale,
+                          const float* k_scale, const float* v_scale,
+                          const fp2_means_cache_t* cache, void* out, float* lse,
+                          uint8_t* block_mask, void* workspace, size_t workspace_bytes,
+                          void* stream) {
   bool work = false;
   fp2_status_t st = validate_common(params, q, cu_seqlens, cu_seqlens_host, cu_seqlens_k,
                                     cu_seqlens_k_host, k_cache, v_cache, block_table, q_scale,
@@ -306,15 +310,59 @@ fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_
   if ((st = validate_ws(params, workspace, workspace_bytes)) != FP2_OK) return st;
   const fp2::Problem pr = make_problem(params, q, cu_seqlens, cu_seqlens_k, k_cache, v_cache,
                                        block_table, q_scale, k_scale, v_scale);
+  fp2::MeansCache mc{nullptr, nullptr, nullptr, 0};
+  if (cache) {
+    if (!cache->khat || !cache->vbar || !cache->pooled_blocks)
+      return fail(FP2_EINVAL, "means cache: khat, vbar and pooled_blocks must be non-null");
+    if (!aligned16(cache->khat) || !aligned16(cache->vbar))
+      return fail(FP2_EINVAL, "means cache: khat and vbar must be 16-byte aligned");
+    mc = fp2::MeansCache{(uint16_t*)cache->khat, (uint16_t*)cache->vbar, cache->pooled_blocks,
+                         params->page_size > 0 ? (params->page_size + fp2::kBlock - 1) / fp2::kBlock
+                                               : 0};
+  }
   const Views vw = views_of(params, workspace);
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = fp2::launch_pool(pr, vw.pooled, s);
+  hipError_t e = fp2::launch_pool(pr, vw.pooled, s, mc);
   if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s);
   if (e == hipSuccess) e = fp2::launch_plan(pr, vw.kl, vw.plan, s);
   if (e == hipSuccess)
     e = fp2::launch_attend(pr, vw.pooled, block_mask, vw.kl, vw.plan, out, lse, s);
   if (e == hipSuccess) e = fp2::launch_combine(pr, vw.plan, out, lse, s);
   return hip_status(e, "fp2_prefill launch");
+}
+
+}  // namespace
+
+fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
+                         const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
+                         const int32_t* cu_seqlens_k_host, const void* k_cache, const void* v_cache,
+                         const int32_t* block_table, const float* q_scale, const float* k_scale,
+                         const float* v_scale, void* out, float* lse, uint8_t* block_mask,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  return prefill_impl(params, q, cu_seqlens, cu_seqlens_host, cu_seqlens_k, cu_seqlens_k_host,
+                      k_cache, v_cache, block_table, q_scale, k_scale, v_scale, nullptr, out, lse,
+                      block_mask, workspace, workspace_bytes, stream);
+}
+
+fp2_status_t fp2_prefill_cached(const fp2_params_t* params, const void* q,
+                                const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                                const int32_t* cu_seqlens_k, const int32_t* cu_seqlens_k_host,
+                                const void* k_cache, const void* v_cache,
+                                const int32_t* block_table, const float* q_scale,
+                                const float* k_scale, const float* v_scale,
+                                const fp2_means_cache_t* cache, void* out, float* lse,
+                                uint8_t* block_mask, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  if (!cache) return fail(FP2_EINVAL, "means cache is null");
+  return prefill_impl(params, q, cu_seqlens, cu_seqlens_host, cu_seqlens_k, cu_seqlens_k_host,
+                      k_cache, v_cache, block_table, q_scale, k_scale, v_scale, cache, out, lse,
+                      block_mask, workspace, workspace_bytes, stream);
+}
+
+size_t fp2_means_cache_slots(const fp2_params_t* params, int64_t num_pages) {
+  if (validate_params(params) != FP2_OK || num_pages < 0) return 0;
+  if (params->page_size == 0) return (size_t)params->batch * (size_t)nbk_of(params);
+  return (size_t)num_pages * (size_t)((params->page_size + fp2::kBlock - 1) / fp2::kBlock);
 }
 
 fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,

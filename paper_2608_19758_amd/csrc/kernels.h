@@ -38,6 +38,20 @@ struct Pooled {
   uint16_t* vbar;           // [batch, Hkv, nbk, d] bf16 value means (correction)
 };
 
+// Block means kept by the caller across calls (chunked prefill, prefix
+// caching): slot of key block J of sequence b = page id of its first token
+// times per_page plus (offset of that token in its page) / B for a paged pool
+// (per_page = ceil(page / B)), b * nbk + J for contiguous KV. Blocks J below
+// min(pooled[b], complete blocks of b) are copied from the cache instead of
+// being pooled; every pooled block is also written to it. khat == nullptr: no
+// cache.
+struct MeansCache {
+  uint16_t* khat;           // [slots, Hkv, d] bf16
+  uint16_t* vbar;           // [slots, Hkv, d] bf16
+  const int32_t* pooled;    // [batch] leading blocks already in the cache
+  int32_t per_page;
+};
+
 struct KeptLists {
   int32_t* idx;             // [batch, Hkv, nbmax, nbk] ascending kept blocks per row
   int32_t* cnt;             // [batch, Hkv, nbmax]
@@ -66,7 +80,8 @@ int attend_items_per_unit(int g, int qtile);
 // Compute units of the current device (0 if it cannot be queried).
 int device_compute_units();
 
-hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s);
+hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s,
+                       const MeansCache& cache = MeansCache{nullptr, nullptr, nullptr, 0});
 hipError_t launch_estimate(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
                            hipStream_t s);
 hipError_t launch_compact(const Problem& p, const uint8_t* mask, KeptLists kl, hipStream_t s);

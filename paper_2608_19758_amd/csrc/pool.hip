@@ -15,7 +15,9 @@
 //    division rounds once).
 // The rounded key mean khat (bf16, one rounding from fp64) is the scoring key
 // of Eq. fused_score and the surrogate key of the correction; vbar is the
-// value mean in bf16.
+// value mean in bf16. With a caller's means cache (chunked prefill), complete
+// blocks it already holds are copied from it (512 bytes per block and head
+// instead of the block's K/V), and every block pooled here is written to it.
 #include "kernels.h"
 
 namespace fp2 {
@@ -24,8 +26,24 @@ namespace {
 
 constexpr int kThreads = 256;
 
+// Element offset of (key block J of sequence b, KV head h) in the caller's
+// means cache.
+__device__ __forceinline__ int64_t cache_offset(const Problem& p, const MeansCache& mc, int b,
+                                                int J, int h) {
+  int64_t slot;
+  if (p.pm.page == 0) {
+    slot = (int64_t)b * p.nbk + J;
+  } else {
+    const int t = J * kBlock;
+    const int pg = p.pm.shift >= 0 ? t >> p.pm.shift : t / p.pm.page;
+    const int off = t - pg * p.pm.page;
+    slot = (int64_t)p.pm.table[(int64_t)b * p.pm.stride + pg] * mc.per_page + off / kBlock;
+  }
+  return (slot * p.hkv + h) * kHeadDim;
+}
+
 template <int FP8>
-__global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
+__global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out, MeansCache mc) {
   const int J = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
   const int64_t tok0 = p.cuk[b];
@@ -39,6 +57,23 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
     }
     return;
   }
+  const int64_t cbase = mc.khat ? cache_offset(p, mc, b, J, h) : 0;
+  if (mc.khat && J < min(mc.pooled[b], L / kBlock)) {   // complete block, already pooled
+    if (tid < kHeadDim) {
+      out.khat[obase + tid] = mc.khat[cbase + tid];
+      out.vbar[obase + tid] = mc.vbar[cbase + tid];
+    }
+    return;
+  }
+  // the means go to the workspace and, with a cache, to the block's slot
+  auto store = [&](uint16_t kh, uint16_t vb) {
+    out.khat[obase + tid] = kh;
+    out.vbar[obase + tid] = vb;
+    if (mc.khat) {
+      mc.khat[cbase + tid] = kh;
+      mc.vbar[cbase + tid] = vb;
+    }
+  };
   const int cnt = min(kBlock, L - J * kBlock);
   __shared__ double redk[16][kHeadDim];
   __shared__ double redv[16][kHeadDim];
@@ -88,8 +123,7 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
         sk += redk[g][tid];
         sv += redv[g][tid];
       }
-      out.khat[obase + tid] = f64_to_bf16(sk / (double)cnt);
-      out.vbar[obase + tid] = f64_to_bf16(sv / (double)cnt);
+      store(f64_to_bf16(sk / (double)cnt), f64_to_bf16(sv / (double)cnt));
     }
   } else {
     // 8 threads per token row (16 codes each), 32 row groups.
@@ -156,21 +190,21 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out) {
         sv += redvi[g * kHeadDim + tid];
       }
       double ks = (double)p.k_scale[h], vs = (double)p.v_scale[h];
-      out.khat[obase + tid] = f64_to_bf16(((double)sk * 0x1p-9 * ks) / (double)cnt);
-      out.vbar[obase + tid] = f64_to_bf16(((double)sv * 0x1p-9 * vs) / (double)cnt);
+      store(f64_to_bf16(((double)sk * 0x1p-9 * ks) / (double)cnt),
+            f64_to_bf16(((double)sv * 0x1p-9 * vs) / (double)cnt));
     }
   }
 }
 
 }  // namespace
 
-hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s) {
+hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s, const MeansCache& cache) {
   if (p.batch == 0 || p.nbk == 0) return hipSuccess;
   dim3 grid(p.nbk, p.hkv, p.batch);
   if (p.fp8)
-    pool_kernel<1><<<grid, kThreads, 0, s>>>(p, out);
+    pool_kernel<1><<<grid, kThreads, 0, s>>>(p, out, cache);
   else
-    pool_kernel<0><<<grid, kThreads, 0, s>>>(p, out);
+    pool_kernel<0><<<grid, kThreads, 0, s>>>(p, out, cache);
   return hipGetLastError();
 }
 

@@ -202,3 +202,29 @@ def test_mask_to_csr_validation():
     assert call(cu=None) == fp2.EINVAL
     assert call() == fp2.EWORKSPACE
     assert fp2.csr_capacity(base(query_tile_rows=7)) == 0
+
+
+def test_means_cache_slots_and_validation():
+    """Slot counts of the block-means cache, and the cached prefill's checks
+    of its cache argument (all before any launch)."""
+    p = base()                                   # page 64: one slot per page
+    assert fp2.means_cache_slots(p, 1000) == 1000
+    assert fp2.means_cache_slots(base(page_size=200, max_pages_per_seq=21), 10) == 20
+    assert fp2.means_cache_slots(base(page_size=128, max_pages_per_seq=32), 10) == 10
+    assert fp2.means_cache_slots(base(page_size=0, max_kv_len=5000), 0) == 2 * 40
+    assert fp2.means_cache_slots(p, -1) == 0
+    assert fp2.means_cache_slots(base(head_dim=64), 10) == 0
+    L = fp2.lib()
+    ws_need = fp2.workspace_bytes(p)
+    ws = ctypes.c_void_p(0x200000)
+
+    def cached(cache):
+        return L.fp2_prefill_cached(ctypes.byref(p), FAKE, FAKE, None, None, None, FAKE, FAKE,
+                                    FAKE, None, None, None, cache, FAKE, None, FAKE, ws, ws_need,
+                                    None)
+    assert cached(None) == fp2.EINVAL
+    assert cached(ctypes.byref(fp2.MeansCache(None, FAKE.value, FAKE.value))) == fp2.EINVAL
+    assert cached(ctypes.byref(fp2.MeansCache(FAKE.value, FAKE.value, None))) == fp2.EINVAL
+    assert "pooled_blocks" in fp2.last_error()
+    assert cached(ctypes.byref(fp2.MeansCache(0x100008, FAKE.value, FAKE.value))) == fp2.EINVAL
+    assert "aligned" in fp2.last_error()
