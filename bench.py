@@ -247,7 +247,9 @@ def chunked(cfg, steps, warmup):
     forward_extend calls with the per-forward metadata prepared beforehand;
     short tail chunks (the last T tokens after a 128K - T prefix) with the
     cost-balanced KV splits against kv_splits = 1; and one continuous-batching
-    forward mixing four requests at different prefix lengths."""
+    forward mixing four requests at different prefix lengths. Chunk sequences
+    and tails are also timed with the block-means cache (complete prefix
+    blocks copied instead of pooled again)."""
     import torch
     import paper_2608_19758_amd.serving as serving
     sp, wl, d = cfg["spec"], cfg["wl"], cfg["d"]
@@ -274,32 +276,54 @@ def chunked(cfg, steps, warmup):
     for C in (16384, 8192):
         be = backend(1, C)
         bt = table(be, 1)
-        calls = []
-        for c0 in range(0, L, C):
-            meta = be.init_forward_metadata([C], [c0], bt)
-            calls.append((meta, d["q"][c0:c0 + C]))
+        mc = be.alloc_means_cache(wl.num_pages)
         out = torch.empty((C, sp.num_q_heads, sp.head_dim), dtype=torch.bfloat16, device=dev)
+        r = {"chunk": C}
+        # without and with the block-means cache (chunk c takes the complete
+        # blocks of its prefix, which the chunks before it pooled)
+        for key, cache in (("total_ms", None), ("total_ms_means_cache", mc)):
+            calls = []
+            for c0 in range(0, L, C):
+                meta = be.init_forward_metadata([C], [c0], bt,
+                                                cached_prefix_lens=None if cache is None else [c0])
+                calls.append((meta, d["q"][c0:c0 + C]))
 
-        def all_chunks():
-            for meta, q in calls:
-                be.forward_extend(q, d["k_cache"], d["v_cache"], meta, out=out, **kw)
-        t, _ = time_loop(all_chunks, max(3, steps // 4), max(1, warmup // 2))
-        res["chunks"].append({"chunk": C, "calls": len(calls), "total_ms": round(t, 4)})
-        print("[bench] chunked %d x %d: %.3f ms" % (len(calls), C, t), file=sys.stderr, flush=True)
-        del be, calls
+            def all_chunks():
+                for meta, q in calls:
+                    be.forward_extend(q, d["k_cache"], d["v_cache"], meta, out=out,
+                                      means_cache=cache, **kw)
+            t, _ = time_loop(all_chunks, max(3, steps // 4), max(1, warmup // 2))
+            r[key] = round(t, 4)
+            r["calls"] = len(calls)
+        res["chunks"].append(r)
+        print("[bench] chunked %d x %d: %.3f ms, with the means cache %.3f ms"
+              % (r["calls"], C, r["total_ms"], r["total_ms_means_cache"]), file=sys.stderr,
+              flush=True)
+        del be, calls, mc
     for T in (128, 1024, 4096):
         r = {"tail_tokens": T, "prefix": L - T}
-        for splits, key in ((0, "ms_planned_splits"), (1, "ms_no_splits")):
+        for splits, key in ((0, "ms_planned_splits"), (1, "ms_no_splits"),
+                            (0, "ms_planned_splits_means_cache")):
             be = backend(1, T, splits)
-            meta = be.init_forward_metadata([T], [L - T], table(be, 1))
             q = d["q"][L - T:]
             out = torch.empty((T, sp.num_q_heads, sp.head_dim), dtype=torch.bfloat16, device=dev)
+            mc = None
+            if key.endswith("means_cache"):
+                # one call fills the cache with the means of every block
+                mc = be.alloc_means_cache(wl.num_pages)
+                fill = be.init_forward_metadata([T], [L - T], table(be, 1))
+                be.forward_extend(q, d["k_cache"], d["v_cache"], fill, out=out, means_cache=mc,
+                                  **kw)
+            meta = be.init_forward_metadata([T], [L - T], table(be, 1),
+                                            cached_prefix_lens=None if mc is None else [L - T])
             r[key] = round(time_loop(lambda: be.forward_extend(q, d["k_cache"], d["v_cache"], meta,
-                                                               out=out, **kw), steps, warmup)[0], 4)
-            del be
+                                                               out=out, means_cache=mc, **kw),
+                                     steps, warmup)[0], 4)
+            del be, mc
         res["tails"].append(r)
-        print("[bench] tail %d: planned splits %.3f ms, none %.3f ms"
-              % (T, r["ms_planned_splits"], r["ms_no_splits"]), file=sys.stderr, flush=True)
+        print("[bench] tail %d: planned splits %.3f ms, none %.3f ms, planned + means cache %.3f ms"
+              % (T, r["ms_planned_splits"], r["ms_no_splits"], r["ms_planned_splits_means_cache"]),
+              file=sys.stderr, flush=True)
     # four requests of the same sequence data at different stages of their
     # prefill, in one forward (continuous batching)
     ext, pre = [8192, 8192, 4096, 1024], [0, 32768, 90112, 130048]
@@ -309,10 +333,17 @@ def chunked(cfg, steps, warmup):
     out = torch.empty((q.shape[0], sp.num_q_heads, sp.head_dim), dtype=torch.bfloat16, device=dev)
     t, _ = time_loop(lambda: be.forward_extend(q, d["k_cache"], d["v_cache"], meta, out=out, **kw),
                      steps, warmup)
+    mc = be.alloc_means_cache(wl.num_pages)
+    be.forward_extend(q, d["k_cache"], d["v_cache"], meta, out=out, means_cache=mc, **kw)   # fill
+    meta_c = be.init_forward_metadata(ext, pre, table(be, 4), cached_prefix_lens=pre)
+    tc, _ = time_loop(lambda: be.forward_extend(q, d["k_cache"], d["v_cache"], meta_c, out=out,
+                                                means_cache=mc, **kw), steps, warmup)
     dense = sum(sp.num_q_heads * 4 * sp.head_dim * (e * p + e * (e + 1) / 2) for e, p in zip(ext, pre))
     res["batched"] = {"extend": ext, "prefix": pre, "ms": round(t, 4),
+                      "ms_means_cache": round(tc, 4),
                       "dense_equiv_tflops": round(dense / (t * 1e-3) / 1e12, 1)}
-    print("[bench] batched forward %s after %s: %.3f ms" % (ext, pre, t), file=sys.stderr, flush=True)
+    print("[bench] batched forward %s after %s: %.3f ms, with the means cache %.3f ms"
+          % (ext, pre, t, tc), file=sys.stderr, flush=True)
     del be
     torch.cuda.empty_cache()
     return res

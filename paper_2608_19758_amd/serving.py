@@ -15,6 +15,13 @@ while decode attention stays dense):
   shared by all layers: the length arrays are uploaded to the device once.
 - ``forward_extend``: one layer's attention over the paged cache, through the
   C ABI. The K/V of the new tokens must already be in the cache.
+- Block means across forwards: ``alloc_means_cache`` gives a layer's cache of
+  pooled key/value means (one slot per 128-token block of the paged pool,
+  about 2/(page * bytes per element) of the KV cache). Passed to
+  ``forward_extend``, a forward pools only the blocks that are new or were
+  incomplete, and copies the complete blocks of the cached prefix, whose
+  means an earlier forward through the same cache wrote (chunked prefill, or
+  prefix pages shared between requests).
 
 Cached prefixes may have any length (a prefix-cache hit is page-granular);
 ``plan_forward`` checks the lengths against the configured bounds before
@@ -111,6 +118,7 @@ class ForwardMetadata:
     cu_q: object                   # device int32 [batch + 1]
     cu_k: object                   # device int32 [batch + 1]
     block_table: object            # device int32 [batch, >= max_pages_per_seq]
+    pooled_blocks: object          # device int32 [batch]: cached complete prefix blocks
 
     @property
     def params(self):
@@ -135,16 +143,36 @@ class PrefillBackend:
                                  dtype=torch.uint8, device=self.device)
 
     def init_forward_metadata(self, extend_lens: Sequence[int], prefix_lens: Optional[Sequence[int]],
-                              block_table) -> ForwardMetadata:
+                              block_table, cached_prefix_lens: Optional[Sequence[int]] = None
+                              ) -> ForwardMetadata:
+        """cached_prefix_lens[b]: leading tokens of sequence b whose block means an
+        earlier forward wrote to the means caches used with this metadata (None:
+        none); only its complete blocks are taken from the cache."""
         import torch
         plan = plan_forward(self.cfg, extend_lens, prefix_lens)
         if fp2.workspace_bytes(plan.params) > self.workspace.numel():
             raise RuntimeError("forward needs more workspace than the configured worst case")
-        cu = torch.from_numpy(np.stack([plan.cu_q, plan.cu_k])).to(self.device)
+        n = len(plan.cu_q) - 1
+        cached = [0] * n if cached_prefix_lens is None else [int(x) for x in cached_prefix_lens]
+        if len(cached) != n:
+            raise ValueError("cached_prefix_lens and extend_lens differ in length")
+        kv = np.diff(plan.cu_k)
+        for b, c in enumerate(cached):
+            if c < 0 or c > kv[b]:
+                raise ValueError("sequence %d: %d cached tokens outside [0, %d]" % (b, c, kv[b]))
+        pooled = np.array([c // BLOCK for c in cached], np.int32)
+        host = np.concatenate([plan.cu_q, plan.cu_k, pooled]).astype(np.int32)
+        dev = torch.from_numpy(host).to(self.device)
         if block_table.shape[1] < self.cfg.max_pages_per_seq:
             raise ValueError("block_table has %d columns, the config needs %d"
                              % (block_table.shape[1], self.cfg.max_pages_per_seq))
-        return ForwardMetadata(plan=plan, cu_q=cu[0], cu_k=cu[1], block_table=block_table)
+        return ForwardMetadata(plan=plan, cu_q=dev[:n + 1], cu_k=dev[n + 1:2 * n + 2],
+                               block_table=block_table, pooled_blocks=dev[2 * n + 2:])
+
+    def alloc_means_cache(self, num_pages: int):
+        """One layer's block-means cache for a pool of num_pages pages:
+        (khat, vbar) bf16 [slots, num_kv_heads, 128]."""
+        return fp2.alloc_means_cache(self.cfg.worst_case_params(), num_pages, self.device)
 
     def block_mask(self, meta: ForwardMetadata):
         """The selection mask written by the last forward_extend, as a view
@@ -155,8 +183,10 @@ class PrefillBackend:
         return self._mask[:n].view(shape)
 
     def forward_extend(self, q, k_cache, v_cache, meta: ForwardMetadata, *, q_scale=None,
-                       k_scale=None, v_scale=None, out=None, lse=None, want_lse=False):
+                       k_scale=None, v_scale=None, out=None, lse=None, want_lse=False,
+                       means_cache=None):
         """One layer: q [total_new_tokens, Hq, 128] against the paged cache.
+        means_cache: this layer's (khat, vbar) from alloc_means_cache, or None.
         Returns (out, lse or None)."""
         import torch
         p = meta.params
@@ -172,7 +202,9 @@ class PrefillBackend:
                     cu_seqlens_host=meta.plan.cu_q, cu_seqlens_k=meta.cu_k,
                     cu_seqlens_k_host=meta.plan.cu_k, q_scale=q_scale, k_scale=k_scale,
                     v_scale=v_scale, out=out, lse=lse, block_mask=self.block_mask(meta),
-                    workspace=self.workspace, stream=self.stream)
+                    workspace=self.workspace, stream=self.stream,
+                    means_cache=None if means_cache is None
+                    else (means_cache[0], means_cache[1], meta.pooled_blocks))
         return out, lse
 
     def forward_decode(self, *args, **kwargs):

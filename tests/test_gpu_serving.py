@@ -4,7 +4,9 @@ through per-forward metadata shared by the layers and one workspace.
 
 Without KV splits every forward reproduces, bit for bit, the rows of one
 whole-sequence fp2_prefill call (outputs, LSE and mask rows); with the default
-cost-balanced splits it agrees within the output tolerance."""
+cost-balanced splits it agrees within the output tolerance. With per-layer
+block-means caches the second forward takes the first chunk's complete blocks
+from them, and the same bars hold."""
 import numpy as np
 import pytest
 import torch
@@ -30,7 +32,8 @@ def layer(seed, dtype):
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp8"])
 @pytest.mark.parametrize("kv_splits", [1, 0])
-def test_backend_chunked_forwards(dtype, kv_splits):
+@pytest.mark.parametrize("cache", [False, True])
+def test_backend_chunked_forwards(dtype, kv_splits, cache):
     layers = [layer(s, dtype) for s in (11, 12)]
     sp = layers[0].spec
     cfg = serving.BackendConfig(num_q_heads=8, num_kv_heads=2, page_size=64, max_batch=2,
@@ -48,15 +51,17 @@ def test_backend_chunked_forwards(dtype, kv_splits):
     ref = [gu.gpu_prefill(wl, gu.params_for(wl, ALPHA, kv_splits=1)) for wl in layers]
     cu = layers[0].cu_seqlens
     forwards = [(CHUNK1, [0, 0]), ([k - c for k, c in zip(KV, CHUNK1)], CHUNK1)]
+    caches = [be.alloc_means_cache(layers[0].num_pages) if cache else None for _ in layers]
     for ext, pre in forwards:
-        meta = be.init_forward_metadata(ext, pre, bt)
+        meta = be.init_forward_metadata(ext, pre, bt, cached_prefix_lens=pre if cache else None)
         rows = np.concatenate([np.arange(cu[b] + p, cu[b] + p + e) for b, (e, p) in
                                enumerate(zip(ext, pre))])
         ridx = torch.from_numpy(rows).cuda()
         for li, (wl, d) in enumerate(zip(layers, dev)):
             out, lse = be.forward_extend(d["q"][ridx].contiguous(), d["k_cache"], d["v_cache"],
                                          meta, q_scale=d["q_scale"], k_scale=d["k_scale"],
-                                         v_scale=d["v_scale"], want_lse=True)
+                                         v_scale=d["v_scale"], want_lse=True,
+                                         means_cache=caches[li])
             torch.cuda.synchronize()
             o = out.float().cpu().numpy().astype(np.float64)
             l = lse.cpu().numpy().astype(np.float64)
@@ -67,8 +72,8 @@ def test_backend_chunked_forwards(dtype, kv_splits):
                 np.testing.assert_array_equal(mask[b, :, :nq, :nk],
                                               rm[b, :, p // 128:p // 128 + nq, :nk])
             d_out = np.abs(o - ro[rows]).max()
-            print("dtype %s splits %d forward %s layer %d: max |backend - whole| %.3g"
-                  % (dtype, kv_splits, ext, li, d_out))
+            print("dtype %s splits %d cache %d forward %s layer %d: max |backend - whole| %.3g"
+                  % (dtype, kv_splits, cache, ext, li, d_out))
             if kv_splits == 1:
                 np.testing.assert_array_equal(o, ro[rows])
                 np.testing.assert_array_equal(l, rl[rows])
@@ -86,5 +91,7 @@ def test_backend_rejects_oversized_forward():
         be.init_forward_metadata([300], [0], bt)
     with pytest.raises(ValueError):
         be.init_forward_metadata([128], [128], bt[:, :2])
+    with pytest.raises(ValueError):
+        be.init_forward_metadata([128], [128], bt, cached_prefix_lens=[300])
     with pytest.raises(NotImplementedError):
         be.forward_decode()
