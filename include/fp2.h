@@ -179,6 +179,13 @@ typedef struct {
                                  positions with all g heads; 128 = one
                                  M-tile of 128 packed rows (128/g positions
                                  with all g heads); see "Query tiles" above */
+  int32_t score_splits;       /* parts of a unit's query rows in the scoring:
+                                 0 = automatic (calls with fewer units than
+                                 half the compute units, i.e. short chunks,
+                                 split each unit's rows over several
+                                 workgroups and merge their block energies);
+                                 n in 1..64 = at most n parts, 1 = none.
+                                 Results depend on it through rounding only */
 } fp2_params_t;
 
 /* Bytes of workspace the entry points need for `params` (0 for a null or

@@ -43,6 +43,7 @@ class Params(ctypes.Structure):
         ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
         ("max_kv_len", ctypes.c_int32), ("kv_splits", ctypes.c_int32),
         ("query_tile_rows", ctypes.c_int32),
+        ("score_splits", ctypes.c_int32),
     ]
 
 
@@ -110,11 +111,13 @@ def make_params(*, batch, num_q_heads, num_kv_heads, max_seq_len, page_size=0,
                 max_pages_per_seq=0, alpha=0.0, sink_blocks=1, window_blocks=2,
                 recent_blocks=0, mean_correction=1, softmax_scale=0.0, dtype="bf16",
                 head_dim=HEAD_DIM, block_size=BLOCK, max_kv_len=0, kv_splits=0,
-                query_tile_rows=0) -> Params:
+                query_tile_rows=0, score_splits=0) -> Params:
     """fp2_params_t; max_kv_len bounds the KV lengths with a prefix (0: max_seq_len);
     kv_splits: 0 = cost-balanced KV splits planned on the device, n = n parts per unit
     (1 = none); query_tile_rows: 0 = query blocks of 128 positions x g heads,
-    128 = tiles of 128 packed rows (128 / g positions x g heads)."""
+    128 = tiles of 128 packed rows (128 / g positions x g heads); score_splits:
+    0 = the scoring splits the rows of units over several workgroups in calls
+    with few units, n = at most n parts (1 = none)."""
     dt = {"bf16": BF16, "fp8": FP8_E4M3}.get(dtype, dtype)
     return Params(batch=batch, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
                   head_dim=head_dim, block_size=block_size, page_size=page_size,
@@ -122,7 +125,8 @@ def make_params(*, batch, num_q_heads, num_kv_heads, max_seq_len, page_size=0,
                   alpha=alpha, sink_blocks=sink_blocks, window_blocks=window_blocks,
                   recent_blocks=recent_blocks, mean_correction=int(mean_correction),
                   softmax_scale=softmax_scale, dtype=dt, max_kv_len=max_kv_len,
-                  kv_splits=kv_splits, query_tile_rows=query_tile_rows)
+                  kv_splits=kv_splits, query_tile_rows=query_tile_rows,
+                  score_splits=score_splits)
 
 
 def tile_positions(p: Params) -> int:

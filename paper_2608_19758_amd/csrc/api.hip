@@ -145,6 +145,8 @@ fp2_status_t validate_params(const fp2_params_t* p) {
     return fail(FP2_EINVAL, "dtype %d unknown", p->dtype);
   if (p->kv_splits < 0 || p->kv_splits > kMaxSplits)
     return fail(FP2_EINVAL, "kv_splits %d not in [0, %d]", p->kv_splits, kMaxSplits);
+  if (p->score_splits < 0 || p->score_splits > 64)
+    return fail(FP2_EINVAL, "score_splits %d not in [0, 64]", p->score_splits);
   if (p->query_tile_rows != 0 && p->query_tile_rows != 128)
     return fail(FP2_EUNSUPPORTED, "query_tile_rows %d not 0 or 128", p->query_tile_rows);
   return FP2_OK;
@@ -242,6 +244,7 @@ fp2::Problem make_problem(const fp2_params_t* p, const void* q, const int32_t* c
   pr.recent = p->recent_blocks;
   pr.corr = p->mean_correction;
   pr.splits = p->kv_splits;
+  pr.ssplits = p->score_splits;
   pr.alpha = p->alpha;
   const double scale = p->softmax_scale > 0.f ? (double)p->softmax_scale : 1.0 / sqrt((double)p->head_dim);
   pr.scale_log2 = (float)(scale * 1.4426950408889634074);
@@ -253,6 +256,7 @@ struct Views {
   fp2::Pooled pooled;
   fp2::KeptLists kl;
   fp2::Plan plan;
+  size_t part_o_floats;   // the partial outputs, also the scoring's row-split scratch
 };
 
 Views views_of(const fp2_params_t* p, void* ws) {
@@ -272,6 +276,8 @@ Views views_of(const fp2_params_t* p, void* ws) {
   v.plan.cap_items = l.cap_items;
   v.plan.cap_slots = l.cap_slots;
   v.plan.target_items = 4 * fp2::device_compute_units();
+  const size_t rpu = (size_t)(p->num_q_heads / p->num_kv_heads) * qtile_of(p);
+  v.part_o_floats = l.part_o ? (size_t)l.cap_slots * rpu * fp2::kHeadDim : 0;
   return v;
 }
 
@@ -323,7 +329,8 @@ fp2_status_t prefill_impl(const fp2_params_t* params, const void* q, const int32
   const Views vw = views_of(params, workspace);
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = fp2::launch_pool(pr, vw.pooled, s, mc);
-  if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s);
+  if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s, vw.plan.part_o,
+                                                vw.part_o_floats);
   if (e == hipSuccess) e = fp2::launch_plan(pr, vw.kl, vw.plan, s);
   if (e == hipSuccess)
     e = fp2::launch_attend(pr, vw.pooled, block_mask, vw.kl, vw.plan, out, lse, s);
@@ -384,7 +391,8 @@ fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32
   const Views vw = views_of(params, workspace);
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = fp2::launch_pool(pr, vw.pooled, s);
-  if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s);
+  if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s, vw.plan.part_o,
+                                                vw.part_o_floats);
   return hip_status(e, "fp2_estimate launch");
 }
 

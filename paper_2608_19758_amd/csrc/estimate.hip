@@ -41,17 +41,73 @@ constexpr int kChunksPerWave = 4;                          // 4 x 32 key blocks 
 constexpr int kGroup = kWaves * kChunksPerWave * 32;       // key blocks per pass (1024)
 constexpr int kQRow = 17;                                  // LDS row stride of a Q tile, 16-byte slots
 
+// Row split of the scoring for calls with few units (short chunks): part u
+// of parts.n scores the unit's 32-row tiles [u ceil(T/n), ...) and writes
+// its block log2-energies to buf (one row of nbk floats per item);
+// select_kernel merges them per unit. parts.n == 1: one item per unit, the
+// selection in the same kernel.
+struct EllParts {
+  float* buf;
+  int n;
+};
+
+// Selection of one unit from its block log2-energies ell[0 .. Ia] in LDS
+// (Eq. select): J is kept iff alpha == 0, ell_J >= max ell + log2 alpha, or
+// J is forced (sink, window counted back from Ia, the band Ja .. Ia, recent).
+// Writes the mask row in full and the ascending kept list with its count.
+template <class Prob>   // Problem, or the kernel-argument copy of it
+__device__ void select_unit(const Prob& p, const float* ell, int Ia, int Ja, int nk,
+                            uint8_t* mrow, int32_t* kidx, int32_t* cnt, float* redf, int* redi,
+                            int tid) {
+  const int lane = tid & 63, w = tid >> 6;
+  float mu = -INFINITY;
+  for (int J = tid; J <= Ia; J += kThreads) mu = fmaxf(mu, ell[J]);
+  mu = wave_max(mu);
+  if (lane == 0) redf[w] = mu;
+  __syncthreads();
+  mu = redf[0];
+#pragma unroll
+  for (int k = 1; k < kWaves; ++k) mu = fmaxf(mu, redf[k]);
+  const bool keep_all = p.alpha == 0.f;
+  const float thr = keep_all ? -INFINITY : mu + fast_log2(p.alpha);
+
+  int base = 0;
+  for (int J0 = 0; J0 < p.nbk; J0 += kThreads) {
+    const int J = J0 + tid;
+    const bool valid = J <= Ia;
+    const bool forced = valid && (J < p.sink || Ia - J < p.window || J >= Ja || J >= nk - p.recent);
+    const bool keep = valid && (keep_all || forced || ell[J] >= thr);
+    if (J < p.nbk) mrow[J] = (uint8_t)((keep ? 1 : 0) | (forced ? 2 : 0));
+    if (J0 <= Ia) {
+      const uint64_t bal = __ballot(keep);
+      const int pre = __popcll(bal & ((1ull << lane) - 1ull));
+      __syncthreads();
+      if (lane == 0) redi[w] = __popcll(bal);
+      __syncthreads();
+      int wpre = 0, tot = 0;
+#pragma unroll
+      for (int k = 0; k < kWaves; ++k) {
+        wpre += k < w ? redi[k] : 0;
+        tot += redi[k];
+      }
+      if (keep) kidx[base + wpre + pre] = J;
+      base += tot;
+    }
+  }
+  if (tid == 0) *cnt = base;
+}
+
 template <int FP8, int G>
 __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled pooled,
                                                             uint8_t* __restrict__ mask,
-                                                            KeptLists kl) {
+                                                            KeptLists kl, EllParts parts) {
   extern __shared__ float ell[];            // [nbk] block log2-energies of this row
   __shared__ uint4 qt[2][64 * kQRow];       // Q tile pairs (double buffer): 2 x 32 rows x 16 chunks of 8 bf16
   __shared__ float redf[kWaves];
   __shared__ int redi[kWaves];
 
   const int nbh = p0.batch * p0.hkv;
-  const int nitems = p0.nbmax * nbh;
+  const int nitems = p0.nbmax * nbh * parts.n;
 
   // Persistent workgroups, items dealt round-robin in order of decreasing
   // query block: the cost of an item is proportional to (I + 1), so every
@@ -68,8 +124,9 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
   asm volatile("" : "+s"(pk));
   KProblem& p = *pk;
 
-  const int I = p.nbmax - 1 - item / nbh;
-  const int bh = item % nbh;
+  const int uidx = item / parts.n, part = item - uidx * parts.n;   // unit, row-tile part
+  const int I = p.nbmax - 1 - uidx / nbh;
+  const int bh = uidx % nbh;
   const int b = bh / p.hkv, h = bh % p.hkv;
   const int lane = tid & 63, w = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
@@ -86,14 +143,25 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
   uint8_t* mrow = mask + row * p.nbk;
 
   if (I >= n) {
-    for (int J = tid; J < p.nbk; J += kThreads) mrow[J] = 0;
-    if (tid == 0) kl.cnt[row] = 0;
+    if (parts.n == 1) {   // (select_kernel clears the row in the split mode)
+      for (int J = tid; J < p.nbk; J += kThreads) mrow[J] = 0;
+      if (tid == 0) kl.cnt[row] = 0;
+    }
     continue;
   }
 
   const int npos = min(p.qtile, L - I * p.qtile);
   const int nrows = npos * G;
   const int ntiles = (nrows + 31) / 32;
+  // this item's 32-row tiles [tlo, thi): all of them, or part `part` of
+  // parts.n; energies of a part go to parts.buf, one row of nbk per item
+  const int tper = (ntiles + parts.n - 1) / parts.n;
+  const int tlo = min(ntiles, part * tper), thi = min(ntiles, tlo + tper);
+  float* pell = parts.buf + (int64_t)item * p.nbk;
+  if (tlo >= thi) {   // an empty part adds nothing
+    for (int J = tid; J <= Ia; J += kThreads) pell[J] = -INFINITY;
+    continue;
+  }
 
   // Row r = 8i + 4*half + j of a 32-row tile has head offset (4*half + j) % G.
   float cs[4];
@@ -111,7 +179,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     uint4 v = make_uint4(0, 0, 0, 0);
     const int r = FP8 ? tid >> 3 : tid >> 4;
     const int pr = t * 32 + r;
-    if (t < ntiles && pr < nrows && (!FP8 || tid < 256)) {
+    if (t < thi && pr < nrows && (!FP8 || tid < 256)) {
       const int pos = I * p.qtile + pr / G, hq = h * G + pr % G;
       if (FP8)
         v = *(const uint4*)((const uint8_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + (tid & 7) * 16);
@@ -164,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     // is scored. Only the last tile can be partial: it runs as a separate
     // instance of the tile body, so the row validity tests stay out of the
     // full tiles.
-    uint4 qa_next = qload(0), qa_next2 = qload(1);
+    uint4 qa_next = qload(tlo), qa_next2 = qload(tlo + 1);
     auto tile = [&](const uint4* qb, int t, auto partial) {
       constexpr bool kPartial = decltype(partial)::value;
 
@@ -246,14 +314,14 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       }
     };
     const int nfull = nrows >> 5;
-    for (int t0 = 0; t0 < ntiles; t0 += 2) {
-      uint4* buf = qt[(t0 >> 1) & 1];
+    for (int t0 = tlo; t0 < thi; t0 += 2) {
+      uint4* buf = qt[((t0 - tlo) >> 1) & 1];
       qstore(buf, qa_next);
       qstore(buf + 32 * kQRow, qa_next2);
       __syncthreads();   // tiles t0, t0+1 visible; every wave is done with the pair before
       qa_next = qload(t0 + 2);
       qa_next2 = qload(t0 + 3);
-      for (int k = 0; k < 2 && t0 + k < ntiles; ++k) {
+      for (int k = 0; k < 2 && t0 + k < thi; ++k) {
         if (t0 + k < nfull)
           tile(buf + k * 32 * kQRow, t0 + k, std::false_type{});
         else
@@ -271,49 +339,72 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       float e1 = m[c] == -INFINITY ? 0.f : E[c] * fast_exp2(m[c] - M);
       float e2 = m2 == -INFINITY ? 0.f : E2 * fast_exp2(m2 - M);
       const int J = grp + 32 * (w + kWaves * c) + l32;
-      if (half == 0 && J <= Ia) ell[J] = M + fast_log2(e1 + e2);
+      if (half == 0 && J <= Ia) {
+        const float v = M + fast_log2(e1 + e2);
+        if (parts.n > 1)
+          pell[J] = v;
+        else
+          ell[J] = v;
+      }
     }
     __syncthreads();   // every wave is done with the Q tile buffers and ell of this group
   }
 
-  // ---- selection: max-based threshold plus forced blocks (Eq. select)
-  float mu = -INFINITY;
-  for (int J = tid; J <= Ia; J += kThreads) mu = fmaxf(mu, ell[J]);
-  mu = wave_max(mu);
-  if (lane == 0) redf[w] = mu;
-  __syncthreads();
-  mu = redf[0];
-#pragma unroll
-  for (int k = 1; k < kWaves; ++k) mu = fmaxf(mu, redf[k]);
-  const bool keep_all = p.alpha == 0.f;
-  const float thr = keep_all ? -INFINITY : mu + fast_log2(p.alpha);
+  // ---- selection (Eq. select), or the part's energies for select_kernel
+  if (parts.n > 1) continue;
+  select_unit(p, ell, Ia, Ja, nk, mrow, kl.idx + row * p.nbk, kl.cnt + row, redf, redi, tid);
+  }
+}
 
-  int32_t* kidx = kl.idx + row * p.nbk;
-  int base = 0;
-  for (int J0 = 0; J0 < p.nbk; J0 += kThreads) {
-    const int J = J0 + tid;
-    const bool valid = J <= Ia;
-    const bool forced = valid && (J < p.sink || Ia - J < p.window || J >= Ja || J >= nk - p.recent);
-    const bool keep = valid && (keep_all || forced || ell[J] >= thr);
-    if (J < p.nbk) mrow[J] = (uint8_t)((keep ? 1 : 0) | (forced ? 2 : 0));
-    if (J0 <= Ia) {
-      const uint64_t bal = __ballot(keep);
-      const int pre = __popcll(bal & ((1ull << lane) - 1ull));
-      __syncthreads();
-      if (lane == 0) redi[w] = __popcll(bal);
-      __syncthreads();
-      int wpre = 0, tot = 0;
+// Merge of the parts' block energies (log-sum-exp over the parts) and the
+// selection, one workgroup per unit.
+__global__ __launch_bounds__(kThreads) void select_kernel(Problem p, uint8_t* __restrict__ mask,
+                                                          KeptLists kl, EllParts parts) {
+  extern __shared__ float ell[];
+  __shared__ float redf[kWaves];
+  __shared__ int redi[kWaves];
+  const int nbh = p.batch * p.hkv;
+  const int uidx = blockIdx.x;
+  const int I = p.nbmax - 1 - uidx / nbh;
+  const int bh = uidx % nbh;
+  const int b = bh / p.hkv, h = bh % p.hkv;
+  const int tid = threadIdx.x;
+  const int L = p.cu[b + 1] - p.cu[b];
+  const int n = (L + p.qtile - 1) / p.qtile;
+  const int64_t row = ((int64_t)b * p.hkv + h) * p.nbmax + I;
+  uint8_t* mrow = mask + row * p.nbk;
+  if (I >= n) {
+    for (int J = tid; J < p.nbk; J += kThreads) mrow[J] = 0;
+    if (tid == 0) kl.cnt[row] = 0;
+    return;
+  }
+  const int Lk = p.cuk[b + 1] - p.cuk[b];
+  const int nk = (Lk + kBlock - 1) / kBlock;
+  const int Ja = (Lk - L + I * p.qtile) / kBlock;
+  const int Ia = (Lk - L + min(L, (I + 1) * p.qtile) - 1) / kBlock;
+  const float* pe = parts.buf + (int64_t)uidx * parts.n * p.nbk;
+  for (int J = tid; J <= Ia; J += kThreads) {
+    // running log-sum-exp over the parts, eight loads in flight at a time
+    float M = -INFINITY, e = 0.f;
+    for (int u0 = 0; u0 < parts.n; u0 += 8) {
+      float v[8];
 #pragma unroll
-      for (int k = 0; k < kWaves; ++k) {
-        wpre += k < w ? redi[k] : 0;
-        tot += redi[k];
-      }
-      if (keep) kidx[base + wpre + pre] = J;
-      base += tot;
+      for (int k = 0; k < 8; ++k)
+        v[k] = u0 + k < parts.n ? pe[(int64_t)(u0 + k) * p.nbk + J] : -INFINITY;
+      float mk = v[0];
+#pragma unroll
+      for (int k = 1; k < 8; ++k) mk = fmaxf(mk, v[k]);
+      const float Mn = fmaxf(M, mk);
+      if (Mn == -INFINITY) continue;
+      e = M == -INFINITY ? 0.f : e * fast_exp2(M - Mn);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) e += fast_exp2(v[k] - Mn);
+      M = Mn;
     }
+    ell[J] = M == -INFINITY ? M : M + fast_log2(e);
   }
-  if (tid == 0) kl.cnt[row] = base;
-  }
+  __syncthreads();
+  select_unit(p, ell, Ia, Ja, nk, mrow, kl.idx + row * p.nbk, kl.cnt + row, redf, redi, tid);
 }
 
 // Kept lists from a caller-given mask (bit 0), ascending; one workgroup per row.
@@ -359,27 +450,39 @@ __global__ __launch_bounds__(256) void compact_kernel(Problem p, const uint8_t* 
 
 template <int FP8>
 hipError_t launch_est_dt(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
-                         hipStream_t s) {
+                         float* scratch, size_t scratch_floats, hipStream_t s) {
   const int cus = device_compute_units();
   if (cus <= 0) return hipErrorInvalidDevice;
-  const unsigned grid = (unsigned)std::min<int64_t>((int64_t)p.nbmax * p.batch * p.hkv, cus);
+  const int64_t units = (int64_t)p.nbmax * p.batch * p.hkv;
+  // few units (short chunks): split their rows so that the grid covers the
+  // CUs, if the scratch holds one energy row per item
+  EllParts parts{scratch, 1};
+  const int tiles = (p.g * p.qtile + 31) / 32;
+  if (scratch && (p.ssplits > 1 || (p.ssplits == 0 && units * 2 <= cus))) {
+    int n = (int)std::min<int64_t>(tiles, p.ssplits > 0 ? p.ssplits : (cus + units - 1) / units);
+    while (n > 1 && (size_t)(units * n) * (size_t)p.nbk > scratch_floats) --n;
+    parts.n = std::max(1, n);
+  }
+  const unsigned grid = (unsigned)std::min<int64_t>(units * parts.n, cus);
   const size_t smem = (size_t)p.nbk * sizeof(float);
   switch (p.g) {
-    case 1: estimate_kernel<FP8, 1><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
-    case 2: estimate_kernel<FP8, 2><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
-    case 4: estimate_kernel<FP8, 4><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
-    case 8: estimate_kernel<FP8, 8><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl); break;
+    case 1: estimate_kernel<FP8, 1><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); break;
+    case 2: estimate_kernel<FP8, 2><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); break;
+    case 4: estimate_kernel<FP8, 4><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); break;
+    case 8: estimate_kernel<FP8, 8><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); break;
     default: return hipErrorInvalidValue;
   }
+  if (parts.n > 1) select_kernel<<<(unsigned)units, kThreads, smem, s>>>(p, mask, kl, parts);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_estimate(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
-                           hipStream_t s) {
+                           hipStream_t s, float* scratch, size_t scratch_floats) {
   if (p.batch == 0 || p.nbmax == 0) return hipSuccess;
-  return p.fp8 ? launch_est_dt<1>(p, pooled, mask, kl, s) : launch_est_dt<0>(p, pooled, mask, kl, s);
+  return p.fp8 ? launch_est_dt<1>(p, pooled, mask, kl, scratch, scratch_floats, s)
+               : launch_est_dt<0>(p, pooled, mask, kl, scratch, scratch_floats, s);
 }
 
 hipError_t launch_compact(const Problem& p, const uint8_t* mask, KeptLists kl, hipStream_t s) {

@@ -27,6 +27,7 @@ struct Problem {
   int32_t nbk;              // key blocks per sequence bound (mask columns, pooled rows)
   int32_t sink, window, recent, corr;
   int32_t splits;           // KV splits: 0 = cost-balanced plan, n >= 1 = n per unit
+  int32_t ssplits;          // scoring row parts: 0 = automatic, n >= 1 = at most n
   float alpha;
   float scale_log2;         // softmax_scale * log2(e)
   int32_t fp8;
@@ -83,7 +84,7 @@ int device_compute_units();
 hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s,
                        const MeansCache& cache = MeansCache{nullptr, nullptr, nullptr, 0});
 hipError_t launch_estimate(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,
-                           hipStream_t s);
+                           hipStream_t s, float* scratch = nullptr, size_t scratch_floats = 0);
 hipError_t launch_compact(const Problem& p, const uint8_t* mask, KeptLists kl, hipStream_t s);
 hipError_t launch_plan(const Problem& p, const KeptLists& kl, const Plan& plan, hipStream_t s);
 hipError_t launch_attend(const Problem& p, const Pooled& pooled, const uint8_t* mask,

@@ -260,14 +260,26 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan plan,
     float lt = wgt * l;
     for (int o = 16; o > 0; o >>= 1) lt += __shfl_xor(lt, o, 32);
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int u = 0; u < U; ++u) {
-      const float wu = __shfl(wgt, u, 32);
-      if (wu == 0.f) continue;
-      const float4 o = *(const float4*)(plan.part_o + ((int64_t)(slot0 + u) * rpu + pr) * kHeadDim + c);
-      acc.x = fmaf(wu, o.x, acc.x);
-      acc.y = fmaf(wu, o.y, acc.y);
-      acc.z = fmaf(wu, o.z, acc.z);
-      acc.w = fmaf(wu, o.w, acc.w);
+    for (int u0 = 0; u0 < U; u0 += 4) {   // four parts' loads in flight at a time
+      float wu[4];
+      float4 o[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int u = u0 + k;
+        wu[k] = __shfl(wgt, u & 31, 32);
+        o[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (u < U && wu[k] != 0.f)
+          o[k] = *(const float4*)(plan.part_o + ((int64_t)(slot0 + u) * rpu + pr) * kHeadDim + c);
+        else
+          wu[k] = 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        acc.x = fmaf(wu[k], o[k].x, acc.x);
+        acc.y = fmaf(wu[k], o[k].y, acc.y);
+        acc.z = fmaf(wu[k], o[k].z, acc.z);
+        acc.w = fmaf(wu[k], o[k].w, acc.w);
+      }
     }
     const float inv = (FP8 ? p.v_scale[h] : 1.f) / lt;
     const int hq = h * G + pr % G;

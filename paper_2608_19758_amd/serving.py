@@ -56,6 +56,7 @@ class BackendConfig:
     kv_splits: int = 0             # 0: cost-balanced plan on the device
     softmax_scale: float = 0.0     # <= 0: 1/sqrt(128)
     query_tile_rows: int = 0       # 0: query blocks of 128 positions; 128: 128-row tiles
+    score_splits: int = 0          # 0: rows of few units split over workgroups; 1: never
 
     @property
     def max_pages_per_seq(self) -> int:
@@ -69,7 +70,8 @@ class BackendConfig:
             sink_blocks=self.sink_blocks, window_blocks=self.window_blocks,
             recent_blocks=self.recent_blocks, mean_correction=int(self.mean_correction),
             softmax_scale=self.softmax_scale, dtype=self.dtype, max_kv_len=max_kv,
-            kv_splits=self.kv_splits, query_tile_rows=self.query_tile_rows)
+            kv_splits=self.kv_splits, query_tile_rows=self.query_tile_rows,
+            score_splits=self.score_splits)
 
     def worst_case_params(self) -> "fp2.Params":
         return self.params(self.max_batch, self.max_extend_len, self.max_kv_len)

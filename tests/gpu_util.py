@@ -20,7 +20,7 @@ LSE_TOL = {"bf16": 1e-2, "fp8": 0.0625}
 
 
 def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=0.0, kv_splits=0,
-               query_tile_rows=0):
+               query_tile_rows=0, score_splits=0):
     sp = wl.spec
     return fp2.make_params(
         batch=sp.batch, num_q_heads=sp.num_q_heads, num_kv_heads=sp.num_kv_heads,
@@ -31,7 +31,7 @@ def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=
         mean_correction=sp.mean_correction if corr is None else corr,
         softmax_scale=scale, dtype=sp.dtype,
         max_kv_len=sp.max_kv_len if sp.prefix is not None else 0, kv_splits=kv_splits,
-        query_tile_rows=query_tile_rows)
+        query_tile_rows=query_tile_rows, score_splits=score_splits)
 
 
 def device_tensors(wl):

@@ -72,6 +72,8 @@ def call_prefill(p, **over):
     (dict(num_q_heads=48, num_kv_heads=8), fp2.EUNSUPPORTED),      # g = 6
     (dict(num_q_heads=128, num_kv_heads=8), fp2.EUNSUPPORTED),     # g = 16
     (dict(head_dim=64), fp2.EUNSUPPORTED),
+    (dict(score_splits=-1), fp2.EINVAL),
+    (dict(score_splits=65), fp2.EINVAL),
     (dict(head_dim=0), fp2.EINVAL),
     (dict(block_size=64), fp2.EUNSUPPORTED),
     (dict(page_size=-1), fp2.EINVAL),

@@ -158,8 +158,8 @@ def test_chunk_equals_whole_on_gpu(case, alpha):
     print("chunk case", kv, pre, case, alpha, flush=True)
     whole = synth.generate(spec(kv, None, **case))
     chunk = synth.generate(spec([L - P for L, P in zip(kv, pre)], pre, **case))
-    ow, mw, lw = gu.gpu_prefill(whole, gu.params_for(whole, alpha, kv_splits=1))
-    oc, mc, lc = gu.gpu_prefill(chunk, gu.params_for(chunk, alpha, kv_splits=1))
+    ow, mw, lw = gu.gpu_prefill(whole, gu.params_for(whole, alpha, kv_splits=1, score_splits=1))
+    oc, mc, lc = gu.gpu_prefill(chunk, gu.params_for(chunk, alpha, kv_splits=1, score_splits=1))
     B = whole.spec.block_size
     for b, (L, P) in enumerate(zip(kv, pre)):
         rw = slice(int(whole.cu_seqlens[b]) + P, int(whole.cu_seqlens[b + 1]))
@@ -182,8 +182,8 @@ def test_chunked_prefill_fullsize_sampled():
     whole = synth.generate(base)
     chunk = synth.generate(base.replace(seqlens=[L - P], prefix=[P]))
     print("chunk of %d after prefix %d, alpha %g" % (L - P, P, alpha), flush=True)
-    o1, m1, l1 = gu.gpu_prefill(chunk, gu.params_for(chunk, alpha, kv_splits=1))
-    ow, mw, lw = gu.gpu_prefill(whole, gu.params_for(whole, alpha, kv_splits=1))
+    o1, m1, l1 = gu.gpu_prefill(chunk, gu.params_for(chunk, alpha, kv_splits=1, score_splits=1))
+    ow, mw, lw = gu.gpu_prefill(whole, gu.params_for(whole, alpha, kv_splits=1, score_splits=1))
     B = base.block_size
     np.testing.assert_array_equal(m1[0], mw[0, :, P // B:, :])
     np.testing.assert_array_equal(o1, ow[P:])

@@ -39,7 +39,7 @@ def test_backend_chunked_forwards(dtype, kv_splits, cache):
     cfg = serving.BackendConfig(num_q_heads=8, num_kv_heads=2, page_size=64, max_batch=2,
                                 max_extend_len=1024, max_kv_len=2048, dtype=dtype, alpha=ALPHA,
                                 sink_blocks=sp.sink_blocks, window_blocks=sp.window_blocks,
-                                kv_splits=kv_splits)
+                                kv_splits=kv_splits, score_splits=1)
     be = serving.PrefillBackend(cfg)
     dev = [gu.device_tensors(wl) for wl in layers]
     # the engine's page table: the workload's, widened to the configured stride
@@ -48,7 +48,7 @@ def test_backend_chunked_forwards(dtype, kv_splits, cache):
     for wl in layers[1:]:
         assert np.array_equal(wl.block_table, layers[0].block_table)
     # reference: one whole-sequence call per layer, without splits
-    ref = [gu.gpu_prefill(wl, gu.params_for(wl, ALPHA, kv_splits=1)) for wl in layers]
+    ref = [gu.gpu_prefill(wl, gu.params_for(wl, ALPHA, kv_splits=1, score_splits=1)) for wl in layers]
     cu = layers[0].cu_seqlens
     forwards = [(CHUNK1, [0, 0]), ([k - c for k, c in zip(KV, CHUNK1)], CHUNK1)]
     caches = [be.alloc_means_cache(layers[0].num_pages) if cache else None for _ in layers]
