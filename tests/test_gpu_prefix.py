@@ -209,3 +209,25 @@ def test_chunked_prefill_fullsize_sampled():
         assert np.abs(lc[rs, hs] - olse[rs, hs]).max() <= gu.LSE_TOL["fp8"]
     print("same-mask max-abs err on sampled units %.3g" % worst)
     assert worst <= gu.TOL["fp8"]
+
+
+@pytest.mark.parametrize("name", ["bf16_paged_ragged", "fp8_unaligned", "g1_paged"])
+@pytest.mark.parametrize("ss", [1, 3, 5, 64])
+def test_score_splits_parity(name, ss):
+    """The scoring with its query rows split into at most `ss` parts per unit
+    (uneven and empty parts included) against the oracle; the same bars as
+    the prefill parity, and the kept lists agree with the mask."""
+    wl = _wl(name)
+    sp = wl.spec
+    alpha = 0.98
+    out, gmask, lse = gu.gpu_prefill(wl, gu.params_for(wl, alpha, score_splits=ss))
+    inp = oracle.Inputs(wl)
+    op = gu.oracle_params(inp, alpha)
+    omask, ell, mu = oracle.estimate(inp, op, want_scores=True)
+    ob, ibm, ib = gu.compare_masks(gmask, omask, ell, mu, alpha, gu.units_of(wl))
+    print("score_splits %d: mask outside-band mismatches %d, in-band %d of %d" % (ss, ob, ibm, ib))
+    assert ob == 0
+    oout, olse = oracle.attend(inp, op, gmask)
+    err = np.abs(out - oout).max() if out.size else 0.0
+    assert err <= gu.TOL[sp.dtype]
+    assert (np.abs(lse - olse).max() if lse.size else 0.0) <= gu.LSE_TOL[sp.dtype]
