@@ -133,6 +133,49 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes": n, "copies": 3}), flush=True)
 
 
+def measured_peaks():
+    """Reference rates measured on this GPU in the same run: a 1 GiB device
+    copy (bytes read + written per second), and the library GEMMs (hipBLASLt
+    through torch) at 8192^3 in bf16 and fp8 e4m3 -- what a dense contraction
+    reaches here, next to the vendor peaks the roofline uses."""
+    import torch
+
+    def timed(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+
+    res = {}
+    n = 1 << 30
+    x = torch.empty(n, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    res["copy_gbs"] = round(2 * n / timed(lambda: y.copy_(x)) / 1e9, 1)
+    del x, y
+    m = 8192
+    a = torch.randn(m, m, device="cuda", dtype=torch.bfloat16)
+    bt = torch.randn(m, m, device="cuda", dtype=torch.bfloat16)
+    res["gemm_bf16_tflops"] = round(2 * m ** 3 / timed(lambda: a @ bt) / 1e12, 1)
+    try:
+        a8 = a.to(torch.float8_e4m3fn)
+        b8 = bt.to(torch.float8_e4m3fn).t().contiguous().t()
+        one = torch.ones((), device="cuda", dtype=torch.float32)
+        res["gemm_fp8_tflops"] = round(2 * m ** 3 / timed(
+            lambda: torch._scaled_mm(a8, b8, scale_a=one, scale_b=one,
+                                     out_dtype=torch.bfloat16)) / 1e12, 1)
+    except Exception as e:   # the fp8 GEMM path may be missing from this torch build
+        res["gemm_fp8_tflops"] = None
+        print("[bench] fp8 GEMM reference unavailable: %s" % e, file=sys.stderr, flush=True)
+    del a, bt
+    torch.cuda.empty_cache()
+    return res
+
+
 def setup(name, target, correction=None, tile_rows=0):
     import torch
     import numpy as np  # noqa: F401
@@ -411,6 +454,8 @@ def main():
         print("[bench] cpu baseline: %s" % cpu["sample"], file=sys.stderr, flush=True)
 
     chunk_res = chunked(cfg, args.steps, args.warmup) if args.chunked else None
+    peaks = measured_peaks()
+    print("[bench] measured on this GPU: %s" % json.dumps(peaks), file=sys.stderr, flush=True)
 
     variants = []
     if args.variants:
@@ -487,6 +532,8 @@ def main():
                        "traffic_unit": "GB per call",
                        "measured_gbs": None if etraffic is None
                        else round(etraffic / 1e9 / (m["estimate_ms"] / 1e3), 1)},
+        # reference rates measured in this run (device copy, library GEMMs)
+        "measured_peaks": peaks,
         "cpu_baseline": None if cpu is None else {k: (round(v, 6) if isinstance(v, float) else v)
                                                   for k, v in cpu.items() if k != "seconds"},
     }

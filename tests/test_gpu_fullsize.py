@@ -3,7 +3,8 @@ checked against the oracle on sampled (sequence, KV head, query block) units
 that the oracle computes one by one, plus properties that hold at any size:
 every output finite, forced-block bits exact for every block, rows past a
 sequence zero, and the kept ratio equal to the oracle-calibrated one up to
-blocks inside the margin band."""
+blocks inside the margin band. The error against dense attention (every
+block kept) on four of the sampled units is reported beside the same-mask error."""
 import numpy as np
 import pytest
 
@@ -56,6 +57,21 @@ def test_fullsize_sampled_parity(name, target):
         assert np.abs(lse[rs, hs] - olse[rs, hs]).max() <= gu.LSE_TOL[sp.dtype]
     print("same-mask max-abs err on sampled units %.3g (tol %g)" % (worst, gu.TOL[sp.dtype]))
     assert worst <= gu.TOL[sp.dtype]
+    # reported next to it: the error of the sparse output against dense
+    # attention (every block kept, the oracle at alpha = 0) on four of the units
+    du = units[::4]
+    op0 = gu.oracle_params(inp, 0.0)
+    dmask = oracle.estimate(inp, op0, units=du)
+    dout, _ = oracle.attend(inp, op0, dmask, units=du)
+    dworst, num, den = 0.0, 0.0, 0.0
+    for rs, hs in gu.unit_rows(wl, du):
+        diff = out[rs, hs] - dout[rs, hs]
+        dworst = max(dworst, float(np.abs(diff).max()))
+        num += float((diff ** 2).sum())
+        den += float((dout[rs, hs] ** 2).sum())
+    print("vs dense attention on %d units: max-abs err %.3g, relative Frobenius %.3g "
+          "(same-mask max-abs %.3g)" % (len(du), dworst, (num / max(den, 1e-300)) ** 0.5, worst))
+    assert np.isfinite(dworst)
     kept = oracle.kept_ratio(gmask, sp.seqlens, B)
     want = synth.alphas()[name]["kept_ratio"][target]
     tot = sum((L + B - 1) // B * ((L + B - 1) // B + 1) // 2 for L in sp.seqlens) * sp.num_kv_heads
