@@ -13,6 +13,10 @@
  *                  max-based thresholding, forced blocks, kept-block lists.
  *   fp2_attend   = the attention stage only, under a caller-given mask.
  *   fp2_pool     = the block means alone (exposed for verification).
+ *   fp2_prefill_cached = fp2_prefill with block means kept across calls
+ *                  (chunked prefill); fp2_means_cache_slots sizes the cache.
+ *   fp2_mask_to_csr = a mask as the CSR index of 64-token key tiles;
+ *                  fp2_csr_capacity sizes it.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -46,7 +50,9 @@
  * L_kv = L_q (P = 0, Ja = Jb = I). The selection of a query block depends
  * only on its own rows and the keys before them, so with P a multiple of
  * block_size a chunked prefill gives, row for row, the output of one call
- * over the whole sequence.
+ * over the whole sequence (bit for bit with kv_splits == 1 and
+ * score_splits == 1, whose work splitting does not depend on the call's
+ * size; else up to rounding).
  *
  * KV splits and the work plan (Sec. 3.3 Eq. split and Eq. cost)
  * --------------------------------------------------------------
@@ -193,7 +199,9 @@ typedef struct {
  * and their counts, the attention work plan with its work counter (rebuilt
  * by every call, so a workspace can be reused without clearing) and the
  * partial outputs of split units (520 bytes per packed query row: 34 MB for
- * kv_splits == 0, n x 520 bytes per packed row of the problem for n > 1). */
+ * kv_splits == 0, n x 520 bytes per packed row of the problem for n > 1),
+ * which the row-split scoring also uses as its scratch before the attention
+ * (it falls back to fewer parts when they do not fit). */
 size_t fp2_workspace_bytes(const fp2_params_t* params);
 
 /* Full prefill (Algorithm 1 of Sec. 3.4): block means, fused scoring and
