@@ -4,15 +4,17 @@
 // A persistent grid (one 8-wave workgroup per compute unit) deals the units
 // (sequence b, KV head h, query block I) round-robin, heaviest (largest I)
 // first. The query rows of block I are the g*B packed rows of Eq. packgqa
-// (position I*B + r/g, head h*g + r%g). They stream through two LDS buffers
-// in 32-row tiles, the global loads running two tiles ahead; each wave keeps up to four 32-wide chunks of pooled keys khat
-// in registers (the MFMA B operand) and computes S = Q khat^T with
-// v_mfma_f32_32x32x16_bf16 (fp32 accumulation). Lane l of the accumulator
-// owns key block J = chunk + l%32 and 16 query rows, so the row sum of
-// exp2(S * scale*log2e - m) for its block is a per-lane running sum with a
-// per-lane running maximum m (the per-(I,J) maximum of Eq. (1), no
-// cross-lane traffic). At the end the two lane halves and the running maxima
-// are merged into ell_J = log2 E_J.
+// (position I*B + r/g, head h*g + r%g). They stream through LDS in pairs of
+// 32-row tiles (one barrier per pair), the global loads one pair ahead; each
+// wave keeps up to four 32-wide chunks of pooled keys khat in registers (the
+// MFMA B operand) and computes S = Q khat^T with v_mfma_f32_32x32x16_bf16
+// (fp32 accumulation). Lane l of the accumulator owns key block J = chunk +
+// l%32 and 16 query rows, so the row sum of exp2(S * scale*log2e - m) for its
+// block is a per-lane running sum with a per-lane offset m (the role of the
+// per-(I,J) maximum of Eq. (1), moved only when a tile's sum would leave a
+// safe range; no cross-lane traffic). At the end the two lane halves are
+// merged into ell_J = log2 E_J. Calls with few units split a unit's tiles
+// over several workgroups (EllParts) and merge the parts in select_kernel.
 //
 // Selection (Eq. select): J is kept iff alpha == 0, ell_J >= max_J ell +
 // log2(alpha), or J is forced (sink, window incl. diagonal, recent). The mask
