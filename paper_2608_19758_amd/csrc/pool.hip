@@ -75,10 +75,10 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out, M
     }
   };
   const int cnt = min(kBlock, L - J * kBlock);
-  __shared__ double redk[16][kHeadDim];
-  __shared__ double redv[16][kHeadDim];
 
-  if (!FP8) {
+  if constexpr (!FP8) {
+    __shared__ double redk[16][kHeadDim];
+    __shared__ double redv[16][kHeadDim];
     const int c = tid & 15, rg = tid >> 4;
     double ak[8], av[8];
 #pragma unroll
@@ -174,21 +174,30 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out, M
       ak[i] = (int)(fk[i] * 512.f);
       av[i] = (int)(fv[i] * 512.f);
     }
-    // integer partial sums are exact in fp64
-    int* redki = (int*)&redk[0][0];
-    int* redvi = (int*)&redv[0][0];
+    // integer sums (exact): over the wave's 8 row groups with lane
+    // exchanges, then over the 4 waves through LDS (4 KiB, so LDS does not
+    // bound the workgroups per CU)
+    __shared__ int redki[4][kHeadDim];
+    __shared__ int redvi[4][kHeadDim];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      redki[rg * kHeadDim + c * 16 + i] = ak[i];
-      redvi[rg * kHeadDim + c * 16 + i] = av[i];
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+      for (int o = 8; o < 64; o <<= 1) {
+        ak[i] += __shfl_xor(ak[i], o, 64);
+        av[i] += __shfl_xor(av[i], o, 64);
+      }
+    const int w = tid >> 6;
+    if ((tid & 63) < 8) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        redki[w][c * 16 + i] = ak[i];
+        redvi[w][c * 16 + i] = av[i];
+      }
     }
     __syncthreads();
     if (tid < kHeadDim) {
-      int sk = 0, sv = 0;
-      for (int g = 0; g < 32; ++g) {
-        sk += redki[g * kHeadDim + tid];
-        sv += redvi[g * kHeadDim + tid];
-      }
+      const int sk = (redki[0][tid] + redki[1][tid]) + (redki[2][tid] + redki[3][tid]);
+      const int sv = (redvi[0][tid] + redvi[1][tid]) + (redvi[2][tid] + redvi[3][tid]);
       double ks = (double)p.k_scale[h], vs = (double)p.v_scale[h];
       store(f64_to_bf16(((double)sk * 0x1p-9 * ks) / (double)cnt),
             f64_to_bf16(((double)sv * 0x1p-9 * vs) / (double)cnt));
