@@ -135,10 +135,13 @@ def copy_calibration():
 
 def measured_peaks():
     """Reference rates measured on this GPU in the same run: a 1 GiB device
-    copy (bytes read + written per second), and the library GEMMs (hipBLASLt
-    through torch) at 8192^3 in bf16 and fp8 e4m3 -- what a dense contraction
-    reaches here, next to the vendor peaks the roofline uses."""
+    copy (bytes read + written per second); the library's MFMA and exp loops
+    (fp2_calibrate: the matrix instructions the kernels issue, and v_exp_f32,
+    on every SIMD with no memory traffic); and the library GEMMs (hipBLASLt
+    through torch) at 8192^3 in bf16 and fp8 e4m3 -- next to the vendor peaks
+    the roofline uses."""
     import torch
+    import paper_2608_19758_amd as fp2
 
     def timed(fn, reps=5):
         fn()
@@ -157,6 +160,12 @@ def measured_peaks():
     y = torch.empty_like(x)
     res["copy_gbs"] = round(2 * n / timed(lambda: y.copy_(x)) / 1e9, 1)
     del x, y
+    sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    for key, kind, iters, unit in (("mfma_bf16_tflops", "mfma_bf16", 50000, 1e12),
+                                   ("mfma_fp8_tflops", "mfma_fp8", 25000, 1e12),
+                                   ("exp_per_s", "exp", 25000, 1.0)):
+        ops = fp2.calibrate(kind, iters, sink)
+        res[key] = float("%.4g" % (ops / timed(lambda: fp2.calibrate(kind, iters, sink)) / unit))
     m = 8192
     a = torch.randn(m, m, device="cuda", dtype=torch.bfloat16)
     bt = torch.randn(m, m, device="cuda", dtype=torch.bfloat16)

@@ -17,6 +17,7 @@
  *                  (chunked prefill); fp2_means_cache_slots sizes the cache.
  *   fp2_mask_to_csr = a mask as the CSR index of 64-token key tiles;
  *                  fp2_csr_capacity sizes it.
+ *   fp2_calibrate = MFMA and exp rate loops (measurement helper).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -324,6 +325,30 @@ fp2_status_t fp2_mask_to_csr(const fp2_params_t* params, const int32_t* cu_seqle
                              const int32_t* cu_seqlens_k_host, const uint8_t* block_mask,
                              int32_t* csr_offsets, int32_t* csr_indices, size_t capacity,
                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Rate calibration: a measurement helper, not a step of the method. It runs
+ * one fixed instruction loop on every compute unit (two workgroups of four
+ * waves each, so two waves per SIMD, each wave with independent chains) and
+ * sets *ops to the operations the launch performs, so that the caller's
+ * timing of `stream` gives the rate this GPU sustains -- the measured
+ * counterpart of the vendor peaks a roofline uses:
+ *   FP2_CALIB_MFMA_BF16  v_mfma_f32_32x32x16_bf16 (the bf16 attention, the
+ *                        correction and the block scoring), 32768 FLOP each;
+ *   FP2_CALIB_MFMA_FP8   v_mfma_f32_32x32x64_f8f6f4 on e4m3 codes (the fp8
+ *                        attention), 131072 FLOP each;
+ *   FP2_CALIB_EXP        v_exp_f32 (the softmax and scoring exponentials),
+ *                        64 exps each.
+ * iters: loop trips per wave, 1 .. 2^24 (each trip is 4 MFMAs per wave, or
+ * 32 exps per lane). sink: one device float, written only if a loop yields a
+ * value it never does (it keeps the loop's results live). ops: host double.
+ * FP2_EINVAL for an unknown kind, iters out of range or a null pointer. */
+typedef enum {
+  FP2_CALIB_MFMA_BF16 = 0,
+  FP2_CALIB_MFMA_FP8 = 1,
+  FP2_CALIB_EXP = 2
+} fp2_calib_kind_t;
+fp2_status_t fp2_calibrate(fp2_calib_kind_t kind, int32_t iters, float* sink, double* ops,
+                           void* stream);
 
 /* Static description of a status code. */
 const char* fp2_status_str(fp2_status_t status);

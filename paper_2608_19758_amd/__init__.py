@@ -49,7 +49,9 @@ class Params(ctypes.Structure):
 
 EXPORTS = ["fp2_workspace_bytes", "fp2_prefill", "fp2_estimate", "fp2_attend", "fp2_pool",
            "fp2_csr_capacity", "fp2_mask_to_csr", "fp2_means_cache_slots", "fp2_prefill_cached",
-           "fp2_status_str", "fp2_last_error"]
+           "fp2_calibrate", "fp2_status_str", "fp2_last_error"]
+
+CALIB_KINDS = {"mfma_bf16": 0, "mfma_fp8": 1, "exp": 2}
 
 
 class MeansCache(ctypes.Structure):
@@ -86,6 +88,8 @@ def lib():
         L.fp2_prefill_cached.restype = ctypes.c_int
         L.fp2_prefill_cached.argtypes = [P] + [vp] * 11 + [ctypes.POINTER(MeansCache)] + \
             [vp] * 4 + [ctypes.c_size_t, vp]
+        L.fp2_calibrate.restype = ctypes.c_int
+        L.fp2_calibrate.argtypes = [ctypes.c_int, ctypes.c_int32, vp, ctypes.POINTER(ctypes.c_double), vp]
         L.fp2_status_str.restype = ctypes.c_char_p
         L.fp2_status_str.argtypes = [ctypes.c_int]
         L.fp2_last_error.restype = ctypes.c_char_p
@@ -290,6 +294,22 @@ def pool(p: Params, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_seqlen
 
 def csr_capacity(p: Params) -> int:
     return int(lib().fp2_csr_capacity(ctypes.byref(p)))
+
+
+def calibrate(kind: str, iters: int, sink=None, stream=None) -> float:
+    """fp2_calibrate: enqueue one rate-calibration loop ("mfma_bf16",
+    "mfma_fp8" or "exp") and return the operations it performs (FLOP or
+    exps); time it on the stream to get the rate. sink: a device float32
+    tensor of at least one element (allocated when None)."""
+    if kind not in CALIB_KINDS:
+        raise ValueError("calibration kind %r not in %s" % (kind, sorted(CALIB_KINDS)))
+    if sink is None:
+        sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    ops = ctypes.c_double(0.0)
+    st = lib().fp2_calibrate(CALIB_KINDS[kind], int(iters), _ptr(sink), ctypes.byref(ops),
+                             _stream(stream))
+    _check("fp2_calibrate", st)
+    return ops.value
 
 
 def mask_to_csr(p: Params, block_mask, cu_seqlens, *, cu_seqlens_k=None, cu_seqlens_host=None,

@@ -11,7 +11,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libfp2.so")
-SOURCES = ["api.hip", "pool.hip", "estimate.hip", "attend.hip", "schedule.hip", "index.hip"]
+SOURCES = ["api.hip", "pool.hip", "estimate.hip", "attend.hip", "schedule.hip", "index.hip",
+           "calib.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -480,6 +480,16 @@ fp2_status_t fp2_mask_to_csr(const fp2_params_t* params, const int32_t* cu_seqle
                     "fp2_mask_to_csr launch");
 }
 
+fp2_status_t fp2_calibrate(fp2_calib_kind_t kind, int32_t iters, float* sink, double* ops,
+                           void* stream) {
+  if (kind != FP2_CALIB_MFMA_BF16 && kind != FP2_CALIB_MFMA_FP8 && kind != FP2_CALIB_EXP)
+    return fail(FP2_EINVAL, "unknown calibration kind %d", (int)kind);
+  if (iters < 1 || iters > (1 << 24)) return fail(FP2_EINVAL, "iters %d outside [1, 2^24]", iters);
+  if (!sink || !ops) return fail(FP2_EINVAL, "sink or ops is null");
+  return hip_status(fp2::launch_calib((int)kind, iters, sink, ops, (hipStream_t)stream),
+                    "fp2_calibrate launch");
+}
+
 const char* fp2_status_str(fp2_status_t status) {
   switch (status) {
     case FP2_OK: return "ok";

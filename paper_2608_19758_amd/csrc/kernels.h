@@ -81,6 +81,10 @@ int attend_items_per_unit(int g, int qtile);
 // Compute units of the current device (0 if it cannot be queried).
 int device_compute_units();
 
+// Rate-calibration loops (calib.hip): kind is an fp2_calib_kind_t; *ops gets
+// the operations of the launch (FLOP or exps).
+hipError_t launch_calib(int kind, int iters, float* sink, double* ops, hipStream_t s);
+
 hipError_t launch_pool(const Problem& p, Pooled out, hipStream_t s,
                        const MeansCache& cache = MeansCache{nullptr, nullptr, nullptr, 0});
 hipError_t launch_estimate(const Problem& p, const Pooled& pooled, uint8_t* mask, KeptLists kl,

@@ -230,3 +230,16 @@ def test_means_cache_slots_and_validation():
     assert "pooled_blocks" in fp2.last_error()
     assert cached(ctypes.byref(fp2.MeansCache(0x100008, FAKE.value, FAKE.value))) == fp2.EINVAL
     assert "aligned" in fp2.last_error()
+
+
+def test_calibrate_rejects_bad_arguments():
+    L = fp2.lib()
+    ops = ctypes.c_double(0.0)
+    sink = ctypes.c_void_p(16)   # never dereferenced: every call below fails validation
+    for kind, iters, s, o in [(3, 10, sink, ctypes.byref(ops)), (-1, 10, sink, ctypes.byref(ops)),
+                              (0, 0, sink, ctypes.byref(ops)), (1, (1 << 24) + 1, sink, ctypes.byref(ops)),
+                              (2, 10, None, ctypes.byref(ops)), (0, 10, sink, None)]:
+        assert L.fp2_calibrate(kind, iters, s, o, None) == fp2.EINVAL
+        assert fp2.last_error()
+    with pytest.raises(ValueError):
+        fp2.calibrate("mfma_fp4", 10)
