@@ -305,6 +305,9 @@ def calibrate(kind: str, iters: int, sink=None, stream=None) -> float:
         raise ValueError("calibration kind %r not in %s" % (kind, sorted(CALIB_KINDS)))
     if sink is None:
         sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    if not (isinstance(sink, torch.Tensor) and sink.is_cuda and sink.dtype == torch.float32
+            and sink.numel() >= 1):
+        raise ValueError("sink must be a CUDA float32 tensor of at least one element")
     ops = ctypes.c_double(0.0)
     st = lib().fp2_calibrate(CALIB_KINDS[kind], int(iters), _ptr(sink), ctypes.byref(ops),
                              _stream(stream))

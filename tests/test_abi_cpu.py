@@ -7,6 +7,7 @@ import re
 
 import numpy as np
 import pytest
+import torch
 
 import paper_2608_19758_amd as fp2
 
@@ -243,3 +244,5 @@ def test_calibrate_rejects_bad_arguments():
         assert fp2.last_error()
     with pytest.raises(ValueError):
         fp2.calibrate("mfma_fp4", 10)
+    with pytest.raises(ValueError):   # a host tensor never reaches the kernel
+        fp2.calibrate("exp", 10, sink=torch.zeros(1))
