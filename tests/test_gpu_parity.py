@@ -171,3 +171,32 @@ def test_empty_and_degenerate():
     oout, _ = oracle.attend(inp, op, omask)
     assert np.abs(out - oout).max() <= 2e-2
     del e, ws
+
+
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2), (8, 2), (16, 2)], ids=lambda v: str(v))
+def test_packgqa_rows_map_one_to_one(hq, hkv):
+    """Eq. packgqa, exhaustively on small inputs: with every causal block kept
+    (alpha = 0), each output row (position, query head) is nearest to the
+    oracle's row of that same position and head among all rows of the call,
+    so packed row r of block I of KV head h reaches exactly (I*B + r // g,
+    h*g + r % g) -- a swapped head or position would land on another row."""
+    lens = [5, 130, 257]
+    print("packgqa case hq %d hkv %d lens %s" % (hq, hkv, lens), flush=True)
+    wl = synth.generate(spec(lens, hq=hq, hkv=hkv, page=16, order="permuted", seed=17))
+    out, _, _ = gu.gpu_prefill(wl, gu.params_for(wl, 0.0))
+    inp = oracle.Inputs(wl)
+    op = gu.oracle_params(inp, 0.0)
+    oout, _ = oracle.attend(inp, op, oracle.estimate(inp, op))
+    g_rows = out.reshape(-1, 128).astype(np.float64)
+    o_rows = oout.reshape(-1, 128)
+    # squared distances between every GPU row and every oracle row
+    d2 = (g_rows ** 2).sum(1)[:, None] - 2 * g_rows @ o_rows.T + (o_rows ** 2).sum(1)[None, :]
+    # rows the method makes equal (e.g. position 0 of every head of a group
+    # sees key 0 alone) are interchangeable: compare only against rows that
+    # differ from the row's own oracle output
+    od2 = (o_rows ** 2).sum(1)[:, None] - 2 * o_rows @ o_rows.T + (o_rows ** 2).sum(1)[None, :]
+    same = od2 <= 1e-12
+    own = np.diag(d2)
+    others = np.where(same, np.inf, d2).min(axis=1)
+    print("rows %d, interchangeable pairs %d" % (len(own), int(same.sum()) - len(own)))
+    assert (own < others).all()
