@@ -368,14 +368,28 @@ def chunked(cfg, steps, warmup):
                                   **kw)
             meta = be.init_forward_metadata([T], [L - T], table(be, 1),
                                             cached_prefix_lens=None if mc is None else [L - T])
-            r[key] = round(time_loop(lambda: be.forward_extend(q, d["k_cache"], d["v_cache"], meta,
-                                                               out=out, means_cache=mc, **kw),
-                                     steps, warmup)[0], 4)
+            fwd = lambda: be.forward_extend(q, d["k_cache"], d["v_cache"], meta, out=out,   # noqa: E731
+                                            means_cache=mc, **kw)
+            r[key] = round(time_loop(fwd, steps, warmup)[0], 4)
+            if mc is not None:
+                # the same forward captured once in a HIP graph and replayed
+                side = torch.cuda.Stream()
+                side.wait_stream(torch.cuda.current_stream())
+                with torch.cuda.stream(side):
+                    fwd()
+                torch.cuda.current_stream().wait_stream(side)
+                torch.cuda.synchronize()
+                graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(graph):
+                    fwd()
+                r[key + "_graph"] = round(time_loop(graph.replay, steps, warmup)[0], 4)
+                del graph
             del be, mc
         res["tails"].append(r)
         print("[bench] tail %d: planned splits %.3f ms, none %.3f ms, planned + means cache %.3f ms"
-              % (T, r["ms_planned_splits"], r["ms_no_splits"], r["ms_planned_splits_means_cache"]),
-              file=sys.stderr, flush=True)
+              " (%.3f ms replayed from a HIP graph)"
+              % (T, r["ms_planned_splits"], r["ms_no_splits"], r["ms_planned_splits_means_cache"],
+                 r["ms_planned_splits_means_cache_graph"]), file=sys.stderr, flush=True)
     # four requests of the same sequence data at different stages of their
     # prefill, in one forward (continuous batching)
     ext, pre = [8192, 8192, 4096, 1024], [0, 32768, 90112, 130048]
