@@ -22,6 +22,7 @@
 // no key have m_u = -inf and weight 0. It is HBM-bound (U x 520 bytes read
 // and 256 written per packed row) and persistent over (split unit, 8-row
 // group) pairs.
+#include <atomic>
 #include <algorithm>
 
 #include "kernels.h"
@@ -294,16 +295,19 @@ __global__ __launch_bounds__(256) void combine_kernel(Problem p, Plan plan,
 
 }  // namespace
 
+// Compute units of the current device, queried once per device; the cache is
+// atomic so that calls from several host threads are well defined (each may
+// query and store the same value).
 int device_compute_units() {
-  static int cus[64] = {};
+  static std::atomic<int> cus[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  if (cus[dev] == 0) {
-    int n = 0;
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    cus[dev] = n;
+    cus[dev].store(n, std::memory_order_relaxed);
   }
-  return cus[dev];
+  return n;
 }
 
 hipError_t launch_plan(const Problem& p, const KeptLists& kl, const Plan& plan, hipStream_t s) {
