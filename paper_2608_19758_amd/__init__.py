@@ -201,6 +201,17 @@ def prefill(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_
     tokens of longer sequences (a prefix KV); None means no prefix.
     means_cache = (khat, vbar, pooled_blocks) device tensors calls
     fp2_prefill_cached (block means kept across calls)."""
+    if means_cache is not None:
+        kh, vb, pooled = means_cache
+        for name, t in (("khat", kh), ("vbar", vb)):
+            if not (t.is_cuda and t.dtype == torch.bfloat16 and t.dim() == 3
+                    and tuple(t.shape[1:]) == (p.num_kv_heads, p.head_dim) and t.is_contiguous()):
+                raise ValueError("means cache %s must be a contiguous CUDA bf16 tensor "
+                                 "[slots, num_kv_heads, head_dim]" % name)
+        if kh.shape[0] != vb.shape[0]:
+            raise ValueError("means cache khat and vbar hold different slot counts")
+        if not (pooled.is_cuda and pooled.dtype == torch.int32 and pooled.numel() >= p.batch):
+            raise ValueError("pooled_blocks must be a CUDA int32 tensor of batch entries")
     if out is None or block_mask is None:
         o2, m2, l2 = alloc_outputs(p, q.shape[0], q.device, want_lse and lse is None)
         out = o2 if out is None else out

@@ -246,3 +246,15 @@ def test_calibrate_rejects_bad_arguments():
         fp2.calibrate("mfma_fp4", 10)
     with pytest.raises(ValueError):   # a host tensor never reaches the kernel
         fp2.calibrate("exp", 10, sink=torch.zeros(1))
+
+
+def test_means_cache_tensors_checked_before_the_call():
+    """A means cache that is not a CUDA bf16 [slots, H_kv, 128] pair is refused
+    by the binding (host tensors here: nothing reaches the library)."""
+    p = base(batch=1)
+    q = torch.zeros(4, 32, 128, dtype=torch.bfloat16)
+    cu = torch.tensor([0, 4], dtype=torch.int32)
+    kh = torch.zeros(8, 8, 128, dtype=torch.bfloat16)
+    pooled = torch.zeros(1, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        fp2.prefill(p, q, q, q, cu, cu, means_cache=(kh, kh.clone(), pooled))
