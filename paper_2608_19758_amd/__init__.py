@@ -162,7 +162,13 @@ def workspace_bytes(p: Params) -> int:
 
 
 def _ptr(t: Optional[torch.Tensor]):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+    """Device pointer of a CUDA tensor (None passes NULL). A host tensor is
+    refused here: its address would reach a kernel as a device pointer."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a CUDA tensor, got one on %s" % t.device)
+    return ctypes.c_void_p(t.data_ptr())
 
 
 def _host_ptr(a):

@@ -258,3 +258,14 @@ def test_means_cache_tensors_checked_before_the_call():
     pooled = torch.zeros(1, dtype=torch.int32)
     with pytest.raises(ValueError):
         fp2.prefill(p, q, q, q, cu, cu, means_cache=(kh, kh.clone(), pooled))
+
+
+def test_host_tensors_refused_as_device_arguments():
+    """Device arguments must be CUDA tensors: a host tensor raises in the
+    binding (its address never reaches a kernel)."""
+    p = base(batch=1, page_size=0)
+    q = torch.zeros(4, 32, 128, dtype=torch.bfloat16)
+    kv = torch.zeros(4, 8, 128, dtype=torch.bfloat16)
+    cu = torch.tensor([0, 4], dtype=torch.int32)
+    with pytest.raises(ValueError, match="CUDA"):
+        fp2.pool(p, kv, kv, cu)
