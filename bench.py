@@ -439,8 +439,15 @@ def cpu_baseline(cfg, nunits):
         p0, p1 = I * B, min(L, (I + 1) * B)
         pos = np.arange(p0, p1)
         flops += float(g * 4 * sp.head_dim * (pos + 1).sum())
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f
+                              if ln.startswith("model name")), None)
+    except OSError:
+        pass
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s (dense-equivalent)",
-            "cores": op.nthreads, "kind": "oracle",
+            "cores": op.nthreads, "kind": "oracle", "cpu_model": cpu_model,
             "sample": "%d units (all %d KV heads x %d query blocks at an even stride, incl. the last) "
                       "of %s: estimation + attention, %.1f s" % (len(units), sp.num_kv_heads,
                                                                  len(Is), sp.name, dt),
