@@ -128,3 +128,11 @@ def compare_masks(gmask, omask, ell, mu, alpha, units):
         in_band_mis += int((mis & band).sum())
         out_band += int((mis & ~band).sum())
     return out_band, in_band_mis, in_band
+
+
+def alpha_cases(cases):
+    """(case, alpha) pairs: every alpha for bf16 cases; fp8 cases run alpha 0
+    and 0.995 only (their arithmetic differs from bf16 in the attention, not
+    in the selection, which the bf16 cases cover at every alpha)."""
+    return [(name, a) for name, c in cases.items()
+            for a in ((0.0, 0.995) if c.get("dtype") == "fp8" else (0.0, 0.97, 0.995, 2.0))]

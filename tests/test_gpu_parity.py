@@ -69,13 +69,10 @@ def test_pool_bit_exact(name):
     np.testing.assert_array_equal(gv, want_v)
 
 
-@pytest.mark.parametrize("name", BF16_CASES + FP8_CASES)
-@pytest.mark.parametrize("alpha", [0.0, 0.97, 0.995, 2.0])
+@pytest.mark.parametrize("name,alpha", gu.alpha_cases({k: CASES[k] for k in BF16_CASES + FP8_CASES}))
 def test_prefill_parity(name, alpha):
     wl = _wl(name)
     sp = wl.spec
-    if sp.dtype == "fp8" and alpha in (0.97, 2.0):
-        pytest.skip("covered by the other alphas")
     p = gu.params_for(wl, alpha)
     out, gmask, lse = gu.gpu_prefill(wl, p)
     inp = oracle.Inputs(wl)

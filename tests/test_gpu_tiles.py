@@ -49,13 +49,10 @@ def _wl(name):
     return synth.generate(spec(**c))
 
 
-@pytest.mark.parametrize("name", list(CASES))
-@pytest.mark.parametrize("alpha", [0.0, 0.97, 0.995, 2.0])
+@pytest.mark.parametrize("name,alpha", gu.alpha_cases(CASES))
 def test_tiles_prefill_parity(name, alpha):
     wl = _wl(name)
     sp = wl.spec
-    if sp.dtype == "fp8" and alpha in (0.97, 2.0):
-        pytest.skip("covered by the other alphas")
     out, gmask, lse = gu.gpu_prefill(wl, gu.params_for(wl, alpha, query_tile_rows=R))
     inp = oracle.Inputs(wl)
     op = inp.params(alpha, tile_rows=R)
