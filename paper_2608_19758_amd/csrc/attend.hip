@@ -187,9 +187,10 @@ struct Addresser {
 
 // Steps whose copies run ahead of the step being computed (at most the
 // ring depth less one). Measured on 8-wave items: three steps ahead for fp8
-// (of an 8-stage ring) and two for the bf16 steps and the correction (of a
-// 4-stage ring) are 1-2% faster than the whole ring; the latency of a step's
-// copies is covered either way. 4-wave items keep the whole (half) ring.
+// (of an 8-stage ring) and two for the correction (of a 4-stage ring) are
+// 1-2% faster than the whole ring, and the bf16 kept steps take one (set at
+// their call); the latency of a step's copies is covered either way. 4-wave
+// items keep the whole (half) ring.
 constexpr int copy_lead(int W, int FP8, int nst) {
   return W != 8 ? nst - 1 : FP8 ? 3 : 2;
 }
@@ -197,11 +198,11 @@ constexpr int copy_lead(int W, int FP8, int nst) {
 // Ring over steps 0 .. n-1 without cross-step overlap of the compute;
 // body(stage, s) consumes step s. Ends with a barrier (the ring may be
 // refilled).
-template <int W, int FP8, int RING, class Fetch, class Addr, class Body>
+template <int W, int FP8, int RING, int LEAD_SET = 0, class Fetch, class Addr, class Body>
 __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
                                           Fetch fetch, Addr addr, Body body, int tid) {
   using P = CopyPlan<W, FP8, RING>;
-  constexpr int LEAD = copy_lead(W, FP8, P::NST);
+  constexpr int LEAD = LEAD_SET > 0 ? LEAD_SET : copy_lead(W, FP8, P::NST);
   static_assert(LEAD >= 1 && LEAD <= P::NST - 1 && LEAD <= 6, "copy lead");
   Addresser<W, FP8, RING, Fetch, Addr> ad{fetch, addr, tid};
   const uint32_t ring_lds = (uint32_t)(uintptr_t)(lds_void_t*)ring;   // LDS byte address
@@ -527,10 +528,11 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
 
 // Steps 0 .. n-1 of a ring: the scores of a step (qk) then the rest of it
 // (fin). The two waves of a SIMD overlap each other's matrix and vector work.
-template <int W, int FP8, int RT, int RING, class Fetch, class Addr, class QK, class Fin>
+template <int W, int FP8, int RT, int RING, int LEAD_SET = 0, class Fetch, class Addr, class QK,
+          class Fin>
 __device__ __forceinline__ void run_steps(uint4* ring, int n, const uint8_t* Kb, const uint8_t* Vb,
                                           Fetch fetch, Addr addr, QK qk, Fin fin, int tid) {
-  ring_loop<W, FP8, RING>(ring, n, Kb, Vb, fetch, addr, [&](const uint4* st, int s) {
+  ring_loop<W, FP8, RING, LEAD_SET>(ring, n, Kb, Vb, fetch, addr, [&](const uint4* st, int s) {
     Scores<RT> S;
     qk(st, S);
     fin(st, S, s);
@@ -754,7 +756,7 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
               },
               tid);
         } else {
-          run_steps<W, 0, RT, RING>(
+          run_steps<W, 0, RT, RING, W == 8 ? 1 : 0>(   // bf16 kept steps: one step ahead
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
