@@ -29,6 +29,11 @@
  *   fp2_workspace_bytes(params) bytes (256-byte aligned). It may be reused
  *   across calls and layers on one stream; concurrent calls need distinct
  *   workspaces.
+ * - A call only enqueues kernels (no allocation, memset or host
+ *   synchronisation; the work counters are reset by a kernel of the call
+ *   itself), so it may be captured in a HIP graph and replayed, with every
+ *   buffer it names kept at the same address; the host-side arguments
+ *   (params, the _host arrays) are read at capture time only.
  * - Errors are reported as fp2_status_t only; nothing aborts. Host-visible
  *   arguments are validated before any launch (FP2_EINVAL, FP2_EUNSUPPORTED,
  *   FP2_EWORKSPACE); a failed launch returns FP2_EHIP. The consistency of
