@@ -154,7 +154,7 @@ extern "C" {
 typedef enum {
   FP2_OK = 0,
   FP2_EINVAL = 1,        /* a null or inconsistent argument */
-  FP2_EUNSUPPORTED = 2,  /* a valid configuration this build does not cover */
+  FP2_EUNSUPPORTED = 2,  /* a valid configuration the library does not cover */
   FP2_EWORKSPACE = 3,    /* workspace null or smaller than fp2_workspace_bytes */
   FP2_EHIP = 4           /* a HIP launch or runtime call failed */
 } fp2_status_t;
