@@ -49,7 +49,8 @@ class Params(ctypes.Structure):
 
 EXPORTS = ["fp2_workspace_bytes", "fp2_prefill", "fp2_estimate", "fp2_attend", "fp2_pool",
            "fp2_csr_capacity", "fp2_mask_to_csr", "fp2_means_cache_slots", "fp2_prefill_cached",
-           "fp2_calibrate", "fp2_status_str", "fp2_last_error"]
+           "fp2_calibrate", "fp2_time_kernels", "fp2_status_str",
+           "fp2_last_error"]
 
 CALIB_KINDS = {"mfma_bf16": 0, "mfma_fp8": 1, "exp": 2}
 
@@ -90,6 +91,8 @@ def lib():
             [vp] * 4 + [ctypes.c_size_t, vp]
         L.fp2_calibrate.restype = ctypes.c_int
         L.fp2_calibrate.argtypes = [ctypes.c_int, ctypes.c_int32, vp, ctypes.POINTER(ctypes.c_double), vp]
+        L.fp2_time_kernels.restype = ctypes.c_int
+        L.fp2_time_kernels.argtypes = [vp] * 4
         L.fp2_status_str.restype = ctypes.c_char_p
         L.fp2_status_str.argtypes = [ctypes.c_int]
         L.fp2_last_error.restype = ctypes.c_char_p
@@ -171,6 +174,81 @@ def _ptr(t: Optional[torch.Tensor]):
     return ctypes.c_void_p(t.data_ptr())
 
 
+_ESZ = {BF16: 2, FP8_E4M3: 1}
+
+
+def _need(t, name, *, dtypes=None, esz=None, min_numel=None, divisible=None, contiguous=True):
+    """Refuse a tensor the library would misread: wrong dtype (or element
+    size), a non-contiguous view (the library reads dense rows at fixed
+    strides), or too few elements. The device is checked by the caller."""
+    if t is None:
+        return
+    if not isinstance(t, torch.Tensor):
+        raise ValueError("%s must be a torch tensor" % name)
+    if dtypes is not None and t.dtype not in dtypes:
+        raise ValueError("%s must have dtype in %s, got %s" % (name, dtypes, t.dtype))
+    if esz is not None and t.element_size() != esz:
+        raise ValueError("%s must have %d-byte elements, got %s" % (name, esz, t.dtype))
+    if contiguous and not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError("%s holds %d elements, needs at least %d" % (name, t.numel(), min_numel))
+    if divisible is not None and t.numel() % divisible:
+        raise ValueError("%s: %d elements is not a multiple of %d" % (name, t.numel(), divisible))
+
+
+_INT32 = (torch.int32,)
+_F32 = (torch.float32,)
+
+
+def _check_inputs(p: Params, q=None, k_cache=None, v_cache=None, cu_seqlens=None,
+                  block_table=None, cu_seqlens_k=None, q_scale=None, k_scale=None,
+                  v_scale=None, out=None, lse=None, block_mask=None, workspace=None,
+                  mask_in=None):
+    """Dtype, contiguity and size of every device tensor handed to the library
+    (the C ABI sees only pointers)."""
+    esz = _ESZ.get(p.dtype)
+    row_q = p.num_q_heads * p.head_dim
+    row_kv = p.num_kv_heads * p.head_dim
+    _need(q, "q", esz=esz, divisible=row_q)
+    _need(k_cache, "k_cache", esz=esz, divisible=row_kv)
+    _need(v_cache, "v_cache", esz=esz, divisible=row_kv)
+    if k_cache is not None and v_cache is not None and k_cache.numel() != v_cache.numel():
+        raise ValueError("k_cache and v_cache differ in size")
+    _need(cu_seqlens, "cu_seqlens", dtypes=_INT32, min_numel=p.batch + 1)
+    _need(cu_seqlens_k, "cu_seqlens_k", dtypes=_INT32, min_numel=p.batch + 1)
+    if p.page_size > 0 and block_table is not None:
+        # the library reads row b at b * max_pages_per_seq: the table must be
+        # exactly that wide (a wider one would shift every row after the first)
+        if block_table.dim() != 2 or block_table.shape[1] != p.max_pages_per_seq \
+                or block_table.shape[0] < p.batch:
+            raise ValueError("block_table must be int32 [>= batch, max_pages_per_seq = %d], got %s"
+                             % (p.max_pages_per_seq, tuple(block_table.shape)))
+        _need(block_table, "block_table", dtypes=_INT32)
+    if p.dtype == FP8_E4M3:
+        g = p.num_q_heads
+        _need(q_scale, "q_scale", dtypes=_F32, min_numel=g)
+        _need(k_scale, "k_scale", dtypes=_F32, min_numel=p.num_kv_heads)
+        _need(v_scale, "v_scale", dtypes=_F32, min_numel=p.num_kv_heads)
+    rows = None if q is None else q.numel() // row_q
+    if out is not None:
+        _need(out, "out", dtypes=(torch.bfloat16,), min_numel=(rows or 0) * row_q)
+    if lse is not None:
+        _need(lse, "lse", dtypes=_F32, min_numel=(rows or 0) * p.num_q_heads)
+    nmask = p.batch * p.num_kv_heads * max(1, num_blocks(p)) * max(1, num_key_blocks(p))
+    _need(block_mask, "block_mask", dtypes=(torch.uint8,), min_numel=nmask)
+    _need(mask_in, "block_mask", dtypes=(torch.uint8, torch.bool), min_numel=nmask)
+    _need(workspace, "workspace", esz=1)
+    named = (("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("cu_seqlens", cu_seqlens),
+             ("block_table", block_table if p.page_size > 0 else None),
+             ("cu_seqlens_k", cu_seqlens_k), ("q_scale", q_scale), ("k_scale", k_scale),
+             ("v_scale", v_scale), ("out", out), ("lse", lse), ("block_mask", block_mask),
+             ("workspace", workspace), ("block_mask", mask_in))
+    for name, t in named:
+        if t is not None and not t.is_cuda:
+            raise ValueError("%s must be a CUDA tensor" % name)
+
+
 def _host_ptr(a):
     if a is None:
         return None
@@ -225,6 +303,8 @@ def prefill(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_
         lse = l2 if lse is None else lse
     if workspace is None:
         workspace = alloc_workspace(p, q.device)
+    _check_inputs(p, q, k_cache, v_cache, cu_seqlens, block_table, cu_seqlens_k, q_scale,
+                  k_scale, v_scale, out, lse, block_mask, workspace)
     head = (ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
             _ptr(cu_seqlens_k), _host_ptr(cu_seqlens_k_host), _ptr(k_cache), _ptr(v_cache),
             _ptr(block_table), _ptr(q_scale), _ptr(k_scale), _ptr(v_scale))
@@ -237,6 +317,22 @@ def prefill(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_
         mc = MeansCache(_ptr(kh), _ptr(vb), _ptr(pooled))
         _check("fp2_prefill_cached", lib().fp2_prefill_cached(*head, ctypes.byref(mc), *tail))
     return out, block_mask, lse
+
+
+def time_kernels(estimate=None, attend=None):
+    """fp2_time_kernels: estimate / attend are (begin, end) pairs of recorded
+    torch.cuda.Event(enable_timing=True) (or None); later calls on this host
+    thread record them around the estimation kernels / the attention kernel.
+    time_kernels() stops."""
+    def h(ev):
+        if ev is None:
+            return None
+        if not ev.cuda_event:
+            raise ValueError("record each event once before handing it to the library")
+        return ctypes.c_void_p(ev.cuda_event)
+    eb, ee = (None, None) if estimate is None else estimate
+    ab, ae = (None, None) if attend is None else attend
+    _check("fp2_time_kernels", lib().fp2_time_kernels(h(eb), h(ee), h(ab), h(ae)))
 
 
 def means_cache_slots(p: Params, num_pages: int) -> int:
@@ -264,6 +360,8 @@ def estimate(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *,
         block_mask = alloc_mask(p, q.device)
     if workspace is None:
         workspace = alloc_workspace(p, q.device)
+    _check_inputs(p, q, k_cache, v_cache, cu_seqlens, block_table, cu_seqlens_k, q_scale,
+                  k_scale, v_scale, block_mask=block_mask, workspace=workspace)
     st = lib().fp2_estimate(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
                             _ptr(cu_seqlens_k), _host_ptr(cu_seqlens_k_host), _ptr(k_cache),
                             _ptr(v_cache), _ptr(block_table), _ptr(q_scale), _ptr(k_scale),
@@ -285,6 +383,8 @@ def attend(p: Params, q, k_cache, v_cache, cu_seqlens, block_mask, block_table=N
         lse = torch.empty((q.shape[0], p.num_q_heads), dtype=torch.float32, device=q.device)
     if workspace is None:
         workspace = alloc_workspace(p, q.device)
+    _check_inputs(p, q, k_cache, v_cache, cu_seqlens, block_table, cu_seqlens_k, q_scale,
+                  k_scale, v_scale, out, lse, workspace=workspace, mask_in=block_mask)
     st = lib().fp2_attend(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
                           _ptr(cu_seqlens_k), _host_ptr(cu_seqlens_k_host), _ptr(k_cache),
                           _ptr(v_cache), _ptr(block_table), _ptr(q_scale), _ptr(k_scale),
@@ -302,6 +402,8 @@ def pool(p: Params, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_seqlen
     shape = (p.batch, p.num_kv_heads, nb, p.head_dim)
     khat = torch.empty(shape, dtype=torch.bfloat16, device=k_cache.device)
     vbar = torch.empty(shape, dtype=torch.bfloat16, device=k_cache.device)
+    _check_inputs(p, k_cache=k_cache, v_cache=v_cache, cu_seqlens=cu_seqlens,
+                  block_table=block_table, k_scale=k_scale, v_scale=v_scale)
     st = lib().fp2_pool(ctypes.byref(p), _ptr(cu_seqlens), _host_ptr(cu_seqlens_host),
                         _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(k_scale),
                         _ptr(v_scale), _ptr(khat), _ptr(vbar), _stream(stream))

@@ -119,7 +119,7 @@ class ForwardMetadata:
     plan: ForwardPlan
     cu_q: object                   # device int32 [batch + 1]
     cu_k: object                   # device int32 [batch + 1]
-    block_table: object            # device int32 [batch, >= max_pages_per_seq]
+    block_table: object            # device int32 [batch, max_pages_per_seq], dense
     pooled_blocks: object          # device int32 [batch]: cached complete prefix blocks
 
     @property
@@ -165,9 +165,17 @@ class PrefillBackend:
         pooled = np.array([c // BLOCK for c in cached], np.int32)
         host = np.concatenate([plan.cu_q, plan.cu_k, pooled]).astype(np.int32)
         dev = torch.from_numpy(host).to(self.device)
-        if block_table.shape[1] < self.cfg.max_pages_per_seq:
-            raise ValueError("block_table has %d columns, the config needs %d"
-                             % (block_table.shape[1], self.cfg.max_pages_per_seq))
+        w = self.cfg.max_pages_per_seq
+        if not (isinstance(block_table, torch.Tensor) and block_table.is_cuda
+                and block_table.dtype == torch.int32 and block_table.dim() == 2):
+            raise ValueError("block_table must be a CUDA int32 tensor [batch, pages]")
+        if block_table.shape[1] < w or block_table.shape[0] < n:
+            raise ValueError("block_table is %s, the forward needs [>= %d, >= %d]"
+                             % (tuple(block_table.shape), n, w))
+        # the library reads row b at b * max_pages_per_seq: hand it a dense
+        # table of exactly that width (a copy when the caller's is wider or strided)
+        if block_table.shape[1] != w or not block_table.is_contiguous():
+            block_table = block_table[:n, :w].contiguous()
         return ForwardMetadata(plan=plan, cu_q=dev[:n + 1], cu_k=dev[n + 1:2 * n + 2],
                                block_table=block_table, pooled_blocks=dev[2 * n + 2:])
 

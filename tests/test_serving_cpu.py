@@ -52,3 +52,53 @@ def test_worst_case_workspace_bounds_every_forward():
     worst4 = fp2.workspace_bytes(cfg4.worst_case_params())
     plan = serving.plan_forward(cfg4, [8192, 8192], [57344, 0])
     assert fp2.workspace_bytes(plan.params) <= worst4
+
+
+def _inputs(p, total, **over):
+    import torch
+    d = dict(q=torch.zeros(total, p.num_q_heads, 128, dtype=torch.uint8),
+             k_cache=torch.zeros(256, p.num_kv_heads, 128, dtype=torch.uint8),
+             v_cache=torch.zeros(256, p.num_kv_heads, 128, dtype=torch.uint8),
+             cu_seqlens=torch.zeros(p.batch + 1, dtype=torch.int32),
+             block_table=torch.zeros(p.batch, p.max_pages_per_seq, dtype=torch.int32),
+             q_scale=torch.ones(p.num_q_heads), k_scale=torch.ones(p.num_kv_heads),
+             v_scale=torch.ones(p.num_kv_heads))
+    d.update(over)
+    return d
+
+
+@pytest.mark.parametrize("what,bad,msg", [
+    ("block_table", "wider", "block_table must be int32"),
+    ("block_table", "strided", "block_table must be contiguous"),
+    ("block_table", "int64", "block_table must have dtype"),
+    ("q", "bf16", "q must have 1-byte elements"),
+    ("q", "strided", "q must be contiguous"),
+    ("k_cache", "ragged", "k_cache: .* not a multiple"),
+    ("cu_seqlens", "short", "cu_seqlens holds"),
+    ("k_scale", "f64", "k_scale must have dtype"),
+])
+def test_binding_refuses_misshapen_tensors(what, bad, msg):
+    """The C ABI takes bare pointers and reads the page table at row stride
+    max_pages_per_seq: the binding refuses a table of another width, strided
+    views, wrong element types and short arrays before anything is called."""
+    import torch
+    p = CFG.params(2, 1000, 1000)
+    w = p.max_pages_per_seq
+    bad_t = {
+        ("block_table", "wider"): torch.zeros(2, w + 3, dtype=torch.int32),
+        ("block_table", "strided"): torch.zeros(2, 2 * w, dtype=torch.int32)[:, ::2],
+        ("block_table", "int64"): torch.zeros(2, w, dtype=torch.int64),
+        ("q", "bf16"): torch.zeros(16, 32, 128, dtype=torch.bfloat16),
+        ("q", "strided"): torch.zeros(16, 32, 256, dtype=torch.uint8)[:, :, :128],
+        ("k_cache", "ragged"): torch.zeros(256 * 8 * 128 + 5, dtype=torch.uint8),
+        ("cu_seqlens", "short"): torch.zeros(2, dtype=torch.int32),
+        ("k_scale", "f64"): torch.ones(8, dtype=torch.float64),
+    }[(what, bad)]
+    d = _inputs(p, 16, **{what: bad_t})
+    if what == "k_cache":
+        d["v_cache"] = torch.zeros_like(bad_t)
+    with pytest.raises(ValueError, match=msg):
+        fp2._check_inputs(p, **d)
+    # the same call with well-formed (host) tensors gets as far as the device check
+    with pytest.raises(ValueError, match="must be a CUDA tensor"):
+        fp2._check_inputs(p, **_inputs(p, 16))
