@@ -9,12 +9,16 @@ per-head scales, threshold calibrated to ~5% kept blocks, correction on.
 
 Prints ONE JSON line with the dense-equivalent throughput, the latency, the
 kept-block ratio, a roofline entry for the attention kernel (the dominant
-kernel), and the oracle timed on the host cores on a bounded sample;
---variants adds the other 128K variants (kept ratio, correction off, bf16,
-GQA 8:1). The roofline's HBM traffic comes from the committed rocprofv3
-counter summary of the attention kernel, and the estimation stage's traffic
-(pool + estimate kernels) from its own summary, each only while the kernel
-sources are the ones the counters were taken on (else null).
+kernel; its duration from HIP events the library records right around its
+launch), the oracle timed on the host cores on a bounded sample, and a
+`configs` array with every benchmark configuration (2K, 32K bf16, the 128K
+fp8 layer at 10 / 5 / 2 % kept with the correction on and off, the ragged
+batch of 8, the 128K 64/8-head layer in bf16 and fp8 with its error against
+dense attention). --variants adds the paper-literal 128-row selection tile.
+The roofline's HBM traffic comes from the committed rocprofv3 counter summary
+of the attention kernel, and the estimation stage's traffic (pool + estimate
+kernels) from its own summary, each only while the kernel sources are the
+ones the counters were taken on (else null).
 """
 from __future__ import annotations
 
@@ -43,8 +47,10 @@ def parse():
     ap.add_argument("--workload", default="llama128k_fp8")
     ap.add_argument("--target", default="0.05", help="kept-ratio target the alpha was calibrated for")
     ap.add_argument("--variants", action="store_true",
-                    help="also measure the other 128K variants (not part of the headline line)")
-    ap.add_argument("--no-variants", action="store_true", help="(default; kept for old scripts)")
+                    help="also measure the paper-literal 128-row selection tile on the headline "
+                         "workload and the mask-to-CSR conversion")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-config array (every benchmark configuration)")
     ap.add_argument("--chunked", action="store_true",
                     help="also measure chunked prefill of the default workload through the "
                          "serving backend (prefix KV), its short tail chunks with and without KV "
@@ -185,48 +191,47 @@ def measured_peaks():
     return res
 
 
-def setup(name, target, correction=None, tile_rows=0):
+def setup(name, target, correction=None, tile_rows=0, base=None):
+    """Inputs resident on the GPU, buffers and the prefill call of one
+    workload at one calibrated threshold. base: a setup of the same workload
+    whose generated inputs are reused (other threshold or correction)."""
     import torch
-    import numpy as np  # noqa: F401
     import paper_2608_19758_amd as fp2
     import synth
 
-    spec = synth.named(name)
-    if correction is not None:
-        spec = spec.replace(mean_correction=int(correction))
-    wl = synth.generate(spec)
+    if base is not None and base["spec"].name == name:
+        wl, d = base["wl"], base["d"]
+        spec = wl.spec
+    else:
+        spec = synth.named(name)
+        wl = synth.generate(spec)
+        d = wl.device_inputs("cuda")
+        if spec.dtype == "bf16":
+            for k in ("q", "k_cache", "v_cache"):
+                d[k] = d[k].view(torch.bfloat16)
+    corr = spec.mean_correction if correction is None else int(correction)
     alpha = synth.alpha_for(name, target)
-    d = wl.device_inputs("cuda")
-    if spec.dtype == "bf16":
-        for k in ("q", "k_cache", "v_cache"):
-            d[k] = d[k].view(torch.bfloat16)
     p = fp2.make_params(batch=spec.batch, num_q_heads=spec.num_q_heads,
                         num_kv_heads=spec.num_kv_heads, max_seq_len=spec.max_seq_len,
                         page_size=spec.page_size, max_pages_per_seq=wl.max_pages, alpha=alpha,
                         sink_blocks=spec.sink_blocks, window_blocks=spec.window_blocks,
-                        recent_blocks=spec.recent_blocks, mean_correction=spec.mean_correction,
+                        recent_blocks=spec.recent_blocks, mean_correction=corr,
                         dtype=spec.dtype, query_tile_rows=tile_rows)
     out, mask, _ = fp2.alloc_outputs(p, spec.total_tokens)
-    mask2 = torch.empty_like(mask)
     ws = fp2.alloc_workspace(p)
-    ws2 = fp2.alloc_workspace(p)
     bt = d["block_table"] if spec.page_size else None
     kw = dict(cu_seqlens_host=wl.cu_seqlens, q_scale=d["q_scale"], k_scale=d["k_scale"],
               v_scale=d["v_scale"])
 
-    def run_prefill():
+    def run_prefill(out=out, p=p):
         fp2.prefill(p, d["q"], d["k_cache"], d["v_cache"], d["cu_seqlens"], bt, out=out,
                     block_mask=mask, workspace=ws, **kw)
 
-    def run_estimate():
-        fp2.estimate(p, d["q"], d["k_cache"], d["v_cache"], d["cu_seqlens"], bt,
-                     block_mask=mask2, workspace=ws2, **kw)
-
     def run_csr():
-        return fp2.mask_to_csr(p, mask, d["cu_seqlens"], workspace=ws2)
+        return fp2.mask_to_csr(p, mask, d["cu_seqlens"], workspace=ws)
 
-    return dict(spec=spec, wl=wl, alpha=alpha, p=p, d=d, out=out, mask=mask,
-                run_prefill=run_prefill, run_estimate=run_estimate, run_csr=run_csr)
+    return dict(spec=spec, wl=wl, alpha=alpha, p=p, d=d, out=out, mask=mask, ws=ws,
+                target=target, correction=corr, run_prefill=run_prefill, run_csr=run_csr)
 
 
 def time_loop(fn, steps, warmup):
@@ -248,12 +253,43 @@ def time_loop(fn, steps, warmup):
     return e0.elapsed_time(e1) / steps, (t1 - t0) * 1e3 / steps
 
 
+def timed_prefill(cfg, steps, warmup):
+    """K prefill steps timed with HIP events on the library's stream, and in
+    each step the library records one more event pair right around the
+    attention kernel and one around the estimation kernels (fp2_time_kernels):
+    (ms per step, wall ms per step, estimation-kernel ms, attention-kernel
+    ms), averages over the K steps."""
+    import torch
+    import paper_2608_19758_amd as fp2
+    for _ in range(warmup):
+        cfg["run_prefill"]()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for row in ev:
+        for e in row:
+            e.record()   # creates the event the library records into
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    try:
+        for i in range(steps):
+            fp2.time_kernels(estimate=(ev[i][0], ev[i][1]), attend=(ev[i][2], ev[i][3]))
+            cfg["run_prefill"]()
+    finally:
+        fp2.time_kernels()
+    e1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    est = sum(r[0].elapsed_time(r[1]) for r in ev) / steps
+    att = sum(r[2].elapsed_time(r[3]) for r in ev) / steps
+    return e0.elapsed_time(e1) / steps, (t1 - t0) * 1e3 / steps, est, att
+
+
 def measure(cfg, steps, warmup):
     from paper_2608_19758_amd import accounting as acc
     sp = cfg["spec"]
-    t_pre, wall = time_loop(cfg["run_prefill"], steps, warmup)
-    t_est, _ = time_loop(cfg["run_estimate"], steps, warmup)
-    cfg["run_prefill"]()
+    t_pre, wall, t_est, t_attn = timed_prefill(cfg, steps, warmup)
     mask = cfg["mask"].cpu().numpy()
     if cfg["p"].query_tile_rows:
         # kept pairs over visible (tile, key block) pairs of the 128-row tiles
@@ -266,13 +302,13 @@ def measure(cfg, steps, warmup):
             * sp.num_kv_heads)
     dense = acc.dense_equiv_flops(sp.seqlens, sp.num_q_heads)
     fk, fc = acc.attention_flops(mask, sp.seqlens, sp.num_q_heads, sp.num_kv_heads,
-                                 correction=bool(sp.mean_correction),
+                                 correction=bool(cfg["correction"]),
                                  tile_rows=cfg["p"].query_tile_rows)
-    t_attn = max(1e-6, t_pre - t_est)
+    t_attn = max(1e-6, t_attn)
     main_peak = PEAK_TFLOPS[sp.dtype]
     # time-weighted peak: kept tiles run at the dtype's MFMA peak, the
     # correction chunks on bf16 MFMA
-    peak = (fk + fc) / (fk / main_peak + fc / PEAK_TFLOPS["bf16"]) if (fk + fc) else main_peak
+    mix = (fk + fc) / (fk / main_peak + fc / PEAK_TFLOPS["bf16"]) if (fk + fc) else main_peak
     achieved = (fk + fc) / (t_attn * 1e-3) / 1e12
     est_bytes = acc.estimation_bytes(sp.seqlens, sp.num_q_heads, sp.num_kv_heads,
                                      elem=1 if sp.dtype == "fp8" else 2)
@@ -281,13 +317,97 @@ def measure(cfg, steps, warmup):
         ms_per_step=t_pre, wall_ms_per_step=wall, estimate_ms=t_est, attention_ms=t_attn,
         dense_tflops=dense / (t_pre * 1e-3) / 1e12, kept_ratio=kept_ratio,
         attention=dict(executed_tflop=(fk + fc) / 1e12, kept_tflop=fk / 1e12, corr_tflop=fc / 1e12,
-                       achieved_tflops=achieved, peak_tflops=peak, frac=achieved / peak),
+                       achieved_tflops=achieved, peak_tflops=main_peak,
+                       frac=achieved / main_peak, mix_peak_tflops=mix, frac_mix=achieved / mix),
         estimation=dict(alg_bytes=est_bytes, gbs=est_bytes / (t_est * 1e-3) / 1e9,
                         hbm_frac=est_bytes / (t_est * 1e-3) / 1e9 / PEAK_HBM_GBS,
                         scoring_tflop=sflop / 1e12,
                         mfma_frac=sflop / (t_est * 1e-3) / 1e12 / PEAK_TFLOPS["bf16"],
                         exps_per_s=sflop / (2 * sp.head_dim) / (t_est * 1e-3)),
     )
+
+
+def config_entry(cfg, r, cid):
+    """One entry of the per-config array."""
+    sp = cfg["spec"]
+    return {"config": cid, "workload": sp.name, "dtype": sp.dtype, "batch": sp.batch,
+            "seqlens": sp.seqlens if sp.batch <= 8 else None,
+            "num_q_heads": sp.num_q_heads, "num_kv_heads": sp.num_kv_heads,
+            "kept_target": float(cfg["target"]), "alpha": cfg["alpha"],
+            "mean_correction": cfg["correction"],
+            "ms": round(r["ms_per_step"], 4),
+            "dense_tflops": round(r["dense_tflops"], 2),
+            "kept_ratio": round(r["kept_ratio"], 5),
+            "attention_kernel_ms": round(r["attention_ms"], 4),
+            "attention_executed_tflops": round(r["attention"]["achieved_tflops"], 1),
+            "attention_mfma_frac": round(r["attention"]["frac"], 4),
+            "attention_mfma_frac_mix": round(r["attention"]["frac_mix"], 4),
+            "estimate_ms": round(r["estimate_ms"], 4),
+            "estimation_hbm_frac": round(r["estimation"]["hbm_frac"], 4),
+            "estimation_scoring_mfma_frac": round(r["estimation"]["mfma_frac"], 4)}
+
+
+def error_vs_dense(cfg):
+    """The sparse output against dense attention computed by the same kernels
+    with every causal block kept (alpha = 0): max-abs and relative Frobenius
+    error over every output element."""
+    import torch
+    import paper_2608_19758_amd as fp2
+    sp = cfg["spec"]
+    p0 = fp2.make_params(batch=sp.batch, num_q_heads=sp.num_q_heads,
+                         num_kv_heads=sp.num_kv_heads, max_seq_len=sp.max_seq_len,
+                         page_size=sp.page_size, max_pages_per_seq=cfg["wl"].max_pages, alpha=0.0,
+                         sink_blocks=sp.sink_blocks, window_blocks=sp.window_blocks,
+                         recent_blocks=sp.recent_blocks, mean_correction=cfg["correction"],
+                         dtype=sp.dtype)
+    dense = torch.empty_like(cfg["out"])
+    cfg["run_prefill"]()
+    cfg["run_prefill"](out=dense, p=p0)
+    torch.cuda.synchronize()
+    worst, num, den = 0.0, 0.0, 0.0
+    for t0 in range(0, dense.shape[0], 16384):
+        a = cfg["out"][t0:t0 + 16384].float()
+        b = dense[t0:t0 + 16384].float()
+        worst = max(worst, float((a - b).abs().max()))
+        num += float(((a - b) ** 2).sum())
+        den += float((b ** 2).sum())
+    del dense
+    return {"max_abs": float("%.4g" % worst), "rel_fro": float("%.4g" % ((num / max(den, 1e-300)) ** 0.5)),
+            "reference": "dense causal attention by the same kernels at alpha = 0"}
+
+
+def run_configs(head_cfg, head_m, steps, warmup):
+    """Every benchmark configuration: tiny 2K, 32K bf16, the 128K fp8 layer at
+    10 / 5 / 2 % kept with the correction on and off, the ragged batch of 8,
+    and the 128K 64/8-head layer in bf16 and fp8 with its error against dense
+    attention. The headline measurement is reused for its own entry."""
+    import torch
+    entries = []
+    plan = [(0, "tiny2k", "0.30", None), (1, "llama32k", "0.18", None)]
+    plan += [(2, "llama128k_fp8", t, c) for t in ("0.10", "0.05", "0.02") for c in (1, 0)]
+    plan += [(3, "ragged8", "0.18", None), (4, "wide128k_bf16", "0.009", None),
+             (4, "wide128k_fp8", "0.009", None)]
+    base = head_cfg
+    for cid, name, tgt, corr in plan:
+        hs = head_cfg["spec"]
+        if (name, tgt) == (hs.name, head_cfg["target"]) and \
+                (corr is None or corr == head_cfg["correction"]):
+            entries.append(config_entry(head_cfg, head_m, cid))
+            entries[-1]["headline"] = True
+            continue
+        c = setup(name, tgt, corr, base=base if base is not None and base["spec"].name == name
+                  else None)
+        big = c["spec"].max_seq_len >= 65536 or c["spec"].batch > 1
+        r = measure(c, max(5, steps // 2) if big else steps, max(2, warmup // 2))
+        e = config_entry(c, r, cid)
+        if cid == 4:
+            e["error_vs_dense"] = error_vs_dense(c)
+        entries.append(e)
+        print("[bench] config %s" % json.dumps(e), file=sys.stderr, flush=True)
+        if c["spec"].name != head_cfg["spec"].name:
+            del c
+            torch.cuda.empty_cache()
+    return entries
 
 
 def chunked(cfg, steps, warmup):
@@ -487,33 +607,23 @@ def main():
     peaks = measured_peaks()
     print("[bench] measured on this GPU: %s" % json.dumps(peaks), file=sys.stderr, flush=True)
 
+    configs = []
+    if not args.no_configs:
+        configs = run_configs(cfg, m, args.steps, args.warmup)
     variants = []
     if args.variants:
-        vlist = [("llama128k_fp8", "0.10", None, 0), ("llama128k_fp8", "0.02", None, 0),
-                 ("llama128k_fp8", "0.05", 0, 0), ("llama128k_bf16", "0.05", None, 0),
-                 ("wide128k_bf16", "0.009", None, 0), ("wide128k_fp8", "0.009", None, 0),
-                 ("llama128k_fp8", "0.05", None, 128)]
+        # the paper-literal selection tile (128 packed rows) on the headline
+        # workload, and the mask-to-CSR conversion of the headline mask
         csr_ms = time_loop(cfg["run_csr"], max(5, args.steps // 2), 2)[0]
         print("[bench] mask to CSR: %.3f ms" % csr_ms, file=sys.stderr, flush=True)
-        del cfg
+        c = setup(args.workload, args.target, None, 128, base=cfg)
+        r = measure(c, max(5, args.steps // 2), max(2, args.warmup // 2))
+        e = config_entry(c, r, 2)
+        e["query_tile_rows"] = 128
+        variants.append(e)
+        print("[bench] variant %s" % json.dumps(e), file=sys.stderr, flush=True)
+        del c
         torch.cuda.empty_cache()
-        for name, tgt, corr, tile in vlist:
-            if name == args.workload and tgt == args.target and corr is None and not tile:
-                continue
-            c = setup(name, tgt, corr, tile)
-            r = measure(c, max(5, args.steps // 2), max(2, args.warmup // 2))
-            variants.append({"workload": name, "kept_target": float(tgt),
-                             "query_tile_rows": tile,
-                             "mean_correction": c["spec"].mean_correction,
-                             "ms": round(r["ms_per_step"], 4),
-                             "dense_tflops": round(r["dense_tflops"], 2),
-                             "kept_ratio": round(r["kept_ratio"], 5),
-                             "attention_ms": round(r["attention_ms"], 4),
-                             "estimate_ms": round(r["estimate_ms"], 4),
-                             "attention_mfma_frac": round(r["attention"]["frac"], 4)})
-            print("[bench] variant %s" % json.dumps(variants[-1]), file=sys.stderr, flush=True)
-            del c
-            torch.cuda.empty_cache()
 
     att = m["attention"]
     headline = (args.workload, args.target) == ("llama128k_fp8", "0.05")
@@ -540,12 +650,21 @@ def main():
                    "window_blocks": sp.window_blocks, "mean_correction": sp.mean_correction},
         "kept_ratio": round(m["kept_ratio"], 5),
         "latency_ms": {"prefill": round(m["ms_per_step"], 4),
-                       "estimate": round(m["estimate_ms"], 4),
-                       "attention": round(m["attention_ms"], 4)},
+                       "estimate_kernels": round(m["estimate_ms"], 4),
+                       "attention_kernel": round(m["attention_ms"], 4)},
+        # the attention kernel: executed FLOPs (kept blocks at the dtype's
+        # MFMA rate, the correction's pooled keys on bf16 MFMA) over its own
+        # duration (HIP events recorded by the library right around its
+        # launch in every timed step), against the dtype's MFMA peak; frac_mix
+        # against the time-weighted peak of the two MFMA rates
         "roofline": {"bound": "mfma", "kernel": "attend_kernel",
                      "achieved": round(att["achieved_tflops"], 2),
                      "peak": round(att["peak_tflops"], 1), "unit": "TFLOP/s",
                      "frac": round(att["frac"], 4),
+                     "frac_mix": round(att["frac_mix"], 4),
+                     "peak_mix": round(att["mix_peak_tflops"], 1),
+                     "kernel_ms": round(m["attention_ms"], 4),
+                     "executed_tflop": round(att["executed_tflop"], 4),
                      "traffic": None if traffic is None else round(traffic / 1e9, 3),
                      "traffic_unit": "GB per launch"},
         # the index stage (pooling + scoring + selection): its HBM fraction, and
@@ -567,6 +686,8 @@ def main():
         "cpu_baseline": None if cpu is None else {k: (round(v, 6) if isinstance(v, float) else v)
                                                   for k, v in cpu.items() if k != "seconds"},
     }
+    if configs:
+        line["configs"] = configs
     if variants:
         line["variants"] = variants
         line["mask_to_csr_ms"] = round(csr_ms, 4)

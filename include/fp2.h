@@ -139,7 +139,9 @@
  * the probabilities of kept keys are rounded to e4m3 as P~ = e4m3(2^8 *
  * exp(S - m)) before the value product, and the softmax denominator sums
  * those rounded P~ (so out is a convex combination of values); the 2^8 is
- * removed from lse. Scales must be positive and finite.
+ * removed from lse. The running maximum m moves only when a logit passes it
+ * by more than tau = 0.8 (base 2), so P~ lies in [0, 2^8.8] (2^8.8 < 446,
+ * below 448, the largest e4m3 value). Scales must be positive and finite.
  */
 #ifndef FP2_H
 #define FP2_H
@@ -354,6 +356,20 @@ typedef enum {
 } fp2_calib_kind_t;
 fp2_status_t fp2_calibrate(fp2_calib_kind_t kind, int32_t iters, float* sink, double* ops,
                            void* stream);
+
+/* Measurement helper, not a step of the method: from this call on, the
+ * entry points called on this host thread record the given HIP events
+ * (hipEvent_t created by the caller; NULL = none) on the call's stream:
+ * estimate_begin right before the block-means kernel and estimate_end right
+ * after the scoring and selection kernels (fp2_prefill, fp2_prefill_cached,
+ * fp2_estimate), attend_begin right before the attention kernel and
+ * attend_end right after it (fp2_prefill, fp2_prefill_cached, fp2_attend).
+ * Each call records each event once, so the elapsed time between a pair is
+ * the duration of those kernels in that call; time K calls with K pairs set
+ * between the calls. Pass all NULL to stop. Events come in begin/end pairs
+ * (FP2_EINVAL otherwise). Nothing else about a call changes. */
+fp2_status_t fp2_time_kernels(void* estimate_begin, void* estimate_end, void* attend_begin,
+                              void* attend_end);
 
 /* Static description of a status code. */
 const char* fp2_status_str(fp2_status_t status);

@@ -9,10 +9,19 @@
 
 #include "fp2.h"
 #include "kernels.h"
+#include "abi.h"
 
 namespace {
 
 thread_local std::string g_last_error;
+
+// Events of fp2_time_kernels for calls made on this host thread (null: none).
+struct KernelEvents {
+  hipEvent_t est_begin = nullptr, est_end = nullptr, att_begin = nullptr, att_end = nullptr;
+};
+thread_local KernelEvents g_events;
+
+hipError_t record(hipEvent_t ev, hipStream_t s) { return ev ? hipEventRecord(ev, s) : hipSuccess; }
 
 fp2_status_t fail(fp2_status_t st, const char* fmt, ...) {
   char buf[512];
@@ -295,7 +304,9 @@ size_t fp2_workspace_bytes(const fp2_params_t* params) {
   return layout_of(params).total;
 }
 
-namespace {
+}  // extern "C"
+
+namespace fp2 {
 
 fp2_status_t prefill_impl(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
                           const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
@@ -328,17 +339,34 @@ fp2_status_t prefill_impl(const fp2_params_t* params, const void* q, const int32
   }
   const Views vw = views_of(params, workspace);
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = fp2::launch_pool(pr, vw.pooled, s, mc);
+  const KernelEvents ev = g_events;
+  hipError_t e = record(ev.est_begin, s);
+  if (e == hipSuccess) e = fp2::launch_pool(pr, vw.pooled, s, mc);
   if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s, vw.plan.part_o,
                                                 vw.part_o_floats);
+  if (e == hipSuccess) e = record(ev.est_end, s);
   if (e == hipSuccess) e = fp2::launch_plan(pr, vw.kl, vw.plan, s);
+  if (e == hipSuccess) e = record(ev.att_begin, s);
   if (e == hipSuccess)
     e = fp2::launch_attend(pr, vw.pooled, block_mask, vw.kl, vw.plan, out, lse, s);
+  if (e == hipSuccess) e = record(ev.att_end, s);
   if (e == hipSuccess) e = fp2::launch_combine(pr, vw.plan, out, lse, s);
   return hip_status(e, "fp2_prefill launch");
 }
 
+size_t workspace_need(const fp2_params_t* params) {
+  return validate_params(params) != FP2_OK ? 0 : layout_of(params).total;
+}
+
+fp2_status_t set_error(fp2_status_t st, const char* msg) { return fail(st, "%s", msg); }
+
+}  // namespace fp2
+
+namespace {
+using fp2::prefill_impl;
 }  // namespace
+
+extern "C" {
 
 fp2_status_t fp2_prefill(const fp2_params_t* params, const void* q, const int32_t* cu_seqlens,
                          const int32_t* cu_seqlens_host, const int32_t* cu_seqlens_k,
@@ -390,9 +418,12 @@ fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32
                                        block_table, q_scale, k_scale, v_scale);
   const Views vw = views_of(params, workspace);
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = fp2::launch_pool(pr, vw.pooled, s);
+  const KernelEvents ev = g_events;
+  hipError_t e = record(ev.est_begin, s);
+  if (e == hipSuccess) e = fp2::launch_pool(pr, vw.pooled, s);
   if (e == hipSuccess) e = fp2::launch_estimate(pr, vw.pooled, block_mask, vw.kl, s, vw.plan.part_o,
                                                 vw.part_o_floats);
+  if (e == hipSuccess) e = record(ev.est_end, s);
   return hip_status(e, "fp2_estimate launch");
 }
 
@@ -419,8 +450,11 @@ fp2_status_t fp2_attend(const fp2_params_t* params, const void* q, const int32_t
   if (params->mean_correction) e = fp2::launch_pool(pr, vw.pooled, s);
   if (e == hipSuccess) e = fp2::launch_compact(pr, block_mask_in, vw.kl, s);
   if (e == hipSuccess) e = fp2::launch_plan(pr, vw.kl, vw.plan, s);
+  const KernelEvents ev = g_events;
+  if (e == hipSuccess) e = record(ev.att_begin, s);
   if (e == hipSuccess)
     e = fp2::launch_attend(pr, vw.pooled, block_mask_in, vw.kl, vw.plan, out, lse, s);
+  if (e == hipSuccess) e = record(ev.att_end, s);
   if (e == hipSuccess) e = fp2::launch_combine(pr, vw.plan, out, lse, s);
   return hip_status(e, "fp2_attend launch");
 }
@@ -488,6 +522,16 @@ fp2_status_t fp2_calibrate(fp2_calib_kind_t kind, int32_t iters, float* sink, do
   if (!sink || !ops) return fail(FP2_EINVAL, "sink or ops is null");
   return hip_status(fp2::launch_calib((int)kind, iters, sink, ops, (hipStream_t)stream),
                     "fp2_calibrate launch");
+}
+
+fp2_status_t fp2_time_kernels(void* estimate_begin, void* estimate_end, void* attend_begin,
+                              void* attend_end) {
+  if ((estimate_begin == nullptr) != (estimate_end == nullptr) ||
+      (attend_begin == nullptr) != (attend_end == nullptr))
+    return fail(FP2_EINVAL, "events come in begin/end pairs");
+  g_events = KernelEvents{(hipEvent_t)estimate_begin, (hipEvent_t)estimate_end,
+                          (hipEvent_t)attend_begin, (hipEvent_t)attend_end};
+  return ok();
 }
 
 const char* fp2_status_str(fp2_status_t status) {

@@ -269,3 +269,12 @@ def test_host_tensors_refused_as_device_arguments():
     cu = torch.tensor([0, 4], dtype=torch.int32)
     with pytest.raises(ValueError, match="CUDA"):
         fp2.pool(p, kv, kv, cu)
+
+
+def test_time_kernels_pairs():
+    lib = fp2.lib()
+    assert lib.fp2_time_kernels(None, None, None, None) == fp2.OK
+    assert lib.fp2_time_kernels(ctypes.c_void_p(16), None, None, None) == fp2.EINVAL
+    assert lib.fp2_time_kernels(None, None, None, ctypes.c_void_p(16)) == fp2.EINVAL
+    assert "pairs" in fp2.last_error()
+
