@@ -76,11 +76,7 @@ def test_pages_prefill_parity(page, dtype):
     print("mask: outside-band mismatches %d, in-band mismatches %d of %d in-band" % (ob, ibm, ib))
     assert ob == 0
     oout, olse = oracle.attend(inp, op, gmask)
-    err = np.abs(out - oout).max()
-    lerr = np.abs(lse - olse).max()
-    print("same-mask max-abs err %.3g (tol %g), lse err %.3g" % (err, gu.TOL[dtype], lerr))
-    assert err <= gu.TOL[dtype]
-    assert lerr <= gu.LSE_TOL[dtype]
+    gu.check_close(out, oout, lse, olse, dtype)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp8"])

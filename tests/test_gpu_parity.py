@@ -87,12 +87,7 @@ def test_prefill_parity(name, alpha):
         n = (L + sp.block_size - 1) // sp.block_size
         assert (gmask[b, :, n:, :] == 0).all() and (gmask[b, :, :, n:] == 0).all()
     oout, olse = oracle.attend(inp, op, gmask)
-    err = np.abs(out - oout).max()
-    rel = np.linalg.norm(out - oout) / max(1e-30, np.linalg.norm(oout))
-    lerr = np.abs(lse - olse).max()
-    print("same-mask max-abs err %.3g (tol %g), rel fro %.3g, lse err %.3g" % (err, gu.TOL[sp.dtype], rel, lerr))
-    assert err <= gu.TOL[sp.dtype]
-    assert lerr <= gu.LSE_TOL[sp.dtype]
+    gu.check_close(out, oout, lse, olse, sp.dtype)
 
 
 @pytest.mark.parametrize("name", ["g4_contig_2k", "g2_perm_p16", "g4_fp8"])
@@ -114,10 +109,8 @@ def test_attend_external_mask(name, corr):
                           q_scale=d["q_scale"], k_scale=d["k_scale"], v_scale=d["v_scale"],
                           want_lse=True)
     torch.cuda.synchronize()
-    err = np.abs(out.float().cpu().numpy() - oout).max()
-    print("external-mask err %.3g" % err)
-    assert err <= gu.TOL[sp.dtype]
-    assert np.abs(lse.cpu().numpy() - olse).max() <= gu.LSE_TOL[sp.dtype]
+    gu.check_close(out.float().cpu().numpy(), oout, lse.cpu().numpy(), olse, sp.dtype,
+                   label="external-mask")
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp8"])

@@ -105,11 +105,7 @@ def test_prefix_prefill_parity(name, alpha):
             assert (gmask[b, :, I, Jb + 1:] == 0).all()
             assert (gmask[b, :, I, Ja:Jb + 1] == 3).all()
     oout, olse = oracle.attend(inp, op, gmask)
-    err = np.abs(out - oout).max() if out.size else 0.0
-    lerr = np.abs(lse - olse).max() if lse.size else 0.0
-    print("same-mask max-abs err %.3g (tol %g), lse err %.3g" % (err, gu.TOL[sp.dtype], lerr))
-    assert err <= gu.TOL[sp.dtype]
-    assert lerr <= gu.LSE_TOL[sp.dtype]
+    gu.check_close(out, oout, lse, olse, sp.dtype)
 
 
 @pytest.mark.parametrize("name", ["bf16_paged_ragged", "fp8_perm", "bf16_unaligned"])
@@ -132,10 +128,8 @@ def test_prefix_attend_external_mask(name, corr):
                           k_scale=d["k_scale"], v_scale=d["v_scale"], want_lse=True,
                           **gu.kv_args(wl, d))
     torch.cuda.synchronize()
-    err = np.abs(out.float().cpu().numpy() - oout).max()
-    print("external-mask err %.3g" % err)
-    assert err <= gu.TOL[sp.dtype]
-    assert np.abs(lse.cpu().numpy() - olse).max() <= gu.LSE_TOL[sp.dtype]
+    gu.check_close(out.float().cpu().numpy(), oout, lse.cpu().numpy(), olse, sp.dtype,
+                   label="external-mask")
 
 
 CHUNKS = [
@@ -200,12 +194,8 @@ def test_chunked_prefill_fullsize_sampled():
     print("mask on %d units: outside-band mismatches %d, in-band %d of %d" % (len(units), ob, ibm, ib))
     assert ob == 0
     oout, olse = oracle.attend(inp, op, mc, units=units)
-    worst = 0.0
-    for rs, hs in gu.unit_rows(chunk, units):
-        worst = max(worst, float(np.abs(oc[rs, hs] - oout[rs, hs]).max()))
-        assert np.abs(lc[rs, hs] - olse[rs, hs]).max() <= gu.LSE_TOL["fp8"]
-    print("same-mask max-abs err on sampled units %.3g" % worst)
-    assert worst <= gu.TOL["fp8"]
+    gu.check_close(oc, oout, lc, olse, "fp8", rows=gu.unit_rows(chunk, units),
+                   label="same-mask (%d sampled units)" % len(units))
 
 
 @pytest.mark.parametrize("name", ["bf16_paged_ragged", "fp8_unaligned", "g1_paged"])
@@ -225,6 +215,4 @@ def test_score_splits_parity(name, ss):
     print("score_splits %d: mask outside-band mismatches %d, in-band %d of %d" % (ss, ob, ibm, ib))
     assert ob == 0
     oout, olse = oracle.attend(inp, op, gmask)
-    err = np.abs(out - oout).max() if out.size else 0.0
-    assert err <= gu.TOL[sp.dtype]
-    assert (np.abs(lse - olse).max() if lse.size else 0.0) <= gu.LSE_TOL[sp.dtype]
+    gu.check_close(out, oout, lse, olse, sp.dtype)

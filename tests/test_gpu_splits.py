@@ -55,11 +55,7 @@ def _check(wl, out, gmask, lse, alpha, corr=None):
     inp = oracle.Inputs(wl)
     op = gu.oracle_params(inp, alpha, corr=corr)
     oout, olse = oracle.attend(inp, op, gmask)
-    err = np.abs(out - oout).max()
-    lerr = np.abs(lse - olse).max()
-    print("same-mask max-abs err %.3g (tol %g), lse err %.3g" % (err, gu.TOL[sp.dtype], lerr))
-    assert err <= gu.TOL[sp.dtype]
-    assert lerr <= gu.LSE_TOL[sp.dtype]
+    gu.check_close(out, oout, lse, olse, sp.dtype)
     return oout
 
 
@@ -95,10 +91,8 @@ def test_splits_attend_external_mask(name, corr):
                           k_scale=d["k_scale"], v_scale=d["v_scale"], want_lse=True,
                           **gu.kv_args(wl, d))
     torch.cuda.synchronize()
-    err = np.abs(out.float().cpu().numpy() - oout).max()
-    print("external-mask err with 5 splits %.3g" % err)
-    assert err <= gu.TOL[sp.dtype]
-    assert np.abs(lse.cpu().numpy() - olse).max() <= gu.LSE_TOL[sp.dtype]
+    gu.check_close(out.float().cpu().numpy(), oout, lse.cpu().numpy(), olse, sp.dtype,
+                   label="external-mask with 5 splits")
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp8"])
@@ -136,9 +130,5 @@ def test_splits_fullsize_tail_chunk_sampled():
     inp = oracle.Inputs(wl)
     op = gu.oracle_params(inp, alpha)
     oout, olse = oracle.attend(inp, op, gmask, units=units)
-    worst = 0.0
-    for rs, hs in gu.unit_rows(wl, units):
-        worst = max(worst, float(np.abs(out[rs, hs] - oout[rs, hs]).max()))
-        assert np.abs(lse[rs, hs] - olse[rs, hs]).max() <= gu.LSE_TOL["fp8"]
-    print("same-mask max-abs err on sampled units %.3g" % worst)
-    assert worst <= gu.TOL["fp8"]
+    gu.check_close(out, oout, lse, olse, "fp8", rows=gu.unit_rows(wl, units),
+                   label="same-mask (%d sampled units)" % len(units))

@@ -63,11 +63,7 @@ def test_tiles_prefill_parity(name, alpha):
     print("mask: outside-band mismatches %d, in-band mismatches %d of %d in-band" % (ob, ibm, ib))
     assert ob == 0
     oout, olse = oracle.attend(inp, op, gmask)
-    err = np.abs(out - oout).max()
-    lerr = np.abs(lse - olse).max()
-    print("same-mask max-abs err %.3g (tol %g), lse err %.3g" % (err, gu.TOL[sp.dtype], lerr))
-    assert err <= gu.TOL[sp.dtype]
-    assert lerr <= gu.LSE_TOL[sp.dtype]
+    gu.check_close(out, oout, lse, olse, sp.dtype)
 
 
 @pytest.mark.parametrize("name", ["g4_paged", "g8_fp8_prefix"])
@@ -86,10 +82,8 @@ def test_tiles_attend_external_mask(name):
                           k_scale=d["k_scale"], v_scale=d["v_scale"], want_lse=True,
                           **gu.kv_args(wl, d))
     torch.cuda.synchronize()
-    err = np.abs(out.float().cpu().numpy() - oout).max()
-    print("external-mask err %.3g" % err)
-    assert err <= gu.TOL[sp.dtype]
-    assert np.abs(lse.cpu().numpy() - olse).max() <= gu.LSE_TOL[sp.dtype]
+    gu.check_close(out.float().cpu().numpy(), oout, lse.cpu().numpy(), olse, sp.dtype,
+                   label="external-mask")
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp8"])
@@ -159,9 +153,5 @@ def test_tiles_fullsize_sampled():
     print("mask on %d units: outside-band mismatches %d, in-band %d of %d" % (len(units), ob, ibm, ib))
     assert ob == 0
     oout, olse = oracle.attend(inp, op, gmask, units=units)
-    worst = 0.0
-    for rs, hs in gu.unit_rows(wl, units, query_tile_rows=R):
-        worst = max(worst, float(np.abs(out[rs, hs] - oout[rs, hs]).max()))
-        assert np.abs(lse[rs, hs] - olse[rs, hs]).max() <= gu.LSE_TOL["bf16"]
-    print("same-mask max-abs err on sampled units %.3g" % worst)
-    assert worst <= gu.TOL["bf16"]
+    gu.check_close(out, oout, lse, olse, "bf16", rows=gu.unit_rows(wl, units, query_tile_rows=R),
+                   label="same-mask (%d sampled units)" % len(units))
