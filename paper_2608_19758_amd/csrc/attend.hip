@@ -33,7 +33,8 @@
 //    transposing reads ds_read_b64_tr_b16 / _b8 (no transpose pass).
 // fp8 (OCP e4m3fn) uses v_mfma_f32_32x32x64_f8f6f4 on the raw codes; the
 // per-head scales c_q c_k are applied to the fp32 scores, the probabilities
-// are stored as e4m3(2^8 * exp(S - m)) (range [0, 256]) and the denominator
+// are stored as e4m3(2^8 * exp(S - m)) (range [0, 2^(8 + tau)] with the lazy
+// rescale below, tau = 0.8: at most 446 < 448) and the denominator
 // sums those stored values (Sec. 3.3 Eq. fp8); c_v is applied in the
 // epilogue and the 2^8 is removed from the LSE. Within a step the two waves
 // of a SIMD overlap each other's matrix and vector work; the vector issue
