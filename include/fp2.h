@@ -371,6 +371,30 @@ fp2_status_t fp2_calibrate(fp2_calib_kind_t kind, int32_t iters, float* sink, do
 fp2_status_t fp2_time_kernels(void* estimate_begin, void* estimate_end, void* attend_begin,
                               void* attend_end);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * fp2_prefill with its scratch memory in a static device array of the
+ * library, FP2_NOALLOC_SCRATCH_BYTES (96 MiB) on each GPU the library runs
+ * on, held until the process ends, instead of a caller workspace. Arguments,
+ * results and errors otherwise as fp2_prefill (the same kernels, so the same
+ * outputs bit for bit). Returns FP2_EWORKSPACE when fp2_workspace_bytes(params)
+ * exceeds the array: 128K-token sequences with 8 KV heads need about 69 MiB,
+ * and the need grows with batch * num_kv_heads * max_seq_len^2 / 2^14 bytes
+ * (the kept lists). The library allocates nothing for this call; the first
+ * call on a device resolves the array's address there (make that first call
+ * outside a graph capture). Every call on a GPU uses that GPU's one array,
+ * which keeps the last call's contents: calls that overlap on one GPU (other
+ * streams or host threads) race; calls in order on one stream are safe, since
+ * each call's kernels rebuild everything they read from it. */
+#define FP2_NOALLOC_SCRATCH_BYTES ((size_t)96 << 20)
+fp2_status_t fp2_prefill_noalloc(const fp2_params_t* params, const void* q,
+                                 const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                                 const int32_t* cu_seqlens_k, const int32_t* cu_seqlens_k_host,
+                                 const void* k_cache, const void* v_cache,
+                                 const int32_t* block_table, const float* q_scale,
+                                 const float* k_scale, const float* v_scale, void* out,
+                                 float* lse, uint8_t* block_mask, void* stream);
+
 /* Static description of a status code. */
 const char* fp2_status_str(fp2_status_t status);
 

@@ -49,7 +49,7 @@ class Params(ctypes.Structure):
 
 EXPORTS = ["fp2_workspace_bytes", "fp2_prefill", "fp2_estimate", "fp2_attend", "fp2_pool",
            "fp2_csr_capacity", "fp2_mask_to_csr", "fp2_means_cache_slots", "fp2_prefill_cached",
-           "fp2_calibrate", "fp2_time_kernels", "fp2_status_str",
+           "fp2_calibrate", "fp2_time_kernels", "fp2_prefill_noalloc", "fp2_status_str",
            "fp2_last_error"]
 
 CALIB_KINDS = {"mfma_bf16": 0, "mfma_fp8": 1, "exp": 2}
@@ -93,6 +93,8 @@ def lib():
         L.fp2_calibrate.argtypes = [ctypes.c_int, ctypes.c_int32, vp, ctypes.POINTER(ctypes.c_double), vp]
         L.fp2_time_kernels.restype = ctypes.c_int
         L.fp2_time_kernels.argtypes = [vp] * 4
+        L.fp2_prefill_noalloc.restype = ctypes.c_int
+        L.fp2_prefill_noalloc.argtypes = [P] + [vp] * 15
         L.fp2_status_str.restype = ctypes.c_char_p
         L.fp2_status_str.argtypes = [ctypes.c_int]
         L.fp2_last_error.restype = ctypes.c_char_p
@@ -316,6 +318,34 @@ def prefill(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *, cu_
         kh, vb, pooled = means_cache
         mc = MeansCache(_ptr(kh), _ptr(vb), _ptr(pooled))
         _check("fp2_prefill_cached", lib().fp2_prefill_cached(*head, ctypes.byref(mc), *tail))
+    return out, block_mask, lse
+
+
+NOALLOC_SCRATCH_BYTES = 96 << 20   # FP2_NOALLOC_SCRATCH_BYTES
+
+
+def prefill_noalloc(p: Params, q, k_cache, v_cache, cu_seqlens, block_table=None, *,
+                    cu_seqlens_host=None, cu_seqlens_k=None, cu_seqlens_k_host=None,
+                    q_scale=None, k_scale=None, v_scale=None, out=None, lse=None,
+                    block_mask=None, stream=None):
+    """fp2_prefill_noalloc: fp2_prefill with the library's static scratch array
+    instead of a workspace (the library allocates nothing; out, lse and
+    block_mask are allocated here when not given). Returns (out, block_mask,
+    lse)."""
+    if out is None:
+        out = torch.empty((q.shape[0], p.num_q_heads, p.head_dim), dtype=torch.bfloat16,
+                          device=q.device)
+    if block_mask is None:
+        block_mask = alloc_mask(p, q.device)
+    _check_inputs(p, q, k_cache, v_cache, cu_seqlens, block_table, cu_seqlens_k, q_scale,
+                  k_scale, v_scale, out, lse, block_mask)
+    st = lib().fp2_prefill_noalloc(ctypes.byref(p), _ptr(q), _ptr(cu_seqlens),
+                                   _host_ptr(cu_seqlens_host), _ptr(cu_seqlens_k),
+                                   _host_ptr(cu_seqlens_k_host), _ptr(k_cache), _ptr(v_cache),
+                                   _ptr(block_table), _ptr(q_scale), _ptr(k_scale),
+                                   _ptr(v_scale), _ptr(out), _ptr(lse), _ptr(block_mask),
+                                   _stream(stream))
+    _check("fp2_prefill_noalloc", st)
     return out, block_mask, lse
 
 

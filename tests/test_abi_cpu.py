@@ -278,3 +278,24 @@ def test_time_kernels_pairs():
     assert lib.fp2_time_kernels(None, None, None, ctypes.c_void_p(16)) == fp2.EINVAL
     assert "pairs" in fp2.last_error()
 
+
+def test_noalloc_limits_checked_before_any_device_call():
+    """The no-allocation prefill refuses a call whose scratch need exceeds the
+    static array (a host-side check, no GPU touched), and validates params as
+    fp2_prefill does; the 128K-token workloads with 8 KV heads fit."""
+    lib = fp2.lib()
+    for hq in (32, 64):
+        p = fp2.make_params(batch=1, num_q_heads=hq, num_kv_heads=8, max_seq_len=131072,
+                            page_size=64, max_pages_per_seq=2048, alpha=0.98, dtype="fp8")
+        assert 0 < fp2.workspace_bytes(p) <= fp2.NOALLOC_SCRATCH_BYTES
+    big = fp2.make_params(batch=4, num_q_heads=32, num_kv_heads=8, max_seq_len=131072,
+                          page_size=64, max_pages_per_seq=2048, alpha=0.98)
+    assert fp2.workspace_bytes(big) > fp2.NOALLOC_SCRATCH_BYTES
+    st = lib.fp2_prefill_noalloc(ctypes.byref(big), *([None] * 14), None)
+    assert st == fp2.EWORKSPACE
+    assert "static array" in fp2.last_error()
+    bad = fp2.make_params(batch=1, num_q_heads=3, num_kv_heads=2, max_seq_len=128)
+    assert lib.fp2_prefill_noalloc(ctypes.byref(bad), *([None] * 14), None) == fp2.EINVAL
+    # nothing to compute: OK without touching the device
+    empty = fp2.make_params(batch=0, num_q_heads=4, num_kv_heads=1, max_seq_len=128)
+    assert lib.fp2_prefill_noalloc(ctypes.byref(empty), *([None] * 14), None) == fp2.OK
