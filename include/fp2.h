@@ -133,7 +133,9 @@
  * mean_correction, every block J < I that is not kept adds
  * |B_J| * exp(scale * q . kbar_J) * vbar_J to the softmax numerator and
  * |B_J| * exp(scale * q . kbar_J) to its denominator (Sec. 3.2 Eq.
- * correction); kbar/vbar are the block means (stored in bf16 on the GPU).
+ * correction); kbar/vbar are the block means (stored in bf16 on the GPU; for
+ * fp8 inputs the correction uses their e4m3 codes, e4m3(kbar / k_scale) and
+ * e4m3(vbar / v_scale), on the fp8 matrix cores).
  *
  * fp8 (Sec. 3.3 Eq. fp8): scores are c_q c_k (q~ . k~) from the e4m3 codes;
  * the probabilities of kept keys are rounded to e4m3 as P~ = e4m3(2^8 *

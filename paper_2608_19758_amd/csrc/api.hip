@@ -57,7 +57,8 @@ constexpr int kMaxSplits = 32;            // parts per unit (one per lane of the
 constexpr size_t kPartialRows = 65536;    // packed rows of partial outputs, cost-balanced mode
 
 struct Layout {
-  size_t khat, vbar, kidx, kcnt, items, rowinfo, splitrows, counts, part_o, part_ml, total;
+  size_t khat, vbar, khat8, vbar8, kidx, kcnt, items, rowinfo, splitrows, counts, part_o, part_ml,
+      total;
   int32_t cap_items, cap_slots;
 };
 
@@ -88,6 +89,12 @@ Layout layout_of(const fp2_params_t* p) {
   off = align256(off + krows * fp2::kHeadDim * sizeof(uint16_t));
   l.vbar = off;
   off = align256(off + krows * fp2::kHeadDim * sizeof(uint16_t));
+  if (p->dtype == FP2_FP8_E4M3) {   // e4m3 code means for the fp8 correction
+    l.khat8 = off;
+    off = align256(off + krows * fp2::kHeadDim);
+    l.vbar8 = off;
+    off = align256(off + krows * fp2::kHeadDim);
+  }
   l.kidx = off;
   off = align256(off + rows * nbk_of(p) * sizeof(int32_t));
   l.kcnt = off;
@@ -274,6 +281,8 @@ Views views_of(const fp2_params_t* p, void* ws) {
   Views v;
   v.pooled.khat = (uint16_t*)(base + l.khat);
   v.pooled.vbar = (uint16_t*)(base + l.vbar);
+  v.pooled.khat8 = l.khat8 ? (uint8_t*)(base + l.khat8) : nullptr;
+  v.pooled.vbar8 = l.vbar8 ? (uint8_t*)(base + l.vbar8) : nullptr;
   v.kl.idx = (int32_t*)(base + l.kidx);
   v.kl.cnt = (int32_t*)(base + l.kcnt);
   v.plan.items = (int2*)(base + l.items);
@@ -475,7 +484,7 @@ fp2_status_t fp2_pool(const fp2_params_t* params, const int32_t* cu_seqlens,
   if (!khat || !vbar) return fail(FP2_EINVAL, "khat or vbar is null");
   const fp2::Problem pr = make_problem(&pp, nullptr, cu_seqlens, nullptr, k_cache, v_cache,
                                        block_table, nullptr, k_scale, v_scale);
-  fp2::Pooled pooled{(uint16_t*)khat, (uint16_t*)vbar};
+  fp2::Pooled pooled{(uint16_t*)khat, (uint16_t*)vbar, nullptr, nullptr};
   return hip_status(fp2::launch_pool(pr, pooled, (hipStream_t)stream), "fp2_pool launch");
 }
 

@@ -42,9 +42,11 @@
 // (masking only on the diagonal and last correction steps, constants held
 // in registers across steps).
 // bf16 uses v_mfma_f32_32x32x16_bf16. Correction steps use the pooled means
-// as keys khat_J and values vbar_J (bf16, real units, bf16 MFMA for both
-// dtypes), logits shifted by log2|B_J| = 7 (Sec. 3.2 implementation
-// paragraph).
+// as keys and values, logits shifted by log2|B_J| = 7 (Sec. 3.2
+// implementation paragraph): for bf16 the bf16 means khat_J, vbar_J with bf16
+// MFMA; for fp8 their e4m3 codes (khat_J / c_k, vbar_J / c_v, quantized as
+// Sec. 4 quantizes the pooled statistics under fp8) with the same fp8 steps
+// as the kept keys.
 //
 // Prefix KV (chunked prefill, prefix caching): the queries of a sequence may
 // be the last L_q of its L_kv keys. Keys, key blocks and the pooled means are
@@ -487,10 +489,13 @@ __device__ __forceinline__ int pack_e4m3x4(float a, float b, float c, float d) {
 // and of query n+16 (k-groups 1 and 3), so a 0/1 selector A operand whose
 // row m picks the k-groups of parity (m/4)%2 leaves in every element of lane
 // l the row sum of the lane's own query l%32.
-template <int RT>
+// KIND 0: kept keys key0 .. key0+63, masked against pos when `diag`. KIND 1:
+// correction (e4m3 code means as keys and values), column k used iff k < nv
+// (masked when `diag`), logits shifted by log2 |B_J| = 7.
+template <int KIND, int RT>
 __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState<RT>& rs, float cs,
                                         int key0, const int (&pos)[RT], bool diag, int lane,
-                                        const i32x8_t& sel) {
+                                        const i32x8_t& sel, int nv = kStep) {
   const int half = lane >> 5;
   auto& s = S.v;
   i32x8_t va[4];
@@ -505,10 +510,12 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int key = 32 * u + 8 * i + 4 * half + j;
-            s[rt][u][4 * i + j] = (key0 + key > pos[rt]) ? -INFINITY : s[rt][u][4 * i + j];
+            const bool drop = KIND == 1 ? key >= nv : key0 + key > pos[rt];
+            s[rt][u][4 * i + j] = drop ? -INFINITY : s[rt][u][4 * i + j];
           }
     }
-    const float bias = softmax_rescale<2, true>(s[rt], rs, rt, cs, 0.0f, 8.0f, kTauFp8);
+    const float bias = softmax_rescale<2, true>(s[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, 8.0f,
+                                                kTauFp8);
     int pk[8];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
@@ -643,6 +650,20 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
     const float off = FP8 ? 8.f : 0.f;        // log2 of the probability offset
     asm volatile("" : "+v"(qsc), "+v"(vsc), "+v"(ksc));  // loads complete before the rings
 
+    // fp8: the query codes (B operand of the score products) and the selector
+    // A operand of the row-sum MFMA: lane l holds row l%16, k-group l/16 of A,
+    // all e4m3 1.0 (0x38) where the row's parity (l%16)/4 matches the
+    // k-group's, else 0; opaque so that it stays in registers instead of being
+    // rebuilt every step. Both serve the kept keys and the correction.
+    i32x8_t qf[FP8 ? RT : 1][2];
+    i32x8_t sel;
+    if constexpr (FP8) {
+      const int selw = (((lane & 15) >> 2) & 1) == ((lane >> 4) & 1) ? 0x38383838 : 0;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) sel[k] = selw;
+      asm volatile("" : "+v"(sel));
+    }
+
     // ---- kept blocks: step s of a chunk -> its block list entry s/2, half s%2
     {
       const uint8_t* K = (const uint8_t*)p.k;
@@ -674,7 +695,6 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
         return (uint32_t)ptab[pi] * (uint32_t)page + (uint32_t)(t - pi * page);
       };
 
-      i32x8_t qf[FP8 ? RT : 1][2];
       bf16x8_t qb[FP8 ? 1 : RT][8];
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
@@ -738,22 +758,13 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
         };
         const int nst = 2 * nbc;
         if constexpr (FP8) {
-          // selector A operand of the row-sum MFMA: lane l holds row l%16,
-          // k-group l/16 of A, all e4m3 1.0 (0x38) where the row's parity
-          // (l%16)/4 matches the k-group's, else 0; opaque so that it stays in
-          // registers instead of being rebuilt every step
-          const int selw = (((lane & 15) >> 2) & 1) == ((lane >> 4) & 1) ? 0x38383838 : 0;
-          i32x8_t sel;
-#pragma unroll
-          for (int k = 0; k < 8; ++k) sel[k] = selw;
-          asm volatile("" : "+v"(sel));
           run_steps<W, 1, RT, RING>(
               ring, nst, K, V, fetch, addr,
               [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
               [&](const uint4* st, Scores<RT>& S, int s) {
                 const int wp = c0 + (s >> 1);   // walk position of the step's block
-                fin_fp8<RT>(st, S, rs, cs, (wp == 0 ? e0 : e1) * kBlock + kStep * (s & 1), pos,
-                            wp < nmask, lane, sel);
+                fin_fp8<0, RT>(st, S, rs, cs, (wp == 0 ? e0 : e1) * kBlock + kStep * (s & 1), pos,
+                               wp < nmask, lane, sel);
               },
               tid);
         } else {
@@ -771,11 +782,6 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
       }
     }
 
-    if constexpr (FP8) {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) rs.l[rt] += half == 0 ? rs.ls[rt][0] : 0.f;
-    }
-
     // ---- mean correction over the pruned blocks J < Ja (fully visible to
     // every row of the unit), compacted into a list; split sp takes the
     // blocks J in [jlo, jhi)
@@ -784,32 +790,27 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
     if (p.corr && jhi > jlo) {
       const uint8_t* mrow = mask + row * p.nbk;
       uint16_t* plist = (uint16_t*)aux;
-      // Q as bf16 (fp8 codes widen exactly); the fp8 scale goes into cs.
-      bf16x8_t qb[RT][8];
+      // bf16: Q and the bf16 means, bf16 steps (the log2 |B_J| = 7 shift in the
+      // logits). fp8: the query codes and the e4m3 code means of keys and
+      // values, fp8 steps like the kept keys (scores scaled by c_q c_k, value
+      // codes by c_v at the end, P~ in e4m3 with its row sums from the
+      // selector MFMA).
+      bf16x8_t qb[FP8 ? 1 : RT][8];
+      if constexpr (!FP8) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int ds = 0; ds < 8; ++ds) {
-          uint4 v = make_uint4(0, 0, 0, 0);
-          if (qvalid[rt]) {
-            if (!FP8) {
-              v = *(const uint4*)((const uint16_t*)p.q + qoff[rt] + 16 * ds + 8 * half);
-            } else {
-              const uint2 cc = *(const uint2*)((const uint8_t*)p.q + qoff[rt] + 16 * ds + 8 * half);
-              const uint2 lo = e4m3x4_to_bf16(cc.x), hi = e4m3x4_to_bf16(cc.y);
-              v = make_uint4(lo.x, lo.y, hi.x, hi.y);
-            }
+          for (int ds = 0; ds < 8; ++ds) {
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (qvalid[rt]) v = *(const uint4*)((const uint16_t*)p.q + qoff[rt] + 16 * ds + 8 * half);
+            qb[rt][ds] = __builtin_bit_cast(bf16x8_t, v);
+            asm volatile("" : "+v"(qb[rt][ds]));
           }
-          qb[rt][ds] = __builtin_bit_cast(bf16x8_t, v);
-          asm volatile("" : "+v"(qb[rt][ds]));
-        }
-      // fp8: O accumulates code-valued V (c_v applied at the end), so the
-      // real-valued vbar enters with weight 1/c_v.
-      const float pv_scale = FP8 ? 1.f / vsc : 1.f;
-      const float cs = p.scale_log2 * qsc;
+      }
+      const float cs = FP8 ? p.scale_log2 * qsc * ksc : p.scale_log2;
       const int64_t pbase = ((int64_t)b * p.hkv + h) * p.nbk * kHeadDim;
-      const uint8_t* Kh = (const uint8_t*)(pooled.khat + pbase);
-      const uint8_t* Vh = (const uint8_t*)(pooled.vbar + pbase);
+      const uint8_t* Kh = FP8 ? pooled.khat8 + pbase : (const uint8_t*)(pooled.khat + pbase);
+      const uint8_t* Vh = FP8 ? pooled.vbar8 + pbase : (const uint8_t*)(pooled.vbar + pbase);
 #pragma unroll 1
       for (int j0 = jlo; j0 < jhi; j0 += kPlist) {
         const int j1 = min(jhi, j0 + kPlist);
@@ -840,17 +841,34 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
         auto addr = [&](int J, int s, int r) -> int64_t {
           (void)s;
           (void)r;
-          return (int64_t)J * kHeadDim * 2;
+          return (int64_t)J * kHeadDim * (FP8 ? 1 : 2);
         };
-        run_steps<W, 0, RT, RING>(
-            ring, (np + kStep - 1) / kStep, Kh, Vh, fetch, addr,
-            [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
-            [&](const uint4* st, Scores<RT>& S, int s) {
-              fin_bf16<1, RT, NPRE>(st, S, rs, cs, off, pv_scale, 0, pos, false, np - kStep * s,
-                                    lane);
-            },
-            tid);
+        if constexpr (FP8) {
+          run_steps<W, 1, RT, RING>(
+              ring, (np + kStep - 1) / kStep, Kh, Vh, fetch, addr,
+              [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
+              [&](const uint4* st, Scores<RT>& S, int s) {
+                const int nv = np - kStep * s;
+                fin_fp8<1, RT>(st, S, rs, cs, 0, pos, nv < kStep, lane, sel, nv);
+              },
+              tid);
+        } else {
+          run_steps<W, 0, RT, RING>(
+              ring, (np + kStep - 1) / kStep, Kh, Vh, fetch, addr,
+              [&](const uint4* st, Scores<RT>& S) { qk_bf16<RT>(st, qb, S, lane); },
+              [&](const uint4* st, Scores<RT>& S, int s) {
+                fin_bf16<1, RT, NPRE>(st, S, rs, cs, off, 1.f, 0, pos, false, np - kStep * s,
+                                      lane);
+              },
+              tid);
+        }
       }
+    }
+
+    // fp8: the row sums of P~ from the matrix cores join the denominator
+    if constexpr (FP8) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) rs.l[rt] += half == 0 ? rs.ls[rt][0] : 0.f;
     }
 
     // epilogue: O = c_v O^T / l, LSE = (m + log2 l - off) ln 2; with KV

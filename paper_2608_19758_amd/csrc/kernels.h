@@ -35,8 +35,10 @@ struct Problem {
 
 // Workspace views.
 struct Pooled {
-  uint16_t* khat;           // [batch, Hkv, nbk, d] bf16 key means (scoring and correction)
-  uint16_t* vbar;           // [batch, Hkv, nbk, d] bf16 value means (correction)
+  uint16_t* khat;           // [batch, Hkv, nbk, d] bf16 key means (scoring; bf16 correction)
+  uint16_t* vbar;           // [batch, Hkv, nbk, d] bf16 value means (bf16 correction)
+  uint8_t* khat8;           // fp8 inputs: [batch, Hkv, nbk, d] e4m3 code means of the keys,
+  uint8_t* vbar8;           // e4m3(khat / k_scale), and of the values (fp8 correction); else null
 };
 
 // Block means kept by the caller across calls (chunked prefill, prefix

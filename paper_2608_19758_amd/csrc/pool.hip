@@ -15,7 +15,11 @@
 //    division rounds once).
 // The rounded key mean khat (bf16, one rounding from fp64) is the scoring key
 // of Eq. fused_score and the surrogate key of the correction; vbar is the
-// value mean in bf16. With a caller's means cache (chunked prefill), complete
+// value mean in bf16. For fp8 inputs the correction runs on the matrix cores
+// in fp8 like the kept keys (the pooled statistics quantized as Sec. 4 does
+// under fp8): the kernel also writes the e4m3 code means e4m3(khat / k_scale)
+// and e4m3(vbar / v_scale), derived from the bf16 means so that blocks taken
+// from a means cache give the same codes. With a caller's means cache (chunked prefill), complete
 // blocks it already holds are copied from it (512 bytes per block and head
 // instead of the block's K/V), and every block pooled here is written to it.
 #include "kernels.h"
@@ -50,18 +54,32 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out, M
   const int L = p.cuk[b + 1] - (int)tok0;     // KV tokens, a prefix included
   const int64_t obase = (((int64_t)b * p.hkv + h) * p.nbk + J) * kHeadDim;
   const int n = (L + kBlock - 1) / kBlock;
+  // fp8: the e4m3 code means, from the bf16 means (|mean code| <= 448)
+  auto store8 = [&](uint16_t kh, uint16_t vb) {
+    if (FP8 && out.khat8) {
+      const float kc = __uint_as_float((uint32_t)kh << 16) / p.k_scale[h];
+      const float vc = __uint_as_float((uint32_t)vb << 16) / p.v_scale[h];
+      out.khat8[obase + tid] = (uint8_t)(__builtin_amdgcn_cvt_pk_fp8_f32(
+                                             fminf(fmaxf(kc, -448.f), 448.f), 0.f, 0, false) & 0xFF);
+      out.vbar8[obase + tid] = (uint8_t)(__builtin_amdgcn_cvt_pk_fp8_f32(
+                                             fminf(fmaxf(vc, -448.f), 448.f), 0.f, 0, false) & 0xFF);
+    }
+  };
   if (J >= n) {
     if (tid < kHeadDim) {
       out.khat[obase + tid] = 0;
       out.vbar[obase + tid] = 0;
+      store8(0, 0);
     }
     return;
   }
   const int64_t cbase = mc.khat ? cache_offset(p, mc, b, J, h) : 0;
   if (mc.khat && J < min(mc.pooled[b], L / kBlock)) {   // complete block, already pooled
     if (tid < kHeadDim) {
-      out.khat[obase + tid] = mc.khat[cbase + tid];
-      out.vbar[obase + tid] = mc.vbar[cbase + tid];
+      const uint16_t kh = mc.khat[cbase + tid], vb = mc.vbar[cbase + tid];
+      out.khat[obase + tid] = kh;
+      out.vbar[obase + tid] = vb;
+      store8(kh, vb);
     }
     return;
   }
@@ -69,6 +87,7 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(Problem p, Pooled out, M
   auto store = [&](uint16_t kh, uint16_t vb) {
     out.khat[obase + tid] = kh;
     out.vbar[obase + tid] = vb;
+    store8(kh, vb);
     if (mc.khat) {
       mc.khat[cbase + tid] = kh;
       mc.vbar[cbase + tid] = vb;

@@ -17,11 +17,13 @@ BAND = 1e-4                         # relative distance of a block energy from t
 # with 3 mantissa bits moves each term by at most 2^-4 of itself, so the sum,
 # and its log, by at most ln(1 + 2^-4) < 0.0625.
 LSE_TOL = {"bf16": 1e-2, "fp8": 0.0625}
-# Regression gates beside the parity bars, about twice the largest errors
-# measured over every GPU test case (bf16: relative Frobenius 2.5e-3, LSE
-# 4.9e-4, from fp32 arithmetic and one bf16 rounding of O; fp8: relative
-# Frobenius 2.4e-2, LSE 2.75e-2, from the e4m3 probabilities of Eq. fp8, whose
-# worst rows are early positions where a few keys carry the whole mass).
+# Regression gates beside the parity bars, above the largest errors measured
+# over every GPU test case (bf16: relative Frobenius 2.5e-3, LSE 4.9e-4, from
+# fp32 arithmetic and one bf16 rounding of O; fp8: relative Frobenius 3.3e-2
+# on the tail chunks of the 128K sequence, whose outputs are ~1e-2 in size and
+# carried mostly by the correction on e4m3 code means, LSE 2.75e-2 from the
+# e4m3 probabilities of Eq. fp8 on early positions, where a few keys carry the
+# whole mass).
 REL_GATE = {"bf16": 5e-3, "fp8": 4e-2}
 LSE_GATE = {"bf16": 1e-3, "fp8": 4.5e-2}
 

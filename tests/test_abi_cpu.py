@@ -142,6 +142,8 @@ def ws_parts(p):
         slots = rows * p.kv_splits if p.kv_splits > 1 else 0
         items = wpu * rows * p.kv_splits
     n = 2 * al(krows * 256) + al(rows * fp2.num_key_blocks(p) * 4) + al(rows * 4)
+    if p.dtype == fp2.FP8_E4M3:
+        n += 2 * al(krows * 128)   # e4m3 code means of K and V (the fp8 correction)
     n += al(items * 8) + al(rows * 8) + al((slots // 2 + 1) * 4) + 256
     if slots:
         n += al(slots * rpu * 512) + al(slots * rpu * 8)
@@ -152,7 +154,8 @@ def ws_parts(p):
                                 dict(num_q_heads=64, kv_splits=0), dict(num_q_heads=8),
                                 dict(max_kv_len=12288, max_pages_per_seq=192, kv_splits=3),
                                 dict(query_tile_rows=128), dict(query_tile_rows=128, kv_splits=2),
-                                dict(num_q_heads=64, query_tile_rows=128)])
+                                dict(num_q_heads=64, query_tile_rows=128), dict(dtype="fp8"),
+                                dict(dtype="fp8", max_kv_len=12288, max_pages_per_seq=192)])
 def test_workspace_sections(kw):
     p = base(**kw)
     assert fp2.workspace_bytes(p) == ws_parts(p)
