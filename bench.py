@@ -306,9 +306,11 @@ def measure(cfg, steps, warmup):
                                  tile_rows=cfg["p"].query_tile_rows)
     t_attn = max(1e-6, t_attn)
     main_peak = PEAK_TFLOPS[sp.dtype]
-    # time-weighted peak: kept tiles run at the dtype's MFMA peak, the
-    # correction chunks on bf16 MFMA
-    mix = (fk + fc) / (fk / main_peak + fc / PEAK_TFLOPS["bf16"]) if (fk + fc) else main_peak
+    # time-weighted peak of the MFMA types the kernel issues: the kept tiles
+    # and the correction chunks both run on the workload dtype's MFMA (fp8
+    # inputs score the pooled means' e4m3 codes), so it is the dtype's peak
+    corr_peak = main_peak
+    mix = (fk + fc) / (fk / main_peak + fc / corr_peak) if (fk + fc) else main_peak
     achieved = (fk + fc) / (t_attn * 1e-3) / 1e12
     est_bytes = acc.estimation_bytes(sp.seqlens, sp.num_q_heads, sp.num_kv_heads,
                                      elem=1 if sp.dtype == "fp8" else 2)
@@ -652,11 +654,12 @@ def main():
         "latency_ms": {"prefill": round(m["ms_per_step"], 4),
                        "estimate_kernels": round(m["estimate_ms"], 4),
                        "attention_kernel": round(m["attention_ms"], 4)},
-        # the attention kernel: executed FLOPs (kept blocks at the dtype's
-        # MFMA rate, the correction's pooled keys on bf16 MFMA) over its own
+        # the attention kernel: executed FLOPs (kept blocks and the
+        # correction's pooled keys, both on the dtype's MFMA) over its own
         # duration (HIP events recorded by the library right around its
         # launch in every timed step), against the dtype's MFMA peak; frac_mix
-        # against the time-weighted peak of the two MFMA rates
+        # against the time-weighted peak of the MFMA types issued (equal to
+        # frac since the correction runs on the same type)
         "roofline": {"bound": "mfma", "kernel": "attend_kernel",
                      "achieved": round(att["achieved_tflops"], 2),
                      "peak": round(att["peak_tflops"], 1), "unit": "TFLOP/s",

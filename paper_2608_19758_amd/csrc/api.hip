@@ -100,7 +100,7 @@ Layout layout_of(const fp2_params_t* p) {
   l.kcnt = off;
   off = align256(off + rows * sizeof(int32_t));
   l.items = off;
-  off = align256(off + items * 2 * sizeof(int32_t));
+  off = align256(off + items * 4 * sizeof(int32_t));
   l.rowinfo = off;
   off = align256(off + rows * 2 * sizeof(int32_t));
   l.splitrows = off;
@@ -285,7 +285,7 @@ Views views_of(const fp2_params_t* p, void* ws) {
   v.pooled.vbar8 = l.vbar8 ? (uint8_t*)(base + l.vbar8) : nullptr;
   v.kl.idx = (int32_t*)(base + l.kidx);
   v.kl.cnt = (int32_t*)(base + l.kcnt);
-  v.plan.items = (int2*)(base + l.items);
+  v.plan.items = (int4*)(base + l.items);
   v.plan.rowinfo = (int2*)(base + l.rowinfo);
   v.plan.splitrows = (int32_t*)(base + l.splitrows);
   v.plan.counts = (int32_t*)(base + l.counts);

@@ -110,12 +110,6 @@ __device__ __forceinline__ void wait_ahead(int ahead) {
   else wait_vmcnt<6 * D>();
 }
 
-// Workgroup barrier for LDS traffic: this wave's LDS operations complete,
-// then all waves meet. Outstanding global->LDS copies are not waited for.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"   // m0 is reserved; nothing else here uses it
 // 16-byte copy global -> LDS (global_load_lds_dwordx4): lane i writes LDS
@@ -567,20 +561,15 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
   const int tid0 = threadIdx.x;
 
   // Persistent workgroups: items of the plan's table (unit, KV split, row
-  // slice; decreasing query block, i.e. heaviest first) are taken in order
-  // from a counter; the loop ends for every wave once the counter passes the
-  // last item.
+  // slice, and the unit's split count and partial slot; decreasing query
+  // block, i.e. heaviest first) are taken in order from a counter; the loop
+  // ends for every wave once the counter passes the last item.
 #pragma unroll 1
   for (;;) {
     if (tid0 == 0) {
       const int it = atomicAdd(plan.counts, 1);
       int4 v = make_int4(-1, 0, 0, 0);
-      if (it < plan.counts[1]) {
-        const int2 e = plan.items[it];
-        const int I = p0.nbmax - 1 - e.x / nbh;
-        const int2 ri = plan.rowinfo[(e.x % nbh) * p0.nbmax + I];
-        v = make_int4(e.x, e.y, ri.x, ri.y);
-      }
+      if (it < plan.counts[1]) v = plan.items[it];
       s_item = v;
     }
     __syncthreads();
@@ -606,15 +595,15 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
     const int I = p.nbmax - 1 - u / nbh;
     const int bh = u % nbh;
     const int b = bh / p.hkv, h = bh % p.hkv;
-    const int Lq = p.cu[b + 1] - p.cu[b];
+    const int Lq = ld_uniform(p.cu, b + 1) - ld_uniform(p.cu, b);
     if (I * p.qtile >= Lq) continue;
     // KV tokens of the sequence (a prefix included) and the key blocks Ja,
     // Jb of the unit's first and last row; positions below are absolute, and
     // query position x is packed row qbase + x
-    const int64_t tok0 = p.cuk[b];
-    const int L = p.cuk[b + 1] - (int)tok0;
+    const int64_t tok0 = ld_uniform(p.cuk, b);
+    const int L = ld_uniform(p.cuk, b + 1) - (int)tok0;
     const int Ja = (L - Lq + I * p.qtile) / kBlock;
-    const int64_t qbase = (int64_t)p.cu[b] - (L - Lq);
+    const int64_t qbase = (int64_t)ld_uniform(p.cu, b) - (L - Lq);
 
     const int lane = tid & 63, w = tid >> 6;
     const int half = lane >> 5, l32 = lane & 31;
@@ -645,8 +634,8 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
       rs.l[rt] = 0.f;
     }
     float qsc = FP8 ? p.q_scale[hq] : 1.f;
-    float vsc = FP8 ? p.v_scale[h] : 1.f;
-    float ksc = FP8 ? p.k_scale[h] : 1.f;
+    float vsc = FP8 ? ld_uniform(p.v_scale, h) : 1.f;
+    float ksc = FP8 ? ld_uniform(p.k_scale, h) : 1.f;
     const float off = FP8 ? 8.f : 0.f;        // log2 of the probability offset
     asm volatile("" : "+v"(qsc), "+v"(vsc), "+v"(ksc));  // loads complete before the rings
 
@@ -669,11 +658,11 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
       const uint8_t* K = (const uint8_t*)p.k;
       const uint8_t* V = (const uint8_t*)p.v;
       constexpr int esz = FP8 ? 1 : 2;
-      const int cnt = kl.cnt[row];
+      const int cnt = ld_uniform(kl.cnt, row);
       const int32_t* kidx = kl.idx + row * p.nbk;
       // Kept blocks J >= Ja hold keys after some row of the unit and need the
       // causal mask: at most two (Ja and Jb), the first of the descending walk.
-      const int e0 = cnt > 0 ? kidx[cnt - 1] : -1, e1 = cnt > 1 ? kidx[cnt - 2] : -1;
+      const int e0 = cnt > 0 ? ld_uniform(kidx, cnt - 1) : -1, e1 = cnt > 1 ? ld_uniform(kidx, cnt - 2) : -1;
       const int nmask = (e0 >= Ja) + (e1 >= Ja);
       // Eq. split: part sp walks list positions [lo, hi) of the descending
       // walk, ceil(cnt / nsp) each

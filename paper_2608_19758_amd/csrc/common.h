@@ -100,6 +100,21 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Workgroup barrier for LDS traffic: this wave's LDS operations complete,
+// then all waves meet. Unlike __syncthreads(), outstanding global loads (and
+// global->LDS copies) are not waited for, so prefetches stay in flight.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Read-only metadata (sequence offsets, per-head scales) at a wave-uniform
+// index through the constant address space: a scalar load, which waits only
+// on the scalar counter, not behind the vector loads a kernel has in flight.
+template <class T>
+__device__ __forceinline__ T ld_uniform(const T* ptr, int64_t i) {
+  return ((const __attribute__((address_space(4))) T*)ptr)[i];
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 

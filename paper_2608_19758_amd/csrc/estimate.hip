@@ -42,6 +42,7 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kChunksPerWave = 4;                          // 4 x 32 key blocks per wave
 constexpr int kGroup = kWaves * kChunksPerWave * 32;       // key blocks per pass (1024)
 constexpr int kQRow = 17;                                  // LDS row stride of a Q tile, 16-byte slots
+constexpr int kBufferWord3 = 0x00020000;                   // buffer resource word 3 (gfx9: raw 32-bit data)
 
 // Row split of the scoring for calls with few units (short chunks): part u
 // of parts.n scores the unit's 32-row tiles [u ceil(T/n), ...) and writes
@@ -130,14 +131,15 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
   const int I = p.nbmax - 1 - uidx / nbh;
   const int bh = uidx % nbh;
   const int b = bh / p.hkv, h = bh % p.hkv;
-  const int lane = tid & 63, w = tid >> 6;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: branches on it are scalar
   const int half = lane >> 5, l32 = lane & 31;
-  const int64_t tok0 = p.cu[b];
-  const int L = p.cu[b + 1] - (int)tok0;
+  const int64_t tok0 = ld_uniform(p.cu, b);
+  const int L = ld_uniform(p.cu, b + 1) - (int)tok0;
   const int n = (L + p.qtile - 1) / p.qtile;   // query tiles of the sequence
   // KV tokens and key blocks; the rows of query tile I lie in key blocks
   // Ja .. Ib (Ib = Ja + 1 when the tile straddles a key-block boundary)
-  const int Lk = p.cuk[b + 1] - p.cuk[b];
+  const int Lk = ld_uniform(p.cuk, b + 1) - ld_uniform(p.cuk, b);
   const int nk = (Lk + kBlock - 1) / kBlock;
   const int Ja = (Lk - L + I * p.qtile) / kBlock;
   const int Ia = (Lk - L + min(L, (I + 1) * p.qtile) - 1) / kBlock;   // last visible key block
@@ -167,28 +169,39 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
 
   // Row r = 8i + 4*half + j of a 32-row tile has head offset (4*half + j) % G.
   float cs[4];
+  if constexpr (FP8) {
+    float sc[G];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    int hd = (4 * half + j) % G;
-    cs[j] = FP8 ? p.scale_log2 * p.q_scale[h * G + hd] : p.scale_log2;
+    for (int k = 0; k < G; ++k) sc[k] = p.scale_log2 * ld_uniform(p.q_scale, h * G + k);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cs[j] = half ? sc[(4 + j) % G] : sc[j % G];
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cs[j] = p.scale_log2;
   }
 
-  const uint16_t* khat = pooled.khat + ((int64_t)b * p.hkv + h) * p.nbk * kHeadDim;
+  // Pooled keys through a buffer resource over this unit's blocks 0 .. Ia:
+  // blocks past its last one read as zero keys, without a branch.
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(pooled.khat + ((int64_t)b * p.hkv + h) * p.nbk * kHeadDim), (short)0,
+      (Ia + 1) * kHeadDim * 2, kBufferWord3);
+  // Q rows of this unit as a buffer resource (rows past the tile read as zero).
+  constexpr int esz = FP8 ? 1 : 2;
+  const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)((const char*)p.q + (tok0 + (int64_t)I * p.qtile) * p.hq * kHeadDim * esz), (short)0,
+      npos * p.hq * kHeadDim * esz, kBufferWord3);
 
   // This thread's 16 bytes of Q tile t (bf16: row tid/16, chunk tid%16;
   // fp8: threads < 256, row tid/8, 16 codes tid%8), zero past the block.
   auto qload = [&](int t) -> uint4 {
-    uint4 v = make_uint4(0, 0, 0, 0);
     const int r = FP8 ? tid >> 3 : tid >> 4;
     const int pr = t * 32 + r;
-    if (t < thi && pr < nrows && (!FP8 || tid < 256)) {
-      const int pos = I * p.qtile + pr / G, hq = h * G + pr % G;
-      if (FP8)
-        v = *(const uint4*)((const uint8_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + (tid & 7) * 16);
-      else
-        v = *(const uint4*)((const uint16_t*)p.q + ((tok0 + pos) * p.hq + hq) * kHeadDim + (tid & 15) * 8);
-    }
-    return v;
+    const int off = ((pr / G) * p.hq + h * G + pr % G) * (kHeadDim * esz) + (FP8 ? tid & 7 : tid & 15) * 16;
+    // tiles past the item's last and fp8 threads past the 256 that cover a
+    // tile fetch nothing (an offset past the buffer reads zero)
+    const bool ok = t < thi && (!FP8 || tid < 256);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(qrs, ok ? off : 0x7ffffff0, 0, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
   };
   // Store it into LDS buffer qb (fp8 codes widened to bf16, exact). Rows are
   // kQRow 16-byte slots apart: a lane's eight reads of its row then share
@@ -221,11 +234,11 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       m[c] = -INFINITY;
       E[c] = 0.f;
       const int J = J0 + l32;
+      if (act[c]) {   // (an inactive chunk is never scored)
 #pragma unroll
-      for (int ds = 0; ds < 8; ++ds) {
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (act[c] && J <= Ia) v = *(const uint4*)(khat + (int64_t)J * kHeadDim + 16 * ds + 8 * half);
-        kf[c][ds] = __builtin_bit_cast(bf16x8_t, v);
+        for (int ds = 0; ds < 8; ++ds)
+          kf[c][ds] = __builtin_bit_cast(
+              bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(krs, J * (kHeadDim * 2) + 32 * ds + 16 * half, 0, 0));
       }
     }
 

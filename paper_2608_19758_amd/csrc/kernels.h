@@ -65,7 +65,9 @@ struct KeptLists {
 // row = (b * Hkv + h) * nbmax + I; the attention order is q = (nbmax - 1 - I)
 // * (batch * Hkv) + b * Hkv + h (decreasing query block, heaviest first).
 struct Plan {
-  int2* items;              // [cap_items] {q, k}: split k / wpu, row slice k % wpu
+  int4* items;              // [cap_items] {q, k, U, first partial slot or -1}: unit q in
+                            // attention order, split k / wpu, row slice k % wpu, and the
+                            // unit's rowinfo entry (so one load describes an item)
   int2* rowinfo;            // [rows] {splits U, first partial slot or -1}
   int32_t* splitrows;       // [cap_slots / 2] unit rows with U > 1
   int32_t* counts;          // [0] work counter (zeroed by the plan), [1] items, [2] split rows

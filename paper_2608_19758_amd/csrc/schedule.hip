@@ -213,12 +213,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(Problem p, KeptLists
       if (in_lds) plan.rowinfo[row] = make_int2(-1, -1);
       continue;
     }
-    plan.rowinfo[row] = make_int2(U, U > 1 ? bs : -1);
+    const int slot = U > 1 ? bs : -1;
+    plan.rowinfo[row] = make_int2(U, slot);
     if (U > 1) {
       plan.splitrows[bsr++] = row;
       bs += U;
     }
-    for (int k = 0; k < U * wpu; ++k) plan.items[bi + k] = make_int2(q, k);
+    for (int k = 0; k < U * wpu; ++k) plan.items[bi + k] = make_int4(q, k, U, slot);
     bi += U * wpu;
   }
   if (tid == 0) {

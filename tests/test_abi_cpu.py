@@ -41,14 +41,14 @@ def test_workspace_bytes():
     rows = 2 * 8 * nb
     want = rows * 128 * 2 * 2 + rows * nb * 4 + rows * 4 + 256   # + the work counters
     got = fp2.workspace_bytes(p)
-    assert want <= got <= want + rows * 2 * 8 * 2 + 8 * 256     # + item table and unit info
+    assert want <= got <= want + rows * 2 * 16 + rows * 8 + 8 * 256   # + item table and unit info
     assert fp2.workspace_bytes(base(head_dim=64)) == 0
     assert fp2.workspace_bytes(base(batch=0)) == 0
     # prefix KV: pooled rows and list columns per key block, list rows per query block
     pk = base(max_kv_len=3 * 4096, max_pages_per_seq=192, kv_splits=1)
     nq, nk = 32, 96
     want = 2 * 8 * (nk * 128 * 2 * 2 + nq * nk * 4 + nq * 4) + 256
-    assert want <= fp2.workspace_bytes(pk) <= want + rows * 2 * 8 * 2 + 8 * 256
+    assert want <= fp2.workspace_bytes(pk) <= want + rows * 2 * 16 + rows * 8 + 8 * 256
     # the cost-balanced plan adds 65536 packed rows of partial outputs (520 B each)
     assert fp2.workspace_bytes(base()) - got >= 65536 * 520
 
@@ -144,7 +144,7 @@ def ws_parts(p):
     n = 2 * al(krows * 256) + al(rows * fp2.num_key_blocks(p) * 4) + al(rows * 4)
     if p.dtype == fp2.FP8_E4M3:
         n += 2 * al(krows * 128)   # e4m3 code means of K and V (the fp8 correction)
-    n += al(items * 8) + al(rows * 8) + al((slots // 2 + 1) * 4) + 256
+    n += al(items * 16) + al(rows * 8) + al((slots // 2 + 1) * 4) + 256
     if slots:
         n += al(slots * rpu * 512) + al(slots * rpu * 8)
     return n
