@@ -39,8 +39,12 @@ namespace {
 
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
-constexpr int kChunksPerWave = 4;                          // 4 x 32 key blocks per wave
-constexpr int kGroup = kWaves * kChunksPerWave * 32;       // key blocks per pass (1024)
+// 32-block chunks of pooled keys per wave: 4 (a pass covers 1024 key blocks,
+// one workgroup per CU), or 1 for calls with at most 256 key blocks, whose
+// smaller register budget admits two workgroups per CU (the items of one
+// then run beside those of the other, hiding each item's load and
+// selection latencies).
+constexpr int kChunksPerWave = 4;
 constexpr int kQRow = 17;                                  // LDS row stride of a Q tile, 16-byte slots
 constexpr int kBufferWord3 = 0x00020000;                   // buffer resource word 3 (gfx9: raw 32-bit data)
 
@@ -100,8 +104,8 @@ __device__ void select_unit(const Prob& p, const float* ell, int Ia, int Ja, int
   if (tid == 0) *cnt = base;
 }
 
-template <int FP8, int G>
-__global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled pooled,
+template <int FP8, int G, int CPW>
+__global__ __launch_bounds__(kThreads, CPW == 1 ? 2 : 1) void estimate_kernel(Problem p0, Pooled pooled,
                                                             uint8_t* __restrict__ mask,
                                                             KeptLists kl, EllParts parts) {
   extern __shared__ float ell[];            // [nbk] block log2-energies of this row
@@ -219,16 +223,17 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
     }
   };
 
+  constexpr int kGroup = kWaves * CPW * 32;   // key blocks per pass
   for (int grp = 0; grp <= Ia; grp += kGroup) {
-    bf16x8_t kf[kChunksPerWave][8];
-    float m[kChunksPerWave], E[kChunksPerWave];
-    bool act[kChunksPerWave];
+    bf16x8_t kf[CPW][8];
+    float m[CPW], E[CPW];
+    bool act[CPW];
     // 32-block chunks of this wave in this group that hold a visible block
     // (chunk c of wave w starts at block grp + 32 (w + 8 c)); a wave without
     // any only takes part in the barriers
-    const int ncw = min(kChunksPerWave, max(0, ((Ia - grp) / 32 - w + kWaves) / kWaves));
+    const int ncw = min(CPW, max(0, ((Ia - grp) / 32 - w + kWaves) / kWaves));
 #pragma unroll
-    for (int c = 0; c < kChunksPerWave; ++c) {
+    for (int c = 0; c < CPW; ++c) {
       const int J0 = grp + 32 * (w + kWaves * c);
       act[c] = J0 <= Ia;
       m[c] = -INFINITY;
@@ -323,9 +328,9 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
       switch (ncw) {
         case 0: break;
         case 1: run(std::integral_constant<int, 1>{}); break;
-        case 2: run(std::integral_constant<int, 2>{}); break;
-        case 3: run(std::integral_constant<int, 3>{}); break;
-        default: run(std::integral_constant<int, 4>{}); break;
+        case 2: if constexpr (CPW >= 2) run(std::integral_constant<int, 2>{}); break;
+        case 3: if constexpr (CPW >= 3) run(std::integral_constant<int, 3>{}); break;
+        default: if constexpr (CPW >= 4) run(std::integral_constant<int, 4>{}); break;
       }
     };
     const int nfull = nrows >> 5;
@@ -346,7 +351,7 @@ __global__ __launch_bounds__(kThreads) void estimate_kernel(Problem p0, Pooled p
 
     // merge the two lane halves (same key block, different rows)
 #pragma unroll
-    for (int c = 0; c < kChunksPerWave; ++c) {
+    for (int c = 0; c < CPW; ++c) {
       if (!act[c]) continue;
       const float m2 = __shfl_xor(m[c], 32, 64);
       const float E2 = __shfl_xor(E[c], 32, 64);
@@ -478,13 +483,20 @@ hipError_t launch_est_dt(const Problem& p, const Pooled& pooled, uint8_t* mask, 
     while (n > 1 && (size_t)(units * n) * (size_t)p.nbk > scratch_floats) --n;
     parts.n = std::max(1, n);
   }
-  const unsigned grid = (unsigned)std::min<int64_t>(units * parts.n, cus);
+  // one chunk per wave covers up to 8 x 32 key blocks in one pass
+  const bool small = p.nbk <= kWaves * 32;
+  const unsigned grid = (unsigned)std::min<int64_t>(units * parts.n, (int64_t)cus * (small ? 2 : 1));
   const size_t smem = (size_t)p.nbk * sizeof(float);
-  switch (p.g) {
-    case 1: estimate_kernel<FP8, 1><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); break;
-    case 2: estimate_kernel<FP8, 2><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); break;
-    case 4: estimate_kernel<FP8, 4><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); break;
-    case 8: estimate_kernel<FP8, 8><<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); break;
+  auto go = [&](auto kern) { kern<<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); };
+  switch (p.g * (small ? -1 : 1)) {
+    case 1: go(estimate_kernel<FP8, 1, kChunksPerWave>); break;
+    case 2: go(estimate_kernel<FP8, 2, kChunksPerWave>); break;
+    case 4: go(estimate_kernel<FP8, 4, kChunksPerWave>); break;
+    case 8: go(estimate_kernel<FP8, 8, kChunksPerWave>); break;
+    case -1: go(estimate_kernel<FP8, 1, 1>); break;
+    case -2: go(estimate_kernel<FP8, 2, 1>); break;
+    case -4: go(estimate_kernel<FP8, 4, 1>); break;
+    case -8: go(estimate_kernel<FP8, 8, 1>); break;
     default: return hipErrorInvalidValue;
   }
   if (parts.n > 1) select_kernel<<<(unsigned)units, kThreads, smem, s>>>(p, mask, kl, parts);
