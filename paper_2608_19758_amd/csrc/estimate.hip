@@ -40,10 +40,10 @@ namespace {
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 // 32-block chunks of pooled keys per wave: 4 (a pass covers 1024 key blocks,
-// one workgroup per CU), or 1 for calls with at most 256 key blocks, whose
-// smaller register budget admits two workgroups per CU (the items of one
-// then run beside those of the other, hiding each item's load and
-// selection latencies).
+// one workgroup per CU), or 1 (a pass covers 256), whose smaller register
+// budget admits two workgroups per CU: the items of one then run beside
+// those of the other, hiding each item's load and selection latencies, at
+// the price of streaming a unit's Q tiles once per pass.
 constexpr int kChunksPerWave = 4;
 constexpr int kQRow = 17;                                  // LDS row stride of a Q tile, 16-byte slots
 constexpr int kBufferWord3 = 0x00020000;                   // buffer resource word 3 (gfx9: raw 32-bit data)
@@ -483,8 +483,12 @@ hipError_t launch_est_dt(const Problem& p, const Pooled& pooled, uint8_t* mask, 
     while (n > 1 && (size_t)(units * n) * (size_t)p.nbk > scratch_floats) --n;
     parts.n = std::max(1, n);
   }
-  // one chunk per wave covers up to 8 x 32 key blocks in one pass
-  const bool small = p.nbk <= kWaves * 32;
+  // One chunk per wave (8 x 32 key blocks per pass, two workgroups per CU)
+  // up to 512 key blocks, and up to 1024 when a unit holds at most 512
+  // packed rows (g <= 4): there the latency hidden by the second workgroup
+  // outweighs the Q tiles streamed again for every pass (measured at 128K:
+  // g = 4 0.83 -> 0.79 ms, g = 8 1.43 -> 1.46 ms).
+  const bool small = p.nbk <= 2 * kWaves * 32 || (p.g <= 4 && p.nbk <= 4 * kWaves * 32);
   const unsigned grid = (unsigned)std::min<int64_t>(units * parts.n, (int64_t)cus * (small ? 2 : 1));
   const size_t smem = (size_t)p.nbk * sizeof(float);
   auto go = [&](auto kern) { kern<<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); };
