@@ -54,11 +54,12 @@ def check_close(out, oout, lse, olse, dtype, rows=None, label="same-mask"):
 
 
 def params_for(wl, alpha, corr=None, sink=None, window=None, recent=None, scale=0.0, kv_splits=0,
-               query_tile_rows=0, score_splits=0):
+               query_tile_rows=0, score_splits=0, max_seq_len=None):
     sp = wl.spec
     return fp2.make_params(
         batch=sp.batch, num_q_heads=sp.num_q_heads, num_kv_heads=sp.num_kv_heads,
-        max_seq_len=sp.max_seq_len, page_size=sp.page_size, max_pages_per_seq=wl.max_pages,
+        max_seq_len=sp.max_seq_len if max_seq_len is None else max_seq_len,
+        page_size=sp.page_size, max_pages_per_seq=wl.max_pages,
         alpha=alpha, sink_blocks=sp.sink_blocks if sink is None else sink,
         window_blocks=sp.window_blocks if window is None else window,
         recent_blocks=sp.recent_blocks if recent is None else recent,

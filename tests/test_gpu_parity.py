@@ -126,6 +126,25 @@ def test_paged_equals_contiguous_and_deterministic(dtype):
         np.testing.assert_array_equal(b, c)
 
 
+@pytest.mark.parametrize("hq", [8, 16])
+def test_estimate_chunk_variants_bitwise(hq):
+    """The scoring kernel holds one or four 32-block chunks of pooled keys per
+    wave, chosen from the key-block bound (max_seq_len) and g; either way each
+    block's energy is folded by one lane over the same tiles in the same
+    order, so the masks and the outputs agree bit for bit."""
+    wl = synth.generate(spec([3000, 1100], hq=hq, hkv=2, page=0, seed=5))
+    d = gu.device_tensors(wl)
+    small = gu.gpu_prefill(wl, gu.params_for(wl, 0.97), d)       # 24 key blocks: one chunk
+    big = gu.gpu_prefill(wl, gu.params_for(wl, 0.97, max_seq_len=1100 * 128), d)   # four
+    out_s, mask_s, lse_s = small
+    out_b, mask_b, lse_b = big
+    nq, nk = mask_s.shape[2], mask_s.shape[3]
+    np.testing.assert_array_equal(mask_b[:, :, :nq, :nk], mask_s)
+    assert not mask_b[:, :, nq:, :].any() and not mask_b[:, :, :, nk:].any()
+    np.testing.assert_array_equal(out_b, out_s)
+    np.testing.assert_array_equal(lse_b, lse_s)
+
+
 def test_correction_exact_for_constant_blocks():
     """Keys constant within each block: the corrected output equals dense
     attention (Sec. 3.2 Eq. taylor with every delta = 0), on the GPU too."""
