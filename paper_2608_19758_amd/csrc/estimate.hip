@@ -104,8 +104,10 @@ __device__ void select_unit(const Prob& p, const float* ell, int Ia, int Ja, int
   if (tid == 0) *cnt = base;
 }
 
+// (the second bound is waves per SIMD: four, i.e. two workgroups per CU, for
+// the one-chunk variant, so that it keeps within 128 registers)
 template <int FP8, int G, int CPW>
-__global__ __launch_bounds__(kThreads, CPW == 1 ? 2 : 1) void estimate_kernel(Problem p0, Pooled pooled,
+__global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Problem p0, Pooled pooled,
                                                             uint8_t* __restrict__ mask,
                                                             KeptLists kl, EllParts parts) {
   extern __shared__ float ell[];            // [nbk] block log2-energies of this row
