@@ -243,8 +243,8 @@ fp2_status_t fp2_estimate(const fp2_params_t* params, const void* q, const int32
                           void* workspace,
                           size_t workspace_bytes, void* stream);
 
-/* The attention stage alone (Sec. 3.2 Eq. correction, Sec. 3.3; Algorithm 1
- * steps 6-11) under a caller-given mask: bit 0 of block_mask_in[b][h][I][J]
+/* The attention stage alone (Sec. 3.2 Eq. correction, Sec. 3.3; the sparse
+ * attention of Algorithm 1) under a caller-given mask: bit 0 of block_mask_in[b][h][I][J]
  * selects key block J for query block I (entries with J > Ia are ignored).
  * The caller should select the diagonal J == Ia of every valid block I: the
  * mask is not checked, and a row whose keys are all excluded (no selected
@@ -259,7 +259,7 @@ fp2_status_t fp2_attend(const fp2_params_t* params, const void* q, const int32_t
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* Block means of K and V (Sec. 3.2, the pooled statistics of Eq. correction;
- * Algorithm 1 step 2), dequantised for fp8. Here cu_seqlens are the KV
+ * the block means of Algorithm 1), dequantised for fp8. Here cu_seqlens are the KV
  * lengths (a prefix included) and blocks are counted over max_kv_len. khat
  * [batch, num_kv_heads, nbk, head_dim] receives the bf16 (nearest-even)
  * rounding of the key means, vbar the same layout for the value means;
@@ -317,8 +317,8 @@ fp2_status_t fp2_prefill_cached(const fp2_params_t* params, const void* q,
 size_t fp2_csr_capacity(const fp2_params_t* params);
 
 /* The selection as a CSR index of 64-token key tiles (Sec. 3.3 Eq. csr;
- * Algorithm 1 step 5, logical blocks expanded to B/64 = 2 physical tiles per
- * block): segment s = (b * num_kv_heads + h) * nbq + I, in block_mask row
+ * the compaction of Algorithm 1, logical blocks expanded to B/64 = 2 physical
+ * tiles per block): segment s = (b * num_kv_heads + h) * nbq + I, in block_mask row
  * order, owns csr_indices[csr_offsets[s] .. csr_offsets[s+1]), which lists in
  * ascending order the tiles j (keys 64j .. 64j+63 of sequence b) of every key
  * block J with bit 0 of block_mask[b][h][I][J] set and J <= Ia: 2J, and 2J+1

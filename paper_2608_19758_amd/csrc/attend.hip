@@ -1,5 +1,5 @@
 // Sparse attention over the kept key blocks with the mean correction
-// (Sec. 3.2 Eq. correction, Sec. 3.3; Algorithm 1 steps 6-11).
+// (Sec. 3.2 Eq. correction, Sec. 3.3; the sparse attention of Algorithm 1).
 //
 // Work unit: (sequence b, KV head h, query block I) of the packed query rows
 // of Eq. packgqa. A work item is a slice of 32*W of the g*B packed rows of a

@@ -1,13 +1,14 @@
 // Fused block scoring, max-based thresholding and kept-list compaction
-// (Sec. 3.1 Eq. (1)-(2), Eq. fused_score, Eq. select; Algorithm 1 steps 3-5).
+// (Sec. 3.1 Eq. (1)-(2), Eq. fused_score, Eq. select; the scoring, thresholding
+// and compaction of Algorithm 1).
 //
 // A persistent grid (one 8-wave workgroup per compute unit) deals the units
 // (sequence b, KV head h, query block I) round-robin, heaviest (largest I)
 // first. The query rows of block I are the g*B packed rows of Eq. packgqa
 // (position I*B + r/g, head h*g + r%g). They stream through LDS in pairs of
 // 32-row tiles (one barrier per pair), the global loads one pair ahead; each
-// wave keeps up to four 32-wide chunks of pooled keys khat in registers (the
-// MFMA B operand) and computes S = Q khat^T with v_mfma_f32_32x32x16_bf16
+// wave keeps four (or, for calls with fewer key blocks, one) 32-wide chunks of
+// pooled keys khat in registers (the MFMA B operand) and computes S = Q khat^T with v_mfma_f32_32x32x16_bf16
 // (fp32 accumulation). Lane l of the accumulator owns key block J = chunk +
 // l%32 and 16 query rows, so the row sum of exp2(S * scale*log2e - m) for its
 // block is a per-lane running sum with a per-lane offset m (the role of the

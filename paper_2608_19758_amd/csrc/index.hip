@@ -1,6 +1,6 @@
-// The selection as a CSR index of 64-token key tiles (Sec. 3.3 Eq. csr;
-// Algorithm 1 step 5, where logical blocks are expanded to B/64 physical
-// tiles). Segment s = (b * Hkv + h) * nbmax + I follows the mask rows; its
+// The selection as a CSR index of 64-token key tiles (Sec. 3.3 Eq. csr; the
+// compaction of Algorithm 1, where logical blocks are expanded to B/64
+// physical tiles). Segment s = (b * Hkv + h) * nbmax + I follows the mask rows; its
 // entries are, ascending, the key tiles j (keys 64j .. 64j+63) of every kept
 // block J: 2J, and 2J+1 when that tile starts before the sequence's last key.
 //

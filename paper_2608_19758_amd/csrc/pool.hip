@@ -1,5 +1,5 @@
 // Block means of K and V (Sec. 3.2, the pooled statistics kbar_J, vbar_J of
-// Eq. correction; Algorithm 1 step 2). HBM-bound: every K/V byte of the
+// Eq. correction; the block means of Algorithm 1). HBM-bound: every K/V byte of the
 // sequence is read once with 16-byte loads through the page table.
 //
 // One workgroup per (key block J, KV head h, sequence b), 256 threads, over
