@@ -229,8 +229,11 @@ __device__ __forceinline__ void ring_loop(uint4* ring, int n, const uint8_t* Kb,
 __device__ __forceinline__ float xhalf_max(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
                                                   false);
-  const float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
-  return a > b ? a : b;
+  // v_max_f32 directly: the operands are scores (no signalling NaNs), and
+  // fmaxf would first canonicalize each of them
+  float m;
+  asm("v_max_f32 %0, %1, %2" : "=v"(m) : "v"(r[0]), "v"(r[1]));
+  return m;
 }
 
 // Running state of the RT 32-row tiles of one wave.
@@ -250,38 +253,44 @@ struct Scores {
   f32x16_t v[RT][2];
 };
 
-// Lazy rescale thresholds (log2 units): the running maximum m of a row is
-// only moved when a new logit exceeds it by more than tau, so probabilities
-// reach 2^(off + tau). fp8 keeps P~ = e4m3(2^8 exp(x - m)) within the e4m3
-// range: 2^(8 + 0.8) = 445.7 < 448. bf16 probabilities stay far from any
-// limit at 2^(8 + 8).
+// Lazy rescale (log2 units): the reference m of a row's online softmax only
+// moves when a new logit exceeds it by more than tau, and then to that logit
+// plus a headroom h, so that the next move needs a rise of tau + h. The
+// probabilities are 2^(off + x - m) <= 2^(off + tau); right after a move the
+// new maximum sits at 2^(off - h). fp8 keeps P~ = e4m3(2^8 exp(x - m)) within
+// the e4m3 range: 2^(8 + 0.8) = 445.7 < 448, and the headroom of 2 keeps the
+// new maximum at 2^6, well inside the normal range. bf16 probabilities stay
+// far from any limit at 2^(8 + 8).
 constexpr float kTauFp8 = 0.8f;
+constexpr float kHeadFp8 = 2.0f;
 constexpr float kTauBf16 = 8.0f;
+// Reference of a row that has not seen a visible key yet: finite, so that the
+// logit bias stays finite, and far below any logit, so that the first visible
+// key moves it (and the rescale by 2^(m_old - m_new) = 0 clears nothing).
+constexpr float kNoRef = -1e30f;
 
 // Online-softmax rescale of row tile rt for the raw scores s (-inf where
 // masked); the logits are x = cs * s + shift (log2 units, cs > 0). The
-// running maximum moves to the new row maximum only if that exceeds it by
-// more than tau (any finite value moves it from -inf); the accumulators are
-// rescaled only when some row of the wave moved. Returns the bias b with
-// x - m + off = cs * s + b.
+// reference m moves as described above (any visible key moves it from
+// kNoRef); the accumulators are rescaled only when some row of the wave
+// moved. Returns the bias b with x - m + off = cs * s + b.
 template <int NU, bool LS, int RT>
 __device__ __forceinline__ float softmax_rescale(const f32x16_t (&s)[NU], RowState<RT>& rs, int rt,
-                                                 float cs, float shift, float off, float tau) {
+                                                 float cs, float shift, float off, float tau,
+                                                 float head) {
   float mr = -INFINITY;
 #pragma unroll
   for (int u = 0; u < NU; ++u)
 #pragma unroll
     for (int e = 0; e < 16; ++e) mr = fmaxf(mr, s[u][e]);
   mr = xhalf_max(mr);
-  const float mx = mr == -INFINITY ? -INFINITY : fmaf(mr, cs, shift);
-  // m stays -inf only while no key of this row has been visible; the update
-  // is then the identity (scale 1, p = 0), without branching the wave away
-  // from the MFMAs that follow.
-  const bool up = mx > rs.m[rt] + tau;
+  // the row's largest logit plus the headroom; -inf while every key of the
+  // row is masked (cs > 0), which never moves m
+  const float mx = fmaf(mr, cs, shift + head);
+  const bool up = mx > rs.m[rt] + (tau + head);
   const float m_new = up ? mx : rs.m[rt];
-  const float m_use = m_new == -INFINITY ? 0.f : m_new;
   if (__any(up)) {
-    const float a = fast_exp2(rs.m[rt] - m_use);
+    const float a = fast_exp2(rs.m[rt] - m_new);
     rs.l[rt] *= a;
     if (LS) rs.ls[rt][0] *= a;   // the only element of the row-sum tile that is read
 #pragma unroll
@@ -290,7 +299,7 @@ __device__ __forceinline__ float softmax_rescale(const f32x16_t (&s)[NU], RowSta
       for (int e = 0; e < 16; ++e) rs.o[rt][dt][e] *= a;
   }
   rs.m[rt] = m_new;
-  return shift + off - m_use;
+  return shift + off - m_new;
 }
 
 // Pairwise sum of 16 values.
@@ -386,7 +395,7 @@ __device__ __forceinline__ void fin_bf16(const uint4* st, Scores<RT>& S, RowStat
     // KIND 1: the PV weight pv_scale (> 0) enters the exponent as log2
     // pv_scale, and the row sum divides it out once.
     const float bias = softmax_rescale<2, false>(S.v[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off,
-                                                 kTauBf16) +
+                                                 kTauBf16, 0.f) +
                        (KIND == 1 ? lg_pv : 0.f);
     float pv[2][16];
 #pragma unroll
@@ -416,21 +425,58 @@ __device__ __forceinline__ void fin_bf16(const uint4* st, Scores<RT>& S, RowStat
 // ---------------------------------------------------------------------------
 // fp8 pieces: the scores of one 64-key step, then softmax + PV.
 // ---------------------------------------------------------------------------
+// LDS byte offsets, within a stage, of this lane's fp8 operand reads: the K
+// tile (ds, chunk pair; key subtile u = 1 lies 32 rows = 4 KiB further, as
+// rows 32 apart share the swizzle) and the V^T fragments (dt; key group t
+// lies 16 rows = 2 KiB further, the V tile 8 KiB after the K tile).
+// Computed once per item and made opaque, so that a step adds its stage
+// base to each with one instruction; the mask keeps the known range, so the
+// constant distances fold into the LDS instructions' offsets.
+struct Fp8Lane {
+  int k[2][2];
+  int v[4];
+};
+
+__device__ __forceinline__ Fp8Lane fp8_lane_offsets(int lane) {
+  Fp8Lane o;
+  const int half = lane >> 5, l32 = lane & 31;
+#pragma unroll
+  for (int ds = 0; ds < 2; ++ds)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) o.k[ds][t] = 16 * kslot8(l32, 4 * ds + 2 * half + t);
+  // V^T fragment dt, key group t: byte b of lane half H is key
+  // 16t + 8((b%8)/4) + 4H + b%4 (b = 8 r2 + byte of the read)
+  const int g16 = lane >> 4, i16 = lane & 15;
+  const int sidx = i16 >> 1, r2 = i16 & 1;
+  const int key = 8 * (sidx >> 2) + 4 * (g16 >> 1) + (sidx & 3);
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) o.v[dt] = 16 * vslot8(key, 2 * dt + (g16 & 1)) + 8 * r2;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    asm volatile("" : "+v"(o.k[i >> 1][i & 1]), "+v"(o.v[i]));
+    o.k[i >> 1][i & 1] &= 0x3fff;
+    o.v[i] &= 0x3fff;
+  }
+  return o;
+}
+
 template <int RT>
 __device__ __forceinline__ void qk_fp8(const uint4* st, const i32x8_t (&qf)[RT][2], Scores<RT>& S,
-                                       int lane) {
-  const int half = lane >> 5, l32 = lane & 31;
+                                       const Fp8Lane& ol) {
+  const char* sb = (const char*)st;
   i32x8_t a[2][2];
 #pragma unroll
-  for (int u = 0; u < 2; ++u)
+  for (int ds = 0; ds < 2; ++ds) {
+    const char* k0 = sb + ol.k[ds][0];
+    const char* k1 = sb + ol.k[ds][1];
 #pragma unroll
-    for (int ds = 0; ds < 2; ++ds) {
-      const int r = 32 * u + l32;
-      const uint4 c0 = st[kslot8(r, 4 * ds + 2 * half)];
-      const uint4 c1 = st[kslot8(r, 4 * ds + 2 * half + 1)];
+    for (int u = 0; u < 2; ++u) {
+      const uint4 c0 = *(const uint4*)(k0 + 4096 * u);
+      const uint4 c1 = *(const uint4*)(k1 + 4096 * u);
       a[u][ds] = (i32x8_t){(int)c0.x, (int)c0.y, (int)c0.z, (int)c0.w,
                            (int)c1.x, (int)c1.y, (int)c1.z, (int)c1.w};
     }
+  }
 #pragma unroll
   for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -442,23 +488,15 @@ __device__ __forceinline__ void qk_fp8(const uint4* st, const i32x8_t (&qf)[RT][
     }
 }
 
-// V^T fragments of a 64-key fp8 step: byte b of lane half H is key
-// 16(b/8) + 8((b%8)/4) + 4H + b%4.
-__device__ __forceinline__ void vread_fp8(const uint4* st, i32x8_t (&va)[4], int lane) {
-  const int g16 = lane >> 4, i16 = lane & 15;
-  const int sidx = i16 >> 1, r2 = i16 & 1;
-  const int H = g16 >> 1;
-  const uint4* vt = st + kStep * 8;
+// V^T fragments of a 64-key fp8 step (the layout of Fp8Lane::v).
+__device__ __forceinline__ void vread_fp8(const uint4* st, i32x8_t (&va)[4], const Fp8Lane& ol) {
+  const char* vb = (const char*)st + kStep * 8 * 16;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) {
     i32x2_t rd[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int key = 16 * t + 8 * (sidx >> 2) + 4 * H + (sidx & 3);
-      const int c = 2 * dt + (g16 & 1);
-      const int byte = vslot8(key, c) * 16 + 8 * r2;
-      rd[t] = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2_t*)((lds_char_t*)vt + byte));
-    }
+    for (int t = 0; t < 4; ++t)
+      rd[t] = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2_t*)(lds_char_t*)(vb + ol.v[dt] + 2048 * t));
     va[dt] = (i32x8_t){rd[0][0], rd[0][1], rd[1][0], rd[1][1], rd[2][0], rd[2][1], rd[3][0], rd[3][1]};
   }
 }
@@ -489,11 +527,11 @@ __device__ __forceinline__ int pack_e4m3x4(float a, float b, float c, float d) {
 template <int KIND, int RT>
 __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState<RT>& rs, float cs,
                                         int key0, const int (&pos)[RT], bool diag, int lane,
-                                        const i32x8_t& sel, int nv = kStep) {
+                                        const i32x8_t& sel, const Fp8Lane& ol, int nv = kStep) {
   const int half = lane >> 5;
   auto& s = S.v;
   i32x8_t va[4];
-  vread_fp8(st, va, lane);
+  vread_fp8(st, va, ol);
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     if (diag) {
@@ -509,7 +547,7 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
           }
     }
     const float bias = softmax_rescale<2, true>(s[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, 8.0f,
-                                                kTauFp8);
+                                                kTauFp8, kHeadFp8);
     int pk[8];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
@@ -630,7 +668,7 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) rs.o[rt][dt] = f32x16_t{};
       rs.ls[rt] = f32x4_t{};
-      rs.m[rt] = -INFINITY;
+      rs.m[rt] = kNoRef;
       rs.l[rt] = 0.f;
     }
     float qsc = FP8 ? p.q_scale[hq] : 1.f;
@@ -652,6 +690,8 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
       for (int k = 0; k < 8; ++k) sel[k] = selw;
       asm volatile("" : "+v"(sel));
     }
+    [[maybe_unused]] Fp8Lane ol;
+    if constexpr (FP8) ol = fp8_lane_offsets(lane);
 
     // ---- kept blocks: step s of a chunk -> its block list entry s/2, half s%2
     {
@@ -749,11 +789,11 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
         if constexpr (FP8) {
           run_steps<W, 1, RT, RING>(
               ring, nst, K, V, fetch, addr,
-              [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
+              [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, ol); },
               [&](const uint4* st, Scores<RT>& S, int s) {
                 const int wp = c0 + (s >> 1);   // walk position of the step's block
                 fin_fp8<0, RT>(st, S, rs, cs, (wp == 0 ? e0 : e1) * kBlock + kStep * (s & 1), pos,
-                               wp < nmask, lane, sel);
+                               wp < nmask, lane, sel, ol);
               },
               tid);
         } else {
@@ -835,10 +875,10 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
         if constexpr (FP8) {
           run_steps<W, 1, RT, RING>(
               ring, (np + kStep - 1) / kStep, Kh, Vh, fetch, addr,
-              [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, lane); },
+              [&](const uint4* st, Scores<RT>& S) { qk_fp8<RT>(st, qf, S, ol); },
               [&](const uint4* st, Scores<RT>& S, int s) {
                 const int nv = np - kStep * s;
-                fin_fp8<1, RT>(st, S, rs, cs, 0, pos, nv < kStep, lane, sel, nv);
+                fin_fp8<1, RT>(st, S, rs, cs, 0, pos, nv < kStep, lane, sel, ol, nv);
               },
               tid);
         } else {
@@ -878,7 +918,8 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
             *(float4*)(po + d) = make_float4(rs.o[rt][dt][4 * i + 0], rs.o[rt][dt][4 * i + 1],
                                              rs.o[rt][dt][4 * i + 2], rs.o[rt][dt][4 * i + 3]);
           }
-        if (half == 0) *(float2*)(plan.part_ml + 2 * prow) = make_float2(rs.m[rt], l_tot);
+        if (half == 0)   // a part that saw no visible key reports m = -inf
+          *(float2*)(plan.part_ml + 2 * prow) = make_float2(l_tot > 0.f ? rs.m[rt] : -INFINITY, l_tot);
       }
       continue;
     }
