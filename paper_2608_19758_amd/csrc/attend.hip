@@ -756,26 +756,29 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
 #pragma unroll 1
       for (int c0 = lo; c0 < hi; c0 += chunk) {
         const int nbc = min(chunk, hi - c0);
-        // Record (block i, half hf, group e) = {byte offset at which row 0 of
-        // the half would lie if the group's page continued down to it (64-bit,
-        // may be negative), last valid row index}: row r of the half then
-        // lies at base + min(r, last) * rowbytes. Rows past the sequence thus
+        // Record (block i, half hf, group e) = {byte offset base at which row
+        // 0 of the half would lie if the group's page continued down to it
+        // (64-bit, may be negative), limit lim >= 0}: row r of the group then
+        // lies at base + min(r * rowbytes, lim), with lim the offset of the
+        // half's last valid row (at most 63 rows). Rows past the sequence thus
         // repeat its last token (finite data; those keys are masked); a group
-        // that starts past it points at that token directly.
+        // that starts past it points at that token directly (base = the
+        // token, lim = 0). The offset added to base is never negative.
         for (int k = tid; k < nbc * 2 * rph; k += 64 * W) {
           const int i = k / (2 * rph), hk = k - i * 2 * rph;
           const int key0 = kidx[cnt - 1 - (c0 + i)] * kBlock + kStep * (hk >= rph);
-          const int last = L - 1 - key0;
-          int first = (hk % rph) << gshift;
-          uint32_t slot;
+          const int last = L - 1 - key0;   // negative when the half starts past the sequence
+          const int first = (hk % rph) << gshift;
+          int64_t base;
+          uint32_t lim;
           if (first <= last) {
-            slot = slot_of(key0 + first);
+            base = ((int64_t)slot_of(key0 + first) - first) * rowbytes + hbytes;
+            lim = (uint32_t)(min(last, kStep - 1) * rowbytes);
           } else {
-            slot = slot_of(L - 1);
-            first = last;
+            base = (int64_t)slot_of(L - 1) * rowbytes + hbytes;
+            lim = 0u;
           }
-          const int64_t base = ((int64_t)slot - first) * rowbytes + hbytes;
-          aux[k] = make_uint4((uint32_t)base, (uint32_t)((uint64_t)base >> 32), (uint32_t)last, 0u);
+          aux[k] = make_uint4((uint32_t)base, (uint32_t)((uint64_t)base >> 32), lim, 0u);
         }
         __syncthreads();
         auto fetch = [&](int s, int r) -> uint4 { return aux[(s * rph) + (r >> gshift)]; };
@@ -783,7 +786,8 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
         auto addr = [&](uint4 rec, int s, int r) -> int64_t {
           (void)s;
           const int64_t base = (int64_t)(((uint64_t)rec.y << 32) | rec.x);
-          return base + min(r, (int)rec.z) * rowb;
+          // r * rowb is fixed per lane; both operands of min are >= 0
+          return base + (uint32_t)min(r * rowb, (int)rec.z);
         };
         const int nst = 2 * nbc;
         if constexpr (FP8) {
