@@ -141,10 +141,12 @@
  * the probabilities of kept keys are rounded to e4m3 as P~ = e4m3(2^8 *
  * exp(S - m)) before the value product, and the softmax denominator sums
  * those rounded P~ (so out is a convex combination of values); the 2^8 is
- * removed from lse. The reference m of the online softmax moves only when a
- * logit passes it by more than tau = 0.8 (base 2), and then to that logit
- * plus 2, so P~ lies in [0, 2^8.8] (2^8.8 < 446, below 448, the largest e4m3
- * value). Scales must be positive and finite.
+ * removed from lse. The reference m_c of the online softmax moves only when
+ * a logit passes it by more than tau = 0.8 (base 2), so P~ lies in
+ * [0, 2^8.8] (2^8.8 < 446, below 448, the largest e4m3 value); it moves in
+ * whole steps k above the accumulators' reference, and the value products
+ * lift P~ by 2^k through the MFMA scale operands. Scales must be positive and
+ * finite.
  */
 #ifndef FP2_H
 #define FP2_H

@@ -240,10 +240,13 @@ __device__ __forceinline__ float xhalf_max(float v) {
 template <int RT>
 struct RowState {
   f32x16_t o[RT][4];   // O^T accumulators: o[rt][dt][4i+j] = O[row][32dt + 8i + 4*half + j]
-  f32x4_t ls[RT];      // fp8 kept keys: row sums of P~ from the matrix cores (element 0);
-                       // folded into l once the kept blocks are done
-  float m[RT];         // running maximum (log2 units)
-  float l[RT];         // row-sum part summed on the vector ALUs (this lane's keys)
+  f32x4_t ls[RT];      // fp8: row sums of the last step's P~ from the matrix cores
+                       // (element 0, against m + k), folded into l at the next step
+  float m[RT];         // reference of the accumulators o and l (log2 units)
+  float l[RT];         // bf16: row-sum part of this lane's keys; fp8: the row sums
+  int k[RT];           // fp8: P~ is taken against m + k and lifted by 2^k in the PV MFMAs
+  float mc[RT];        // fp8: m + k
+  float p2k[RT];       // fp8: 2^k
 };
 
 // Raw scores S^T of one 64-key step for the RT row tiles: v[rt][u][4i+j] is
@@ -253,17 +256,25 @@ struct Scores {
   f32x16_t v[RT][2];
 };
 
-// Lazy rescale (log2 units): the reference m of a row's online softmax only
-// moves when a new logit exceeds it by more than tau, and then to that logit
-// plus a headroom h, so that the next move needs a rise of tau + h. The
-// probabilities are 2^(off + x - m) <= 2^(off + tau); right after a move the
-// new maximum sits at 2^(off - h). fp8 keeps P~ = e4m3(2^8 exp(x - m)) within
-// the e4m3 range: 2^(8 + 0.8) = 445.7 < 448, and the headroom of 2 keeps the
-// new maximum at 2^6, well inside the normal range. bf16 probabilities stay
-// far from any limit at 2^(8 + 8).
+// Lazy rescale (log2 units): the reference of a row's online softmax only
+// moves when a new logit exceeds it by more than tau, so the probabilities
+// are 2^(off + x - m) <= 2^(off + tau). bf16 (tau = 8) moves the reference m
+// to the new maximum and rescales the accumulators; its probabilities stay
+// far from any limit at 2^(8 + 8). fp8 keeps P~ = e4m3(2^8 exp(x - m_c))
+// within the e4m3 range, 2^(8 + 0.8) = 445.7 < 448, against a reference
+// m_c = m + k that moves in whole steps above the accumulators' reference m:
+// the PV MFMAs lift each query's P~ by 2^k through their per-lane E8M0 B
+// scales (127 + k: the 32 keys a lane holds belong to its own query), and the
+// step's row sums, taken against m + k, join l times 2^k, so a move only
+// changes k and the accumulators keep m. A move sets k = ceil(x_max - m) (the
+// new maximum then lies in (2^7, 2^8]); only a row without a visible key so
+// far, or a lift past 2^64, rebases m to the new maximum and rescales the
+// accumulators.
 constexpr float kTauFp8 = 0.8f;
-constexpr float kHeadFp8 = 2.0f;
 constexpr float kTauBf16 = 8.0f;
+// Largest lift: with P~ <= 2^8.8, value codes <= 448 and at most 2^17 keys a
+// row's accumulators stay below 2^(35 + k), far inside fp32 for k <= 64.
+constexpr int kMaxLift = 64;
 // Reference of a row that has not seen a visible key yet: finite, so that the
 // logit bias stays finite, and far below any logit, so that the first visible
 // key moves it (and the rescale by 2^(m_old - m_new) = 0 clears nothing).
@@ -271,28 +282,25 @@ constexpr float kNoRef = -1e30f;
 
 // Online-softmax rescale of row tile rt for the raw scores s (-inf where
 // masked); the logits are x = cs * s + shift (log2 units, cs > 0). The
-// reference m moves as described above (any visible key moves it from
-// kNoRef); the accumulators are rescaled only when some row of the wave
+// reference m moves to the row's new maximum when that exceeds it by more
+// than tau (any visible key moves it from kNoRef; a fully masked row, -inf,
+// never does); the accumulators are rescaled only when some row of the wave
 // moved. Returns the bias b with x - m + off = cs * s + b.
-template <int NU, bool LS, int RT>
+template <int NU, int RT>
 __device__ __forceinline__ float softmax_rescale(const f32x16_t (&s)[NU], RowState<RT>& rs, int rt,
-                                                 float cs, float shift, float off, float tau,
-                                                 float head) {
+                                                 float cs, float shift, float off, float tau) {
   float mr = -INFINITY;
 #pragma unroll
   for (int u = 0; u < NU; ++u)
 #pragma unroll
     for (int e = 0; e < 16; ++e) mr = fmaxf(mr, s[u][e]);
   mr = xhalf_max(mr);
-  // the row's largest logit plus the headroom; -inf while every key of the
-  // row is masked (cs > 0), which never moves m
-  const float mx = fmaf(mr, cs, shift + head);
-  const bool up = mx > rs.m[rt] + (tau + head);
+  const float mx = fmaf(mr, cs, shift);
+  const bool up = mx > rs.m[rt] + tau;
   const float m_new = up ? mx : rs.m[rt];
   if (__any(up)) {
     const float a = fast_exp2(rs.m[rt] - m_new);
     rs.l[rt] *= a;
-    if (LS) rs.ls[rt][0] *= a;   // the only element of the row-sum tile that is read
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -300,6 +308,42 @@ __device__ __forceinline__ float softmax_rescale(const f32x16_t (&s)[NU], RowSta
   }
   rs.m[rt] = m_new;
   return shift + off - m_new;
+}
+
+// fp8 counterpart of softmax_rescale with the lifted reference described
+// above: returns the bias b with x - m_c + 8 = cs * s + b.
+template <int RT>
+__device__ __forceinline__ float softmax_lift_fp8(const f32x16_t (&s)[2], RowState<RT>& rs, int rt,
+                                                  float cs, float shift) {
+  float mr = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) mr = fmaxf(mr, s[u][e]);
+  mr = xhalf_max(mr);
+  const float mx = fmaf(mr, cs, shift);   // the row's largest logit; -inf while all are masked
+  rs.l[rt] = fmaf(rs.ls[rt][0], rs.p2k[rt], rs.l[rt]);   // the previous step's row sums
+  const bool up = mx > rs.mc[rt] + kTauFp8;
+  if (__any(up)) {
+    // whole steps above m that bring m_c to the new maximum or past it; a
+    // row that saw no key yet (m = kNoRef) or a lift past kMaxLift rebases
+    const float kf = ceilf(mx - rs.m[rt]);
+    const bool rebase = up && !(kf <= (float)kMaxLift);
+    if (__any(rebase)) {
+      const float m_new = rebase ? mx : rs.m[rt];
+      const float a = fast_exp2(rs.m[rt] - m_new);
+      rs.l[rt] *= a;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) rs.o[rt][dt][e] *= a;
+      rs.m[rt] = m_new;
+    }
+    rs.k[rt] = rebase ? 0 : up ? (int)fminf(kf, (float)kMaxLift) : rs.k[rt];
+    rs.mc[rt] = rs.m[rt] + (float)rs.k[rt];
+    rs.p2k[rt] = ldexpf(1.f, rs.k[rt]);
+  }
+  return shift + 8.f - rs.mc[rt];
 }
 
 // Pairwise sum of 16 values.
@@ -394,8 +438,8 @@ __device__ __forceinline__ void fin_bf16(const uint4* st, Scores<RT>& S, RowStat
     }
     // KIND 1: the PV weight pv_scale (> 0) enters the exponent as log2
     // pv_scale, and the row sum divides it out once.
-    const float bias = softmax_rescale<2, false>(S.v[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off,
-                                                 kTauBf16, 0.f) +
+    const float bias = softmax_rescale<2>(S.v[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, off,
+                                          kTauBf16) +
                        (KIND == 1 ? lg_pv : 0.f);
     float pv[2][16];
 #pragma unroll
@@ -546,8 +590,7 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
             s[rt][u][4 * i + j] = drop ? -INFINITY : s[rt][u][4 * i + j];
           }
     }
-    const float bias = softmax_rescale<2, true>(s[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f, 8.0f,
-                                                kTauFp8, kHeadFp8);
+    const float bias = softmax_lift_fp8<RT>(s[rt], rs, rt, cs, KIND == 1 ? 7.0f : 0.0f);
     int pk[8];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
@@ -558,11 +601,16 @@ __device__ __forceinline__ void fin_fp8(const uint4* st, Scores<RT>& S, RowState
                                     fast_exp2(fmaf(s[rt][u][4 * q + 2], cs, bias)),
                                     fast_exp2(fmaf(s[rt][u][4 * q + 3], cs, bias)));
     const i32x8_t pb = {pk[0], pk[1], pk[2], pk[3], pk[4], pk[5], pk[6], pk[7]};
+    // P~ lifted by 2^k (E8M0 B scale of the lane's query, 127 + k; A unscaled,
+    // 127). The row-sum MFMA stays unscaled: in its 16x16 shape a B column
+    // holds two queries, and its B scale is one per column
+    const int sb = 127 + rs.k[rt];
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
       rs.o[rt][dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(va[dt], pb, rs.o[rt][dt], 0, 0, 0,
-                                                                     0, 0, 0);
-    rs.ls[rt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(sel, pb, rs.ls[rt], 0, 0, 0, 0, 0, 0);
+                                                                     127, 0, sb);
+    rs.ls[rt] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(sel, pb, f32x4_t{}, 0, 0, 0, 0, 0,
+                                                                 0);
   }
 }
 
@@ -670,6 +718,9 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
       rs.ls[rt] = f32x4_t{};
       rs.m[rt] = kNoRef;
       rs.l[rt] = 0.f;
+      rs.k[rt] = 0;
+      rs.mc[rt] = kNoRef;
+      rs.p2k[rt] = 1.f;
     }
     float qsc = FP8 ? p.q_scale[hq] : 1.f;
     float vsc = FP8 ? ld_uniform(p.v_scale, h) : 1.f;
@@ -901,7 +952,8 @@ __global__ __launch_bounds__(64 * W, wgs_per_cu(W, FP8)) void attend_kernel(Prob
     // fp8: the row sums of P~ from the matrix cores join the denominator
     if constexpr (FP8) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) rs.l[rt] += half == 0 ? rs.ls[rt][0] : 0.f;
+      for (int rt = 0; rt < RT; ++rt)   // both lane halves hold the row's sums; keep one
+        rs.l[rt] = half == 0 ? fmaf(rs.ls[rt][0], rs.p2k[rt], rs.l[rt]) : 0.f;
     }
 
     // epilogue: O = c_v O^T / l, LSE = (m + log2 l - off) ln 2; with KV
