@@ -200,14 +200,19 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
 
   // This thread's 16 bytes of Q tile t (bf16: row tid/16, chunk tid%16;
   // fp8: threads < 256, row tid/8, 16 codes tid%8), zero past the block.
+  // Packed row t*32 + r is position t*(32/G) + r/G, head h*G + r%G (G
+  // divides 32), so the byte offset is a per-thread constant plus t times
+  // the tile stride. fp8 threads past the 256 that cover a tile start past
+  // the buffer (2^30, so that no tile's offset wraps): they read zero.
+  const int qr = FP8 ? tid >> 3 : tid >> 4;
+  const int qoff0 = !FP8 || tid < 256
+                        ? ((qr / G) * p.hq + h * G + qr % G) * (kHeadDim * esz) + (FP8 ? tid & 7 : tid & 15) * 16
+                        : 0x40000000;
+  const int qtstride = (32 / G) * p.hq * kHeadDim * esz;
   auto qload = [&](int t) -> uint4 {
-    const int r = FP8 ? tid >> 3 : tid >> 4;
-    const int pr = t * 32 + r;
-    const int off = ((pr / G) * p.hq + h * G + pr % G) * (kHeadDim * esz) + (FP8 ? tid & 7 : tid & 15) * 16;
-    // tiles past the item's last and fp8 threads past the 256 that cover a
-    // tile fetch nothing (an offset past the buffer reads zero)
-    const bool ok = t < thi && (!FP8 || tid < 256);
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(qrs, ok ? off : 0x7ffffff0, 0, 0);
+    // tiles past the item's last fetch nothing (an offset past the buffer reads zero)
+    const int off = t < thi ? qoff0 + t * qtstride : 0x7ffffff0;
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(qrs, off, 0, 0);
     return make_uint4(v[0], v[1], v[2], v[3]);
   };
   // Store it into LDS buffer qb (fp8 codes widened to bf16, exact). Rows are
