@@ -57,13 +57,15 @@ __device__ __forceinline__ uint16_t f64_to_bf16(double x) {
 typedef __attribute__((ext_vector_type(2))) float f32x2_t;
 
 // Four OCP e4m3fn codes (the bytes of w, lowest first) -> two packed bf16
-// pairs. Exact: v_cvt_pk_f32_fp8 decodes two codes to fp32 (subnormals
-// included) and every e4m3 value is a bf16 value, so the bf16 packing does
-// not round.
+// pairs, two codes per v_cvt_scalef32_pk_bf16_fp8 (scale 1). Exact: every
+// e4m3 value, subnormals included, is a bf16 value, and the instruction
+// returns it for every non-NaN code (checked against an exact decode of all
+// 256 codes).
 __device__ __forceinline__ uint2 e4m3x4_to_bf16(uint32_t w) {
-  const f32x2_t lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
-  const f32x2_t hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);
-  return make_uint2(pack_bf16x2(lo.x, lo.y), pack_bf16x2(hi.x, hi.y));
+  typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
+  const bf16x2v_t lo = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, false);
+  const bf16x2v_t hi = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, true);
+  return make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
 }
 
 // ---------------------------------------------------------------------------
