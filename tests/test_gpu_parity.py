@@ -91,13 +91,13 @@ def test_prefill_parity(name, alpha):
 
 
 @pytest.mark.parametrize("name", ["g2_perm_p16", "g4_fp8", "g8_fp8_perm"])
-@pytest.mark.parametrize("scale", [1.0, 4.0])
+@pytest.mark.parametrize("scale", [1.0, 4.0, 16.0])
 def test_prefill_parity_large_logits(name, scale):
-    """A softmax scale of 1 and 4 instead of 1/sqrt(d) (Eq. (1) with the scale
-    of R2): logits spread over hundreds of binary places, so the online
-    softmax's reference moves far along the walk (for fp8 past the largest
-    power-of-two lift, which rebases the accumulators) and the selection sees
-    sharply peaked energies."""
+    """Softmax scales of 1, 4 and 16 instead of 1/sqrt(d) (Eq. (1) with the
+    scale of R2): logits spread over hundreds of binary places, so the online
+    softmax's reference moves far along the walk (for fp8 at scale 16 by more
+    than the largest power-of-two lift, 2^64, in one step, which rebases the
+    accumulators) and the selection sees sharply peaked energies."""
     wl = _wl(name)
     sp = wl.spec
     alpha = 0.99
