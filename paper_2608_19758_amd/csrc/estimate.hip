@@ -264,10 +264,9 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
     auto tile = [&](const uint4* qb, int t, auto partial) {
       constexpr bool kPartial = decltype(partial)::value;
 
-      bf16x8_t qa[8];
-#pragma unroll
-      for (int ds = 0; ds < 8; ++ds)
-        qa[ds] = __builtin_bit_cast(bf16x8_t, qb[l32 * kQRow + 2 * ds + half]);
+      // Q operand ds of this lane, read from LDS where it is used (two reads
+      // in flight ahead of the MFMAs, not the tile's eight held in registers)
+      auto qa = [&](int ds) { return __builtin_bit_cast(bf16x8_t, qb[l32 * kQRow + 2 * ds + half]); };
       const int rbase = t * 32 + 4 * half;   // first of this lane's 16 rows
 
       // Scores of chunk c (the other wave of the SIMD runs its vector work
@@ -276,7 +275,7 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
         f32x16_t acc = {};
 #pragma unroll
         for (int ds = 0; ds < 8; ++ds)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[ds], kf[c][ds], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa(ds), kf[c][ds], acc, 0, 0, 0);
         return acc;
       };
       // Fold one chunk's scores into its running (m, E): rows of head
@@ -287,11 +286,12 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
       // whose sum exceeds 2^64 moves m to its maximum and is summed again.
       auto fold = [&](int c, f32x16_t& acc) {
         if constexpr (kPartial) {
+          const int rem = nrows - rbase;   // this lane's rows 8i + j < rem lie in the block
 #pragma unroll
           for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-              acc[4 * i + j] = rbase + 8 * i + j < nrows ? acc[4 * i + j] : -INFINITY;
+              acc[4 * i + j] = 8 * i + j < rem ? acc[4 * i + j] : -INFINITY;
         }
         auto sum_at = [&](float nb) -> float {
           float s4[4];                                  // four independent partial sums
