@@ -259,23 +259,25 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
     // per pair; the global loads of the next pair are in flight while a pair
     // is scored. Only the last tile can be partial: it runs as a separate
     // instance of the tile body, so the row validity tests stay out of the
-    // full tiles.
+    // full tiles. With one chunk per wave a pair of full tiles is scored
+    // together, the second tile's MFMAs issued ahead of the first's fold.
     uint4 qa_next = qload(tlo), qa_next2 = qload(tlo + 1);
-    auto tile = [&](const uint4* qb, int t, auto partial) {
+    auto tile = [&](const uint4* qb, int t, auto partial, auto paired) {
       constexpr bool kPartial = decltype(partial)::value;
+      constexpr bool kPair = decltype(paired)::value;   // tiles t and t+1, both full, one chunk
 
       // Q operand ds of this lane, read from LDS where it is used (two reads
       // in flight ahead of the MFMAs, not the tile's eight held in registers)
-      auto qa = [&](int ds) { return __builtin_bit_cast(bf16x8_t, qb[l32 * kQRow + 2 * ds + half]); };
+      auto qa = [&](const uint4* q, int ds) { return __builtin_bit_cast(bf16x8_t, q[l32 * kQRow + 2 * ds + half]); };
       const int rbase = t * 32 + 4 * half;   // first of this lane's 16 rows
 
       // Scores of chunk c (the other wave of the SIMD runs its vector work
       // while these MFMAs execute).
-      auto score = [&](int c) -> f32x16_t {
+      auto score = [&](int c, const uint4* q) -> f32x16_t {
         f32x16_t acc = {};
 #pragma unroll
         for (int ds = 0; ds < 8; ++ds)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa(ds), kf[c][ds], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa(q, ds), kf[c][ds], acc, 0, 0, 0);
         return acc;
       };
       // Fold one chunk's scores into its running (m, E): rows of head
@@ -324,11 +326,17 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
       // last one score zero keys and are dropped at the end
       auto run = [&](auto nc) {
         constexpr int NC = decltype(nc)::value;
-        f32x16_t acc = score(0);
+        if constexpr (kPair) {   // the second tile's MFMAs issued before the first tile's fold
+          f32x16_t a0 = score(0, qb), a1 = score(0, qb + 32 * kQRow);
+          fold(0, a0);
+          fold(0, a1);
+          return;
+        }
+        f32x16_t acc = score(0, qb);
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
           f32x16_t nxt;
-          if (c + 1 < NC) nxt = score(c + 1);
+          if (c + 1 < NC) nxt = score(c + 1, qb);
           fold(c, acc);
           if (c + 1 < NC) acc = nxt;
         }
@@ -349,11 +357,15 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
       __syncthreads();   // tiles t0, t0+1 visible; every wave is done with the pair before
       qa_next = qload(t0 + 2);
       qa_next2 = qload(t0 + 3);
-      for (int k = 0; k < 2 && t0 + k < thi; ++k) {
-        if (t0 + k < nfull)
-          tile(buf + k * 32 * kQRow, t0 + k, std::false_type{});
-        else
-          tile(buf + k * 32 * kQRow, t0 + k, std::true_type{});
+      if (CPW == 1 && t0 + 1 < nfull && t0 + 1 < thi) {
+        tile(buf, t0, std::false_type{}, std::true_type{});
+      } else {
+        for (int k = 0; k < 2 && t0 + k < thi; ++k) {
+          if (t0 + k < nfull)
+            tile(buf + k * 32 * kQRow, t0 + k, std::false_type{}, std::false_type{});
+          else
+            tile(buf + k * 32 * kQRow, t0 + k, std::true_type{}, std::false_type{});
+        }
       }
     }
 
