@@ -2,7 +2,8 @@
 // (Sec. 3.1 Eq. (1)-(2), Eq. fused_score, Eq. select; the scoring, thresholding
 // and compaction of Algorithm 1).
 //
-// A persistent grid (one 8-wave workgroup per compute unit) deals the units
+// A persistent grid (one 8-wave workgroup per compute unit, two for the
+// one-chunk variant below) deals the units
 // (sequence b, KV head h, query block I) round-robin, heaviest (largest I)
 // first. The query rows of block I are the g*B packed rows of Eq. packgqa
 // (position I*B + r/g, head h*g + r%g). They stream through LDS in pairs of
