@@ -505,11 +505,11 @@ hipError_t launch_est_dt(const Problem& p, const Pooled& pooled, uint8_t* mask, 
     parts.n = std::max(1, n);
   }
   // One chunk per wave (8 x 32 key blocks per pass, two workgroups per CU)
-  // up to 512 key blocks, and up to 1024 when a unit holds at most 512
-  // packed rows (g <= 4): there the latency hidden by the second workgroup
-  // outweighs the Q tiles streamed again for every pass (measured at 128K:
-  // g = 4 0.83 -> 0.79 ms, g = 8 1.43 -> 1.46 ms).
-  const bool small = p.nbk <= 2 * kWaves * 32 || (p.g <= 4 && p.nbk <= 4 * kWaves * 32);
+  // up to 1024 key blocks: the latency hidden by the second workgroup
+  // outweighs the Q tiles streamed again for every pass (measured at 128K,
+  // against four chunks per wave: g = 4 0.83 -> 0.79 ms, g = 8 1.40 -> 1.36
+  // ms fp8 and 1.53 -> 1.43 ms bf16).
+  const bool small = p.nbk <= 4 * kWaves * 32;
   const unsigned grid = (unsigned)std::min<int64_t>(units * parts.n, (int64_t)cus * (small ? 2 : 1));
   const size_t smem = (size_t)p.nbk * sizeof(float);
   auto go = [&](auto kern) { kern<<<grid, kThreads, smem, s>>>(p, pooled, mask, kl, parts); };
