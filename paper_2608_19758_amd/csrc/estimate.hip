@@ -122,9 +122,14 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
 
   // Persistent workgroups, items dealt round-robin in order of decreasing
   // query block: the cost of an item is proportional to (I + 1), so every
-  // workgroup gets an almost equal share.
+  // workgroup gets an almost equal share. Even workgroups take their items
+  // heaviest first and odd ones lightest first (the same items, reversed),
+  // so that the two workgroups sharing a CU are rarely both on units whose
+  // few key-block chunks leave most of their waves idle.
+  const int nmine = (nitems - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
 #pragma unroll 1
-  for (int item = blockIdx.x; item < nitems; item += gridDim.x) {
+  for (int jj = 0; jj < nmine; ++jj) {
+  const int item = (int)blockIdx.x + ((blockIdx.x & 1) ? nmine - 1 - jj : jj) * (int)gridDim.x;
   // Opaque copies of the thread index and of the argument block (the first
   // kernel argument, at offset 0 of the argument segment): values derived
   // from them are recomputed per item instead of living across the loop.
