@@ -293,6 +293,10 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
       // finite, so m need not be the exact running maximum); only a tile
       // whose sum exceeds 2^64 moves m to its maximum and is summed again.
       auto fold = [&](int c, f32x16_t& acc) {
+        // raised wave priority while folding: the SIMD's arbiter then favours
+        // the vector work of a folding wave over the issue of other waves,
+        // whose MFMA chains keep the matrix core busy meanwhile
+        __builtin_amdgcn_s_setprio(1);
         if constexpr (kPartial) {
           const int rem = nrows - rbase;   // this lane's rows 8i + j < rem lie in the block
 #pragma unroll
@@ -325,6 +329,7 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
           e = mn == -INFINITY ? 0.f : sum_at(-mn);   // no valid row yet: every term is 0
         }
         E[c] += e;
+        __builtin_amdgcn_s_setprio(0);
       };
       // the wave's chunks 0 .. NC-1 that hold visible blocks (NC a compile-time
       // count, so the scores of chunk c+1 are issued to the matrix cores
