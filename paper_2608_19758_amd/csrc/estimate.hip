@@ -363,8 +363,10 @@ __global__ __launch_bounds__(kThreads, CPW == 1 ? 4 : 2) void estimate_kernel(Pr
     const int nfull = nrows >> 5;
     for (int t0 = tlo; t0 < thi; t0 += 2) {
       uint4* buf = qt[((t0 - tlo) >> 1) & 1];
+      __builtin_amdgcn_s_setprio(1);   // the staging waves hold up the barrier below
       qstore(buf, qa_next);
       qstore(buf + 32 * kQRow, qa_next2);
+      __builtin_amdgcn_s_setprio(0);
       __syncthreads();   // tiles t0, t0+1 visible; every wave is done with the pair before
       qa_next = qload(t0 + 2);
       qa_next2 = qload(t0 + 3);
